@@ -1,0 +1,361 @@
+"""Pins for the CPU oracle: what the paper and mathematics fix, independent of it.
+
+Each ``check_*`` takes the oracle module (or a copy with a planted mistake)
+and raises AssertionError when the oracle disagrees with:
+
+* closed forms and exact rational arithmetic (``fractions.Fraction``),
+* brute force over all index subsets of tiny inputs (the minimax theorem of
+  Appendix E: TopK minimises the residual activation energy),
+* special cases that reduce to something known (identity weights, unit-
+  vector keys, constant heads),
+* the error identity and the bounds of Sec. 3.5 / Appendix E,
+* hand-worked fixtures under ``tests/golden``.
+
+These checks never call the HIP library.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+from itertools import combinations
+import math
+import os
+
+import numpy as np
+
+import workloads as wl
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden_lines(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                yield line.split()
+
+
+def exact_dot(a, b) -> float:
+    """Correctly rounded dot product of two float64 vectors of bf16/fp32 values.
+
+    Each product of two such values is exact in float64 (<= 48 significant
+    bits), so fsum of the products is the exact dot product, rounded once.
+    """
+    return math.fsum(float(x) * float(y) for x, y in zip(a, b))
+
+
+def exact_matmul(A, B) -> np.ndarray:
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    out = np.empty((A.shape[0], B.shape[1]))
+    for i in range(A.shape[0]):
+        for n in range(B.shape[1]):
+            out[i, n] = exact_dot(A[i, :], B[:, n])
+    return out
+
+
+def _bf16(seed, shape, **kw):
+    return wl.decode(wl.random_case(seed, shape, "bf16", **kw), "bf16").astype(np.float64)
+
+
+def _ints(seed, shape, lo, hi):
+    return wl.decode(wl.integer_case(seed, shape, lo, hi, "f32"), "f32").astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# k = ceil(rho * d)  (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def check_retained_count(o):
+    for r_s, K_s, k_s in _golden_lines("retained_count.txt"):
+        got = o.retained_count(float(r_s), int(K_s))
+        assert got == int(k_s), (r_s, K_s, got, k_s)
+    # ceil of the exact decimal the caller wrote, by rational arithmetic
+    for K in (1, 3, 7, 100, 128, 512, 2048, 4096, 8192, 14336, 28672):
+        for p in range(1, 101):
+            s = f"{p / 100:.2f}"
+            want = max(1, math.ceil(Fraction(s) * K))
+            got = o.retained_count(float(s), K)
+            assert got == want, (s, K, got, want)
+    for bad in (0.0, -0.25, 1.0 + 1e-12, 2.0, float("nan"), float("inf"), -float("inf")):
+        try:
+            o.retained_count(bad, 128)
+        except ValueError:
+            continue
+        raise AssertionError(f"retained_count accepted r={bad}")
+
+
+# ---------------------------------------------------------------------------
+# e_j = ||A[:, j]||^2  (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def check_energies(o):
+    rows = list(_golden_lines("energies_small.txt"))
+    A = np.array([[float(v) for v in r[1:]] for r in rows if r[0] == "A"])
+    e_want = np.array([float(v) for v in next(r for r in rows if r[0] == "e")[1:]])
+    e = o.column_energies(A)
+    assert e.dtype == np.float64 and e.shape == (A.shape[1],)
+    assert np.array_equal(e, e_want), (e, e_want)
+    # exact rational sum of squares, rounded once, for bf16 and fp32 data
+    for seed, shape, dt in ((1, (37, 11), "bf16"), (2, (5, 3), "f32"), (3, (64, 7), "bf16")):
+        X = wl.decode(wl.random_case(seed, shape, dt, n_outlier=2), dt).astype(np.float64)
+        want = np.array([float(sum(Fraction(float(x)) ** 2 for x in X[:, j]))
+                         for j in range(shape[1])])
+        got = o.column_energies(X)
+        assert np.array_equal(got, want), (seed, got - want)
+        # Frobenius identity: sum_j e_j = ||A||_F^2
+        fro = float(np.linalg.norm(X)) ** 2
+        assert abs(math.fsum(got) - fro) <= 1e-12 * fro
+
+
+# ---------------------------------------------------------------------------
+# TopK (Sec. 3.2) vs brute force over subsets (minimax theorem, App. E)
+# ---------------------------------------------------------------------------
+
+def brute_force_topk(e_exact, k):
+    """Among all size-k subsets, the one with minimum residual energy;
+    among those, the lexicographically smallest (ties -> lower indices)."""
+    d = len(e_exact)
+    best, best_res = None, None
+    for S in combinations(range(d), k):          # lexicographic order
+        s = set(S)
+        res = sum(e_exact[j] for j in range(d) if j not in s)
+        if best is None or res < best_res:
+            best, best_res = S, res
+    return list(best)
+
+
+def check_selection(o):
+    cases = []
+    for seed in range(6):
+        cases.append(_ints(10 + seed, (4, 9), -3, 3))       # many exact ties
+    for seed in range(3):
+        cases.append(_ints(20 + seed, (6, 10), -1, 1))      # heavy ties
+    cases.append(np.zeros((3, 6)))                          # all-tied zeros
+    for A in cases:
+        d = A.shape[1]
+        # integer data: exact energies without the oracle
+        e_exact = [sum(Fraction(int(v)) ** 2 for v in A[:, j]) for j in range(d)]
+        e = o.column_energies(A)
+        assert [Fraction(float(v)) for v in e] == e_exact
+        for k in range(1, d + 1):
+            idx = o.topk_indices(e, k)
+            got = [int(v) for v in idx]
+            assert got == sorted(set(got)) and len(got) == k, got
+            assert got == brute_force_topk(e_exact, k), (A, k, got)
+    # real-valued bf16 data, nestedness and monotone residual (Sec. 3.5)
+    for seed in range(4):
+        X = _bf16(30 + seed, (16, 12), n_outlier=2)
+        e = o.column_energies(X)
+        e_exact = [sum(Fraction(float(x)) ** 2 for x in X[:, j]) for j in range(12)]
+        prev_set, prev_res = set(), None
+        for k in range(1, 13):
+            got = [int(v) for v in o.topk_indices(e, k)]
+            assert got == brute_force_topk(e_exact, k)
+            assert prev_set <= set(got)
+            res = sum(e_exact[j] for j in range(12) if j not in set(got))
+            assert prev_res is None or res <= prev_res
+            prev_set, prev_res = set(got), res
+    # non-finite energies (reading: NaN > inf > finite; NaNs tie)
+    rows = list(_golden_lines("nan_ranking.txt"))
+    e = np.array([float(v) for v in next(r for r in rows if r[0] == "e")[1:]])
+    for r in rows:
+        if r[0] == "I":
+            k, want = int(r[1]), [int(v) for v in r[2:]]
+            assert [int(v) for v in o.topk_indices(e, k)] == want, (k, want)
+    # the hand-worked fixture through rmm()
+    rowsA = list(_golden_lines("energies_small.txt"))
+    A = np.array([[float(v) for v in r[1:]] for r in rowsA if r[0] == "A"])
+    for r in rowsA:
+        if r[0] == "I":
+            _, idx, _ = o.rmm(A, np.eye(4), float(r[1]))
+            assert [int(v) for v in idx] == [int(v) for v in r[2:]], r
+
+
+# ---------------------------------------------------------------------------
+# Reduced product (Sec. 3.2 definition; Sec. 3.5 rank-one decomposition)
+# ---------------------------------------------------------------------------
+
+def check_product(o):
+    # identity weights: RMM(A, I_d) = A with the discarded columns zeroed
+    A = _bf16(40, (13, 9))
+    idx = np.array([0, 2, 3, 7])
+    Y = o.reduced_matmul(A, np.eye(9), idx)
+    Z = np.zeros_like(A)
+    Z[:, idx] = A[:, idx]
+    assert Y.shape == (13, 9) and np.array_equal(Y, Z)
+    # cyclic-shift weights (square, not symmetric): row j of B is e_{(j+1) mod d},
+    # so column (j+1) mod d of the output is A[:, j] for j in I, else zero
+    P = np.zeros((9, 9))
+    for j in range(9):
+        P[j, (j + 1) % 9] = 1.0
+    Y = o.reduced_matmul(A, P, idx)
+    Z = np.zeros_like(A)
+    for j in idx:
+        Z[:, (j + 1) % 9] = A[:, j]
+    assert np.array_equal(Y, Z)
+    # non-square operands: shape and values against exact dots of the
+    # explicitly listed retained rank-one terms
+    A = _bf16(41, (7, 11), n_outlier=2)
+    B = _bf16(42, (11, 5))
+    for idx in (np.array([1, 4, 5, 10]), np.arange(11), np.array([6])):
+        Y = o.reduced_matmul(A, B, idx)
+        assert Y.shape == (7, 5)
+        for i in range(7):
+            for n in range(5):
+                want = math.fsum(A[i, j] * B[j, n] for j in idx)
+                assert abs(Y[i, n] - want) <= 1e-14 * (1 + np.abs(A[i, :]) @ np.abs(B[:, n]))
+    # r = 1 is the full product (ceil(1 * d) = d)
+    full = exact_matmul(A, B)
+    Y1, idx1, _ = o.rmm(A, B, 1.0)
+    assert [int(v) for v in idx1] == list(range(11))
+    assert np.allclose(Y1, full, rtol=0, atol=1e-13 * np.abs(full).max())
+    # complement identity: RMM(I) + RMM(Ibar) = AB (Sec. 3.5)
+    for r in (0.25, 0.5, 0.75):
+        Yr, idx, _ = o.rmm(A, B, r)
+        comp = np.array(sorted(set(range(11)) - set(int(v) for v in idx)))
+        Yc = o.reduced_matmul(A, B, comp)
+        assert np.allclose(Yr + Yc, full, rtol=0, atol=1e-13 * np.abs(full).max())
+    # rmm(): index set is TopK of the column energies, output the product
+    X = _bf16(43, (20, 16), n_outlier=3)
+    W = _bf16(44, (16, 6))
+    Y, idx, e = o.rmm(X, W, 0.5)
+    e_exact = [float(sum(Fraction(float(x)) ** 2 for x in X[:, j])) for j in range(16)]
+    assert np.array_equal(e, np.array(e_exact))
+    assert [int(v) for v in idx] == brute_force_topk([Fraction(v) for v in e_exact], 8)
+    # batched: each sequence selects on its own rows (Appendix A)
+    Xb = np.stack([_bf16(45, (6, 10), n_outlier=2), _bf16(46, (6, 10), n_outlier=3)])
+    Wb = _bf16(47, (10, 4))
+    Yb, idxb, eb = o.rmm_batched(Xb, Wb, 0.5)
+    for b in range(2):
+        Ys, ids, es = o.rmm(Xb[b], Wb, 0.5)
+        assert np.array_equal(Yb[b], Ys) and np.array_equal(idxb[b], ids)
+
+
+def check_bounds(o):
+    """Error identity and bounds of Sec. 3.5 / Appendix E hold for the
+    oracle's product; the oracle's bound helpers agree with their definition."""
+    for seed in range(3):
+        A = _bf16(50 + seed, (24, 32), n_outlier=4)
+        B = _bf16(60 + seed, (32, 10), std=0.02)
+        full = exact_matmul(A, B)
+        nA, nB = float(np.linalg.norm(A)), float(np.linalg.norm(B))
+        for r in (0.25, 0.5, 0.75, 1.0):
+            Y, idx, e = o.rmm(A, B, r)
+            comp = sorted(set(range(32)) - set(int(v) for v in idx))
+            err = float(np.linalg.norm(full - Y))
+            b1 = math.fsum(float(np.linalg.norm(A[:, j]) * np.linalg.norm(B[j, :])) for j in comp)
+            b2 = float(np.linalg.norm(A[:, comp]) * np.linalg.norm(B[comp, :])) if comp else 0.0
+            epsA = float(np.linalg.norm(A[:, comp]) ** 2) / nA ** 2 if comp else 0.0
+            epsB = float(np.linalg.norm(B[comp, :]) ** 2) / nB ** 2 if comp else 0.0
+            slack = 1e-12 * nA * nB
+            assert err <= b1 + slack
+            assert b1 <= b2 * (1 + 1e-12) + slack
+            assert err / (nA * nB) <= math.sqrt(epsA * epsB) + 1e-12
+            assert abs(o.rank_one_bound(A, B, idx) - b1) <= 1e-12 * (1 + b1)
+            assert abs(o.factorized_bound(A, B, idx) - b2) <= 1e-12 * (1 + b2)
+            assert abs(o.normalized_bound(A, B, idx) - math.sqrt(epsA * epsB)) <= 1e-12
+            assert abs(o.residual_energy(e, idx) - epsA * nA ** 2) <= 1e-10 * nA ** 2
+            assert abs(o.retained_energy_fraction(e, idx) - (1 - epsA)) <= 1e-12
+            # minimax optimality: any other subset of the same size keeps less energy
+            rng = np.random.default_rng(seed)
+            for _ in range(20):
+                other = rng.choice(32, size=len(idx), replace=False)
+                assert o.residual_energy(e, idx) <= o.residual_energy(e, other) + 1e-12
+
+
+def check_worked_example(o):
+    """Appendix E: top 70% of dims hold 95% of the energy -> eps_A(0.7) = 0.05."""
+    (rho_s, frac_s, eps_s), = list(_golden_lines("worked_example_appE.txt"))
+    rho, frac, eps = float(rho_s), float(frac_s), float(eps_s)
+    d, n = 20, 8
+    k = 14
+    assert math.ceil(Fraction(rho_s) * d) == k
+    # 14 strong columns share `frac` of the energy, 6 weak ones the rest
+    rng = np.random.default_rng(7)
+    A = np.zeros((n, d))
+    strong = rng.choice(d, size=k, replace=False)
+    weak = [j for j in range(d) if j not in set(strong)]
+    for j in strong:
+        v = rng.standard_normal(n)
+        A[:, j] = v / np.linalg.norm(v) * math.sqrt(frac / k)
+    for j in weak:
+        v = rng.standard_normal(n)
+        A[:, j] = v / np.linalg.norm(v) * math.sqrt((1 - frac) / (d - k))
+    B = rng.standard_normal((d, 9))
+    Y, idx, e = o.rmm(A, B, rho)
+    assert sorted(int(v) for v in idx) == sorted(int(v) for v in strong)
+    assert abs(o.discarded_energy_ratio(A, idx, 1) - eps) <= 1e-12
+    assert abs(o.retained_energy_fraction(e, idx) - frac) <= 1e-12
+    full = A @ B
+    epsB = o.discarded_energy_ratio(B, idx, 0)
+    rel = np.linalg.norm(full - Y) / (np.linalg.norm(A) * np.linalg.norm(B))
+    assert rel <= math.sqrt(eps * epsB) + 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Reduced QK^T (Sec. 3.3)
+# ---------------------------------------------------------------------------
+
+def check_qk(o):
+    # GQA map: consecutive query heads share a kv head
+    assert [o.gqa_kv_head(h, 8, 2) for h in range(8)] == [0, 0, 0, 0, 1, 1, 1, 1]
+    assert [o.gqa_kv_head(h, 4, 4) for h in range(4)] == [0, 1, 2, 3]
+    # constant heads: S[h,i,t] = k * (g(h) + 1) / sqrt(D)
+    H, Hkv, L, D, k = 4, 2, 3, 8, 5
+    Q = np.ones((H, L, D))
+    K = np.stack([np.full((L, D), g + 1.0) for g in range(Hkv)])
+    idx = np.stack([np.arange(k)] * H)
+    S = o.reduced_qk(Q, K, idx, causal=False)
+    for h in range(H):
+        assert np.allclose(S[h], k * (h // 2 + 1) / math.sqrt(D), rtol=1e-15, atol=0)
+    # unit-vector keys: S[h,i,t] = Q[h,i,t]/sqrt(D) if t in I_h else 0
+    H, L, D = 2, 4, 8
+    Q = _bf16(70, (H, L, D))
+    K = np.stack([np.eye(D)] * 1)                      # Hkv = 1, Lk = D
+    idx = np.array([[0, 3, 5], [1, 2, 7]])
+    S = o.reduced_qk(Q, K, idx, causal=False)
+    for h in range(H):
+        want = np.zeros((L, D))
+        want[:, idx[h]] = Q[h][:, idx[h]] / math.sqrt(D)
+        assert np.allclose(S[h], want, rtol=1e-15, atol=0)
+    # causal mask, Lq=3, Lk=5, bottom-right aligned (hand table)
+    mask = np.array([[int(v) for v in r] for r in _golden_lines("causal_mask_3x5.txt")],
+                    dtype=bool)
+    Q = _bf16(71, (2, 3, 16))
+    Kt = _bf16(72, (1, 5, 16))
+    idx = np.stack([np.arange(0, 16, 2)] * 2)
+    S = o.reduced_qk(Q, Kt, idx, causal=True)
+    for h in range(2):
+        assert np.array_equal(np.isneginf(S[h]), mask)
+        assert np.all(np.isfinite(S[h][~mask]))
+    # r = 1 is the dense scaled product (exact dots)
+    Q = _bf16(73, (2, 5, 16))
+    Kt = _bf16(74, (1, 6, 16))
+    S, idx, e = o.rmm_qk(Q, Kt, 1.0, causal=False)
+    for h in range(2):
+        want = exact_matmul(Q[h], Kt[0].T) / math.sqrt(16)
+        assert np.allclose(S[h], want, rtol=0, atol=1e-14 * (1 + np.abs(want).max()))
+    # selection is per query head on Q (not on K): integer data, exact energies
+    Q = _ints(75, (3, 6, 8), -3, 3)
+    Kt = _bf16(76, (1, 7, 8))
+    S, idx, e = o.rmm_qk(Q, Kt, 0.5, causal=True)
+    for h in range(3):
+        e_exact = [sum(Fraction(int(v)) ** 2 for v in Q[h][:, j]) for j in range(8)]
+        assert [int(v) for v in idx[h]] == brute_force_topk(e_exact, 4)
+        # each head's scores use only its own index set
+        want = exact_matmul(Q[h][:, idx[h]], Kt[0][:, idx[h]].T) / math.sqrt(8)
+        m = np.triu(np.ones((6, 7), dtype=bool), 2)      # t > i + 1
+        assert np.array_equal(np.isneginf(S[h]), m)
+        assert np.allclose(S[h][~m], want[~m], rtol=0, atol=1e-14 * (1 + np.abs(want).max()))
+
+
+def check_margin(o):
+    assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
+    assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
+    assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 3) == math.inf
+    assert o.selection_margin(np.array([1.0, 3.0, 2.0]), 2) == 0.5
+
+
+ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
+              check_bounds, check_worked_example, check_qk, check_margin)

@@ -1,0 +1,185 @@
+"""The pins are strong enough: each planted mistake in the oracle fails one.
+
+Mistakes are planted into the oracle module on the CPU (monkeypatch), never
+into the HIP path.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import rmm_oracle as ro
+from tests import pins
+
+_reduced_qk = ro.reduced_qk          # unpatched, for mutants built on it
+
+
+def _k_plain_ceil(r, K):
+    if not (0 < r <= 1):
+        raise ValueError
+    return max(1, math.ceil(r * K))
+
+
+def _k_round(r, K):
+    if not (0 < r <= 1):
+        raise ValueError
+    return max(1, round(r * K))
+
+
+def _k_no_domain(r, K):
+    p = r * K
+    n = round(p) if p == p and abs(p) != math.inf else 1
+    return max(1, min(K, int(n) if abs(p - n) <= 1e-9 * K else math.ceil(p)))
+
+
+def _e_l1(A):
+    A = np.asarray(A, dtype=np.float64)
+    return np.array([math.fsum(np.abs(A[:, j])) for j in range(A.shape[1])])
+
+
+def _e_drop_row(A):
+    A = np.asarray(A, dtype=np.float64)[1:]
+    return np.array([math.fsum(A[:, j] ** 2) for j in range(A.shape[1])])
+
+
+def _e_rows(A):
+    A = np.asarray(A, dtype=np.float64)
+    r = np.array([math.fsum(A[i, :] ** 2) for i in range(A.shape[0])])
+    return np.resize(r, A.shape[1])
+
+
+def _topk_smallest(e, k):
+    order = sorted(range(len(e)), key=lambda j: (float(e[j]), j))
+    return np.array(sorted(order[:k]))
+
+
+def _topk_ties_high(e, k):
+    order = sorted(range(len(e)), key=lambda j: (ro._rank_key(float(e[j]), 0), -j))
+    return np.array(sorted(order[:k]))
+
+
+def _topk_unsorted(e, k):
+    order = sorted(range(len(e)), key=lambda j: ro._rank_key(float(e[j]), j))
+    return np.array(order[:k])
+
+
+def _topk_nan_low(e, k):
+    order = sorted(range(len(e)),
+                   key=lambda j: (1, 0.0, j) if math.isnan(e[j]) else (0, -float(e[j]), j))
+    return np.array(sorted(order[:k]))
+
+
+def _mm_transposed(A, B, idx):
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    if B.shape[0] == B.shape[1]:
+        return A[:, idx] @ B[:, idx].T
+    return A[:, idx] @ B[idx, :]
+
+
+def _mm_off_by_one(A, B, idx):
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    idx = np.asarray(idx)
+    return A[:, idx] @ B[np.minimum(idx + 1, B.shape[0] - 1), :]
+
+
+def _mm_sign(A, B, idx):
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    out = A[:, idx] @ B[idx, :]
+    out[:, -1] *= -1
+    return out
+
+
+def _qk_patch(body):
+    def f(Q, K, idx, causal):
+        Q = np.asarray(Q, dtype=np.float64)
+        K = np.asarray(K, dtype=np.float64)
+        H, Lq, D = Q.shape
+        Hkv, Lk, _ = K.shape
+        S = np.empty((H, Lq, Lk))
+        for h in range(H):
+            S[h] = body(Q, K, np.asarray(idx[h]), h, H, Hkv, D)
+            if causal:
+                i = np.arange(Lq)[:, None]
+                t = np.arange(Lk)[None, :]
+                S[h][t > i + (Lk - Lq)] = -np.inf
+        return S
+    return f
+
+
+_qk_scale_k = _qk_patch(lambda Q, K, I, h, H, Hkv, D:
+                        Q[h][:, I] @ K[h // (H // Hkv)][:, I].T / math.sqrt(len(I)))
+_qk_gqa_mod = _qk_patch(lambda Q, K, I, h, H, Hkv, D:
+                        Q[h][:, I] @ K[h % Hkv][:, I].T / math.sqrt(D))
+_qk_no_scale = _qk_patch(lambda Q, K, I, h, H, Hkv, D:
+                         Q[h][:, I] @ K[h // (H // Hkv)][:, I].T)
+
+
+def _qk_mask_off_by_one(Q, K, idx, causal):
+    S = _reduced_qk(Q, K, idx, False)
+    if causal:
+        Lq, Lk = S.shape[1], S.shape[2]
+        i = np.arange(Lq)[:, None]
+        t = np.arange(Lk)[None, :]
+        for h in range(S.shape[0]):
+            S[h][t >= i + (Lk - Lq)] = -np.inf
+    return S
+
+
+def _qk_mask_top_left(Q, K, idx, causal):
+    S = _reduced_qk(Q, K, idx, False)
+    if causal:
+        Lq, Lk = S.shape[1], S.shape[2]
+        i = np.arange(Lq)[:, None]
+        t = np.arange(Lk)[None, :]
+        for h in range(S.shape[0]):
+            S[h][t > i] = -np.inf
+    return S
+
+
+def _rmm_qk_scores_k(Q, K, r, causal):
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    H, _, D = Q.shape
+    k = ro.retained_count(r, D)
+    e = np.stack([ro.column_energies(K[h * K.shape[0] // H]) for h in range(H)])
+    idx = np.stack([ro.topk_indices(e[h], k) for h in range(H)])
+    return ro.reduced_qk(Q, K, idx, causal), idx, e
+
+
+MUTANTS = {
+    "k_plain_ceil": ("retained_count", _k_plain_ceil),
+    "k_round": ("retained_count", _k_round),
+    "k_no_domain_check": ("retained_count", _k_no_domain),
+    "energy_l1": ("column_energies", _e_l1),
+    "energy_drop_row": ("column_energies", _e_drop_row),
+    "energy_rows": ("column_energies", _e_rows),
+    "topk_smallest": ("topk_indices", _topk_smallest),
+    "topk_ties_high": ("topk_indices", _topk_ties_high),
+    "topk_unsorted": ("topk_indices", _topk_unsorted),
+    "topk_nan_low": ("topk_indices", _topk_nan_low),
+    "matmul_transposed": ("reduced_matmul", _mm_transposed),
+    "matmul_off_by_one": ("reduced_matmul", _mm_off_by_one),
+    "matmul_sign": ("reduced_matmul", _mm_sign),
+    "qk_scale_k": ("reduced_qk", _qk_scale_k),
+    "qk_gqa_modulo": ("reduced_qk", _qk_gqa_mod),
+    "qk_no_scale": ("reduced_qk", _qk_no_scale),
+    "qk_mask_off_by_one": ("reduced_qk", _qk_mask_off_by_one),
+    "qk_mask_top_left": ("reduced_qk", _qk_mask_top_left),
+    "qk_scores_on_k": ("rmm_qk", _rmm_qk_scores_k),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    attr, fn = MUTANTS[name]
+    monkeypatch.setattr(ro, attr, fn)
+    failed = []
+    for check in pins.ALL_CHECKS:
+        try:
+            check(ro)
+        except (AssertionError, ValueError, IndexError, TypeError):
+            failed.append(check.__name__)
+    assert failed, f"no pin caught mutant {name}"
