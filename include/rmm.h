@@ -1,0 +1,193 @@
+/*
+ * librmm -- Reduced Matrix Multiplication (RMM) on AMD Instinct MI355X (gfx950).
+ *
+ * RMM (arXiv 2608.13426, Sec. 3.2) replaces a product Y = A B, A in R^{n x d},
+ * B in R^{d x m}, by A[:, I] B[I, :] where I holds the ceil(rho*d) indices of
+ * the shared axis with the largest activation column norms ||A[:, j]||_2.
+ * Sec. 3.3 applies it to linear / MLP projections (A = X, B = W) and, per
+ * attention head, to Q K^T over the head dimension.
+ *
+ * Conventions shared by every entry point:
+ *
+ *  - All tensor pointers are DEVICE pointers unless stated otherwise.  The
+ *    caller allocates and frees every buffer; the library never allocates
+ *    device memory.  Scratch memory, where needed, is a caller-provided
+ *    workspace sized by rmm_workspace_size().
+ *  - Every call validates its arguments on the host first and returns
+ *    RMM_ERR_INVALID_ARGUMENT / RMM_ERR_UNSUPPORTED / RMM_ERR_WORKSPACE_TOO_SMALL
+ *    without touching the device.  Valid calls enqueue kernels on `stream`
+ *    (NULL = the legacy default stream) and return without synchronising;
+ *    RMM_ERR_HIP reports a failed launch.  Nothing is printed, nothing aborts.
+ *  - Matrices are row-major with a leading dimension (elements between
+ *    consecutive rows).  bf16 tensors hold raw bfloat16 bit patterns.
+ *  - Arithmetic: energies are float64 sums of exact squares; bf16 products
+ *    accumulate in fp32 and are rounded to bf16 (round-to-nearest-even) on
+ *    output; the fp32 path accumulates and outputs fp32.
+ *  - Index sets are int32, strictly ascending, one set per selection unit.
+ *    Selection is deterministic: energy descending, ties to the lower index,
+ *    NaN above +inf above every finite value.  No call uses floating-point
+ *    atomics, so repeated calls give bit-identical results.
+ *  - Calls are reentrant and may run concurrently on different streams with
+ *    distinct output and workspace buffers.
+ */
+#ifndef RMM_H
+#define RMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rmm_status {
+    RMM_OK = 0,
+    RMM_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, r outside (0,1], ... */
+    RMM_ERR_UNSUPPORTED = 2,        /* valid but not implemented (dtype, alignment) */
+    RMM_ERR_WORKSPACE_TOO_SMALL = 3,
+    RMM_ERR_HIP = 4                 /* a HIP launch failed (no device, bad stream) */
+} rmm_status_t;
+
+typedef enum rmm_dtype {
+    RMM_F32 = 0,    /* float32 in, float32 out */
+    RMM_BF16 = 1    /* bfloat16 in, fp32 accumulate, bfloat16 out */
+} rmm_dtype_t;
+
+typedef enum rmm_op {
+    RMM_OP_SCORE = 0,   /* rmm_score   */
+    RMM_OP_SELECT = 1,  /* rmm_select  */
+    RMM_OP_LINEAR = 2   /* rmm_linear  */
+} rmm_op_t;
+
+/*
+ * Number of retained indices k = ceil(r * K)   (Sec. 3.2: |I| = ceil(rho d)).
+ *
+ * r is read as the decimal the caller meant: when r*K lies within 1e-9*K of
+ * an integer that integer is k (so r = 0.07, K = 100 gives 7, not 8).  The
+ * result is clamped to [1, K].  Host-only; returns -1 when r is not in
+ * (0, 1] (or is NaN), when K < 1, or when K > INT32_MAX.
+ */
+int64_t rmm_retained_count(double r, int64_t K);
+
+/*
+ * Bytes of workspace a call needs (0 if none).  Arguments as in the call:
+ *   RMM_OP_SCORE : B, M, K        (k ignored)
+ *   RMM_OP_SELECT: always 0
+ *   RMM_OP_LINEAR: B, M, K, k     (k = rmm_retained_count(r, K))
+ * Returns 0 for non-positive sizes.  Host-only.
+ */
+size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t k);
+
+/*
+ * Column energies   (Sec. 3.2, score s_j = ||A[:, j]||_2; Sec. 3.3 for Q).
+ *
+ *   energy[b*K + j] = sum_{m < M} X[b][m][j]^2          (= s_j^2)
+ *
+ * X        : B selection units, each M rows of K values, row stride ldx
+ *            (ldx >= K), unit stride M*ldx.  For attention scores pass Q
+ *            [batch*H][Lq][D] with B = batch*H, M = Lq, K = ldx = D.
+ * dtype    : RMM_BF16 or RMM_F32.
+ * energy   : float64 [B*K], written.  Squares are exact; the sum is float64
+ *            in a fixed order that depends only on (B, M, K).  NaN/Inf
+ *            inputs propagate into the energies.
+ * workspace: rmm_workspace_size(RMM_OP_SCORE, B, M, K, 0) bytes, 8-byte
+ *            aligned (may be NULL when that size is 0).
+ * Errors   : INVALID_ARGUMENT for null pointers, B/M/K < 1, ldx < K, K >
+ *            INT32_MAX, a misaligned workspace; UNSUPPORTED for B > 65535;
+ *            WORKSPACE_TOO_SMALL.
+ */
+rmm_status_t rmm_score(const void *X, rmm_dtype_t dtype, int64_t B, int64_t M,
+                       int64_t K, int64_t ldx, double *energy,
+                       void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * TopK selection   (Sec. 3.2: I = TopK({s_j}, ceil(rho d))).
+ *
+ * For each unit b, writes the k indices of the largest energy[b*K + j] to
+ * idx[b*k .. b*k + k) in ascending order.  Order: larger energy first; equal
+ * energies (including -0 == +0) go to the lower index; any NaN ranks above
+ * +inf and NaNs tie with each other.  Integer-exact: the result depends
+ * only on the float64 values passed in.
+ *
+ * energy : float64 [B*K] (device).        idx : int32 [B*k] (device), written.
+ * Errors : INVALID_ARGUMENT for null pointers, B < 1, K < 1, k outside [1, K],
+ *          K > INT32_MAX.
+ */
+rmm_status_t rmm_select(const double *energy, int64_t B, int64_t K, int64_t k,
+                        int32_t *idx, hipStream_t stream);
+
+/*
+ * Gathered reduced product   (Sec. 3.2: RMM = A[:, I] B[I, :]; Sec. 3.3
+ * projections Y~ = X[:, I] W[I, :]).
+ *
+ *   Y[b][m][n] = sum_{t < k} X[b][m][idx[b*k + t]] * W[idx[b*k + t]][n]
+ *
+ * X   : [B][M][ldx], ldx >= K.     W : [K][ldw], ldw >= N, shared by all units
+ *       (row j of W is contraction index j; an nn.Linear weight [N][K] must
+ *       be transposed once at load time).
+ * idx : int32 [B*k], each unit's list strictly ascending with values in
+ *       [0, K) -- e.g. from rmm_select, or any caller-chosen list (a static
+ *       or random baseline).  Lists violating this are not detected; values
+ *       outside [0, K) are undefined behaviour.
+ * Y   : [B][M][ldy], ldy >= N, written (bf16 or fp32 per dtype).
+ * The operands are gathered on the fly inside the GEMM; no compacted copy
+ * of X[:, I] or W[I, :] is written to memory.
+ * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, k outside [1, K],
+ *         ld too small, sizes above INT32_MAX.
+ */
+rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx,
+                              rmm_dtype_t dtype, int64_t B, int64_t M, int64_t N,
+                              int64_t K, int64_t k, int64_t ldx, int64_t ldw,
+                              void *Y, int64_t ldy, hipStream_t stream);
+
+/*
+ * Reduced attention scores over head-dim slices   (Sec. 3.3, Attention:
+ * S~ = (1/sqrt(d_h)) Q[:, I] K[:, I]^T, then the optional causal mask M).
+ *
+ *   S[b][h][i][t] = scale * sum_{u < k} Q[b][h][i][I(u)] * Kc[b][g][t][I(u)]
+ *   with I = idx[(b*H + h)*k ..], g = h / (H / Hkv)  (consecutive query heads
+ *   share a kv head), and S = -inf where causal != 0 and t > i + (Lk - Lq).
+ *
+ * Q     : [batch][H][Lq][D].   Kc : [batch][Hkv][Lk][D].
+ * idx   : int32 [batch*H*k], ascending per head, values in [0, D) -- the
+ *         per-head selection on Q (rmm_score + rmm_select with B = batch*H).
+ * scale : multiplies the fp32 accumulator; the paper uses 1/sqrt(D) with
+ *         the full head dimension.
+ * S     : [batch][H][Lq][Lk], written in full (masked entries are -inf).
+ * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, H % Hkv != 0,
+ *         k outside [1, D]; UNSUPPORTED for D > 256.
+ */
+rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx,
+                            rmm_dtype_t dtype, int64_t batch, int64_t H,
+                            int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                            int64_t k, float scale, int causal, void *S,
+                            hipStream_t stream);
+
+/*
+ * Fused RMM projection   (Sec. 3.2 + Sec. 3.3 "MLP and linear projections").
+ *
+ * k = rmm_retained_count(r, K); then rmm_score -> rmm_select ->
+ * rmm_reduced_gemm on `stream`, with no host synchronisation (k depends
+ * only on r and K).  Each of the B units selects from its own M rows.
+ *
+ * idx_out   : int32 [B*k] receiving the index sets, or NULL (kept in the
+ *             workspace).
+ * workspace : rmm_workspace_size(RMM_OP_LINEAR, B, M, K, k) bytes, 256-byte
+ *             aligned.  Other arguments as in rmm_reduced_gemm.
+ * Errors    : as rmm_score / rmm_reduced_gemm, plus INVALID_ARGUMENT when
+ *             r is not in (0, 1].
+ */
+rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtype,
+                        int64_t B, int64_t M, int64_t N, int64_t K, int64_t ldx,
+                        int64_t ldw, void *Y, int64_t ldy, int32_t *idx_out,
+                        void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char *rmm_status_string(rmm_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RMM_H */

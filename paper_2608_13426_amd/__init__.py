@@ -1,0 +1,245 @@
+"""Python binding of librmm (Reduced Matrix Multiplication on MI355X).
+
+Thin ctypes layer over the C-ABI declared in ``include/rmm.h``: it reads
+sizes and strides off torch tensors, passes raw device pointers and the
+current HIP stream, and raises ``RmmError`` on a non-zero status.  Every
+step of the computation runs in librmm's gfx950 kernels; torch only owns the
+device memory and the stream.  Importing this package fails loudly when
+``librmm.so`` has not been built (``python -m paper_2608_13426_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "RmmError", "LIB_PATH", "lib", "RMM_F32", "RMM_BF16", "RMM_OP_SCORE",
+    "RMM_OP_SELECT", "RMM_OP_LINEAR", "rmm_retained_count", "rmm_workspace_size",
+    "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
+    "rmm_reduced_qk", "rmm_linear", "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
+
+RMM_F32, RMM_BF16 = 0, 1
+RMM_OP_SCORE, RMM_OP_SELECT, RMM_OP_LINEAR = 0, 1, 2
+
+_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_SIGS = {
+    "rmm_retained_count": (_i64, [ctypes.c_double, _i64]),
+    "rmm_workspace_size": (ctypes.c_size_t, [ctypes.c_int, _i64, _i64, _i64, _i64]),
+    "rmm_score": (ctypes.c_int, [_p, ctypes.c_int, _i64, _i64, _i64, _i64, _p, _p,
+                                 ctypes.c_size_t, _p]),
+    "rmm_select": (ctypes.c_int, [_p, _i64, _i64, _i64, _p, _p]),
+    "rmm_reduced_gemm": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64,
+                                        _i64, _i64, _i64, _p, _i64, _p]),
+    "rmm_reduced_qk": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64, _i64,
+                                      _i64, _i64, ctypes.c_float, ctypes.c_int, _p, _p]),
+    "rmm_linear": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
+                                  _i64, _i64, _i64, _p, _i64, _p, _p, ctypes.c_size_t, _p]),
+    "rmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+}
+EXPORTED_SYMBOLS = tuple(_SIGS)
+
+
+class RmmError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {rmm_status_string(status)} (status {status})")
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"librmm.so is missing at {LIB_PATH}; build it with "
+                          "`python -m paper_2608_13426_amd.build`")
+    handle = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(handle, name)
+        fn.restype = res
+        fn.argtypes = args
+    return handle
+
+
+lib = _load()
+
+
+# ---------------------------------------------------------------- helpers
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return RMM_BF16
+    if t.dtype == torch.float32:
+        return RMM_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; librmm takes bfloat16 or float32")
+
+
+def _dev(*ts: torch.Tensor) -> torch.device:
+    d = ts[0].device
+    for t in ts:
+        if t.device.type != "cuda":
+            raise ValueError("librmm tensors must live on the GPU")
+        if t.device != d:
+            raise ValueError("all tensors must be on one device")
+    return d
+
+
+def _stream(device: torch.device, stream) -> int:
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    return s.cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _rows(t: torch.Tensor, name: str):
+    """View a [U, M, K] or [M, K] tensor as U units of M rows with stride ldx."""
+    if t.dim() == 2:
+        t3 = t.unsqueeze(0)
+    elif t.dim() == 3:
+        t3 = t
+    else:
+        raise ValueError(f"{name} must be 2-D or 3-D")
+    U, M, K = t3.shape
+    if t3.stride(2) != 1:
+        raise ValueError(f"{name} rows must be contiguous")
+    ldx = t3.stride(1)
+    if U > 1 and t3.stride(0) != M * ldx:
+        raise ValueError(f"{name} units must be packed (stride M*ldx)")
+    return U, M, K, ldx
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise RmmError(fn, status)
+
+
+# ---------------------------------------------------------------- C-ABI
+
+def rmm_retained_count(r: float, K: int) -> int:
+    """k = ceil(r*K) (Sec. 3.2); -1 for r outside (0, 1] or K < 1."""
+    return int(lib.rmm_retained_count(float(r), int(K)))
+
+
+def rmm_workspace_size(op: int, B: int, M: int, K: int, k: int = 0) -> int:
+    return int(lib.rmm_workspace_size(int(op), int(B), int(M), int(K), int(k)))
+
+
+def rmm_status_string(status: int) -> str:
+    return lib.rmm_status_string(int(status)).decode()
+
+
+def rmm_score(X: torch.Tensor, energy: torch.Tensor, workspace: torch.Tensor | None = None,
+              stream=None) -> torch.Tensor:
+    """Column energies of each unit of X ([B, M, K] or [M, K]) into float64 energy [B, K]."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, energy)
+    if energy.dtype != torch.float64 or energy.numel() != B * K or not energy.is_contiguous():
+        raise ValueError("energy must be a contiguous float64 tensor of B*K elements")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("rmm_score", lib.rmm_score(X.data_ptr(), _dtype_code(X), B, M, K, ldx,
+                                      energy.data_ptr(), _ptr(workspace), ws_bytes,
+                                      _stream(d, stream)))
+    return energy
+
+
+def rmm_select(energy: torch.Tensor, k: int, idx: torch.Tensor, stream=None) -> torch.Tensor:
+    """TopK (ascending int32 indices) of each unit's energies.
+
+    energy holds B units of K float64 energies ([B, K], or flat); idx holds
+    B*k int32 slots, from which B is read.
+    """
+    d = _dev(energy, idx)
+    k = int(k)
+    if energy.dtype != torch.float64 or not energy.is_contiguous():
+        raise ValueError("energy must be contiguous float64")
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or k < 1 or idx.numel() % k:
+        raise ValueError("idx must be a contiguous int32 tensor of B*k elements")
+    B = idx.numel() // k
+    if B < 1 or energy.numel() % B:
+        raise ValueError("energy must hold B*K values")
+    K = energy.numel() // B
+    _check("rmm_select", lib.rmm_select(energy.data_ptr(), B, K, k, idx.data_ptr(),
+                                        _stream(d, stream)))
+    return idx
+
+
+def rmm_reduced_gemm(X: torch.Tensor, W: torch.Tensor, idx: torch.Tensor, Y: torch.Tensor,
+                     stream=None) -> torch.Tensor:
+    """Y[b] = X[b][:, I_b] @ W[I_b, :] for X [B, M, K], W [K, N], idx [B, k], Y [B, M, N]."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, W, idx, Y)
+    if W.dim() != 2 or W.shape[0] != K or W.stride(1) != 1:
+        raise ValueError("W must be [K, N] with contiguous rows")
+    N, ldw = W.shape[1], W.stride(0)
+    By, My, Ny, ldy = _rows(Y, "Y")
+    if (By, My, Ny) != (B, M, N):
+        raise ValueError("Y must be [B, M, N]")
+    if not (X.dtype == W.dtype == Y.dtype):
+        raise TypeError("X, W and Y must share one dtype")
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.numel() % B:
+        raise ValueError("idx must be contiguous int32 [B, k]")
+    k = idx.numel() // B
+    _check("rmm_reduced_gemm", lib.rmm_reduced_gemm(
+        X.data_ptr(), W.data_ptr(), idx.data_ptr(), _dtype_code(X), B, M, N, K, k, ldx, ldw,
+        Y.data_ptr(), ldy, _stream(d, stream)))
+    return Y
+
+
+def rmm_reduced_qk(Q: torch.Tensor, Kc: torch.Tensor, idx: torch.Tensor, S: torch.Tensor,
+                   causal: bool = True, scale: float | None = None, stream=None) -> torch.Tensor:
+    """Reduced scores for Q [batch, H, Lq, D], Kc [batch, Hkv, Lk, D], idx [batch, H, k]."""
+    if Q.dim() == 3:
+        Q, Kc, S = Q.unsqueeze(0), Kc.unsqueeze(0), S.unsqueeze(0)
+    batch, H, Lq, D = Q.shape
+    bk, Hkv, Lk, Dk = Kc.shape
+    d = _dev(Q, Kc, idx, S)
+    if bk != batch or Dk != D:
+        raise ValueError("Kc must be [batch, Hkv, Lk, D]")
+    if tuple(S.shape) != (batch, H, Lq, Lk):
+        raise ValueError("S must be [batch, H, Lq, Lk]")
+    for t, n in ((Q, "Q"), (Kc, "Kc"), (S, "S"), (idx, "idx")):
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    if not (Q.dtype == Kc.dtype == S.dtype):
+        raise TypeError("Q, Kc and S must share one dtype")
+    if idx.dtype != torch.int32 or idx.numel() % (batch * H):
+        raise ValueError("idx must be int32 [batch, H, k]")
+    k = idx.numel() // (batch * H)
+    if scale is None:
+        scale = D ** -0.5
+    _check("rmm_reduced_qk", lib.rmm_reduced_qk(
+        Q.data_ptr(), Kc.data_ptr(), idx.data_ptr(), _dtype_code(Q), batch, H, Hkv, Lq, Lk, D,
+        k, float(scale), 1 if causal else 0, S.data_ptr(), _stream(d, stream)))
+    return S
+
+
+def rmm_linear(X: torch.Tensor, W: torch.Tensor, r: float, Y: torch.Tensor,
+               idx_out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+               stream=None) -> torch.Tensor:
+    """Fused score -> select -> gathered GEMM at retention ratio r."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, W, Y)
+    if W.dim() != 2 or W.shape[0] != K or W.stride(1) != 1:
+        raise ValueError("W must be [K, N] with contiguous rows")
+    N, ldw = W.shape[1], W.stride(0)
+    By, My, Ny, ldy = _rows(Y, "Y")
+    if (By, My, Ny) != (B, M, N):
+        raise ValueError("Y must be [B, M, N]")
+    if not (X.dtype == W.dtype == Y.dtype):
+        raise TypeError("X, W and Y must share one dtype")
+    k = rmm_retained_count(r, K)
+    if idx_out is not None and (idx_out.dtype != torch.int32 or idx_out.numel() != B * max(k, 0)
+                                or not idx_out.is_contiguous()):
+        raise ValueError("idx_out must be contiguous int32 [B, k]")
+    if workspace is None:
+        workspace = torch.empty(max(rmm_workspace_size(RMM_OP_LINEAR, B, M, K, k), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_linear", lib.rmm_linear(
+        X.data_ptr(), W.data_ptr(), float(r), _dtype_code(X), B, M, N, K, ldx, ldw,
+        Y.data_ptr(), ldy, _ptr(idx_out), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    return Y

@@ -1,0 +1,184 @@
+// C-ABI of librmm: host-side validation, the k = ceil(r*K) rule, workspace
+// layout and dispatch to the gfx950 kernels.  Every check happens before
+// the first HIP call, so invalid calls never touch the device.
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/rmm.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int64_t kInt32Max = 2147483647;
+constexpr int64_t kGridYZMax = 65535;
+
+inline size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
+
+inline bool valid_dtype(rmm_dtype_t dt) { return dt == RMM_F32 || dt == RMM_BF16; }
+
+inline rmm_status_t from_hip(hipError_t e) { return e == hipSuccess ? RMM_OK : RMM_ERR_HIP; }
+
+rmm_status_t check_score(const void *X, rmm_dtype_t dt, int64_t B, int64_t M, int64_t K,
+                         int64_t ldx, const double *energy) {
+    if (!X || !energy) return RMM_ERR_INVALID_ARGUMENT;
+    if (!valid_dtype(dt)) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || M < 1 || K < 1 || ldx < K) return RMM_ERR_INVALID_ARGUMENT;
+    if (K > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (B > kGridYZMax) return RMM_ERR_UNSUPPORTED;
+    return RMM_OK;
+}
+
+// Checks shared by rmm_reduced_gemm and rmm_linear (whose index list lives
+// in the workspace or idx_out, so it has no idx pointer to check here).
+rmm_status_t check_gemm_shapes(const void *X, const void *W, rmm_dtype_t dt, int64_t B,
+                               int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx,
+                               int64_t ldw, const void *Y, int64_t ldy) {
+    if (!X || !W || !Y) return RMM_ERR_INVALID_ARGUMENT;
+    if (!valid_dtype(dt)) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || M < 1 || N < 1 || K < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (k < 1 || k > K) return RMM_ERR_INVALID_ARGUMENT;
+    if (ldx < K || ldw < N || ldy < N) return RMM_ERR_INVALID_ARGUMENT;
+    if (K > kInt32Max || M > kInt32Max || N > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (B > kGridYZMax || M > kGridYZMax * 64) return RMM_ERR_UNSUPPORTED;
+    return RMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t rmm_retained_count(double r, int64_t K) {
+    if (K < 1 || K > kInt32Max) return -1;
+    if (!(r > 0.0 && r <= 1.0)) return -1;     // also rejects NaN
+    const double p = r * static_cast<double>(K);
+    const double nearest = std::nearbyint(p);
+    int64_t k;
+    if (std::fabs(p - nearest) <= 1e-9 * static_cast<double>(K))
+        k = static_cast<int64_t>(nearest);
+    else
+        k = static_cast<int64_t>(std::ceil(p));
+    if (k < 1) k = 1;
+    if (k > K) k = K;
+    return k;
+}
+
+size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t k) {
+    if (B < 1 || K < 1) return 0;
+    switch (op) {
+    case RMM_OP_SCORE:
+        return M < 1 ? 0 : rmm::score_workspace_bytes(B, M, K);
+    case RMM_OP_SELECT:
+        return 0;
+    case RMM_OP_LINEAR:
+        if (M < 1 || k < 1 || k > K) return 0;
+        return align256(rmm::score_workspace_bytes(B, M, K)) +
+               align256(static_cast<size_t>(B * K) * sizeof(double)) +
+               align256(static_cast<size_t>(B * k) * sizeof(int32_t));
+    }
+    return 0;
+}
+
+rmm_status_t rmm_score(const void *X, rmm_dtype_t dtype, int64_t B, int64_t M, int64_t K,
+                       int64_t ldx, double *energy, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream) {
+    rmm_status_t st = check_score(X, dtype, B, M, K, ldx, energy);
+    if (st != RMM_OK) return st;
+    const size_t need = rmm::score_workspace_bytes(B, M, K);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+        if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
+    }
+    return from_hip(rmm::launch_score(X, dtype == RMM_BF16, B, M, K, ldx, energy,
+                                      static_cast<double *>(workspace), stream));
+}
+
+rmm_status_t rmm_select(const double *energy, int64_t B, int64_t K, int64_t k, int32_t *idx,
+                        hipStream_t stream) {
+    if (!energy || !idx) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || K < 1 || k < 1 || k > K || K > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (B > kInt32Max) return RMM_ERR_UNSUPPORTED;
+    return from_hip(rmm::launch_select(energy, B, K, k, idx, stream));
+}
+
+rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx, rmm_dtype_t dtype,
+                              int64_t B, int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx,
+                              int64_t ldw, void *Y, int64_t ldy, hipStream_t stream) {
+    if (!idx) return RMM_ERR_INVALID_ARGUMENT;
+    rmm_status_t st = check_gemm_shapes(X, W, dtype, B, M, N, K, k, ldx, ldw, Y, ldy);
+    if (st != RMM_OK) return st;
+    if (dtype == RMM_BF16)
+        return from_hip(rmm::launch_gemm_bf16(
+            static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(W), idx, B, M, N, K, k,
+            ldx, ldw, static_cast<uint16_t *>(Y), ldy, stream));
+    return from_hip(rmm::launch_gemm_f32(static_cast<const float *>(X),
+                                         static_cast<const float *>(W), idx, B, M, N, K, k, ldx,
+                                         ldw, static_cast<float *>(Y), ldy, stream));
+}
+
+rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx, rmm_dtype_t dtype,
+                            int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
+                            int64_t D, int64_t k, float scale, int causal, void *S,
+                            hipStream_t stream) {
+    if (!Q || !Kc || !idx || !S) return RMM_ERR_INVALID_ARGUMENT;
+    if (!valid_dtype(dtype)) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (H % Hkv != 0) return RMM_ERR_INVALID_ARGUMENT;
+    if (k < 1 || k > D) return RMM_ERR_INVALID_ARGUMENT;
+    if (Lq > kInt32Max || Lk > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (D > 256) return RMM_ERR_UNSUPPORTED;
+    if (batch * H > kGridYZMax || Lq > kGridYZMax * 64) return RMM_ERR_UNSUPPORTED;
+    if (dtype == RMM_BF16)
+        return from_hip(rmm::launch_qk_bf16(static_cast<const uint16_t *>(Q),
+                                            static_cast<const uint16_t *>(Kc), idx, batch, H, Hkv,
+                                            Lq, Lk, D, k, scale, causal != 0,
+                                            static_cast<uint16_t *>(S), stream));
+    return from_hip(rmm::launch_qk_f32(static_cast<const float *>(Q), static_cast<const float *>(Kc),
+                                       idx, batch, H, Hkv, Lq, Lk, D, k, scale, causal != 0,
+                                       static_cast<float *>(S), stream));
+}
+
+rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtype, int64_t B,
+                        int64_t M, int64_t N, int64_t K, int64_t ldx, int64_t ldw, void *Y,
+                        int64_t ldy, int32_t *idx_out, void *workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+    const int64_t k = rmm_retained_count(r, K);
+    if (k < 0) return RMM_ERR_INVALID_ARGUMENT;
+    rmm_status_t st = check_gemm_shapes(X, W, dtype, B, M, N, K, k, ldx, ldw, Y, ldy);
+    if (st != RMM_OK) return st;
+    const size_t need = rmm_workspace_size(RMM_OP_LINEAR, B, M, K, k);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
+
+    char *ws = static_cast<char *>(workspace);
+    double *partials = reinterpret_cast<double *>(ws);
+    ws += align256(rmm::score_workspace_bytes(B, M, K));
+    double *energy = reinterpret_cast<double *>(ws);
+    ws += align256(static_cast<size_t>(B * K) * sizeof(double));
+    int32_t *idx = idx_out ? idx_out : reinterpret_cast<int32_t *>(ws);
+
+    hipError_t e = rmm::launch_score(X, dtype == RMM_BF16, B, M, K, ldx, energy, partials, stream);
+    if (e != hipSuccess) return RMM_ERR_HIP;
+    e = rmm::launch_select(energy, B, K, k, idx, stream);
+    if (e != hipSuccess) return RMM_ERR_HIP;
+    if (dtype == RMM_BF16)
+        e = rmm::launch_gemm_bf16(static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(W),
+                                  idx, B, M, N, K, k, ldx, ldw, static_cast<uint16_t *>(Y), ldy,
+                                  stream);
+    else
+        e = rmm::launch_gemm_f32(static_cast<const float *>(X), static_cast<const float *>(W), idx,
+                                 B, M, N, K, k, ldx, ldw, static_cast<float *>(Y), ldy, stream);
+    return from_hip(e);
+}
+
+const char *rmm_status_string(rmm_status_t status) {
+    switch (status) {
+    case RMM_OK: return "success";
+    case RMM_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case RMM_ERR_UNSUPPORTED: return "unsupported argument combination";
+    case RMM_ERR_WORKSPACE_TOO_SMALL: return "workspace missing or too small";
+    case RMM_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,49 @@
+// Internal launchers of librmm's gfx950 kernels.  Arguments are validated by
+// the C-ABI layer (api.hip) before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rmm {
+
+// ---------------------------------------------------------------- scoring
+// Column energies are reduced in two levels: a grid of (column block, row
+// split, unit) workgroups writes float64 partial sums, then a second kernel
+// adds the splits in a fixed order.  Splits depend only on (B, M, K).
+constexpr int kScoreCols = 128;        // columns per workgroup
+constexpr int kScoreMinRows = 64;      // fewest rows per split
+constexpr int kScoreTargetBlocks = 1024;
+
+int64_t score_splits(int64_t B, int64_t M, int64_t K);
+size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K);
+
+hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t K,
+                        int64_t ldx, double *energy, double *partials,
+                        hipStream_t stream);
+
+// -------------------------------------------------------------- selection
+hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
+                         int32_t *idx, hipStream_t stream);
+
+// ------------------------------------------------------- gathered GEMM
+hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx,
+                            int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                            int64_t ldx, int64_t ldw, uint16_t *Y, int64_t ldy,
+                            hipStream_t stream);
+hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx,
+                           int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                           int64_t ldx, int64_t ldw, float *Y, int64_t ldy,
+                           hipStream_t stream);
+
+// --------------------------------------------------------- reduced QK^T
+hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *idx,
+                          int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
+                          int64_t Lk, int64_t D, int64_t k, float scale, bool causal,
+                          uint16_t *S, hipStream_t stream);
+hipError_t launch_qk_f32(const float *Q, const float *Kc, const int32_t *idx,
+                         int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
+                         int64_t Lk, int64_t D, int64_t k, float scale, bool causal,
+                         float *S, hipStream_t stream);
+
+}  // namespace rmm

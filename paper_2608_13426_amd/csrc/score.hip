@@ -1,0 +1,169 @@
+// Column energies e_j = sum_m X[m][j]^2 of each selection unit
+// (Sec. 3.2 score s_j = ||A[:, j]||_2, ranked through s_j^2).
+//
+// HBM-bound streaming reduction.  Each workgroup owns 128 columns of one row
+// split of one unit; its lanes read whole 16-byte vectors along a row, so a
+// wave touches full 128-byte lines.  bf16/fp32 values are squared exactly in
+// float64 and accumulated in float64 in a fixed order: per thread over its
+// rows, then the row groups of the workgroup in order, then the splits in
+// order (second kernel).  No atomics, so results are bit-reproducible.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace rmm {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ double to_f64(uint16_t v) { return static_cast<double>(bf16_to_f32(v)); }
+__device__ __forceinline__ double to_f64(float v) { return static_cast<double>(v); }
+
+// VEC = elements per 16-byte load, or 1 for the element-wise path used when
+// rows are not 16-byte aligned.
+template <typename T, int VEC>
+__global__ __launch_bounds__(kThreads) void score_partial_kernel(
+    const T *__restrict__ X, int64_t M, int64_t K, int64_t ldx, int64_t rows_per_split,
+    double *__restrict__ out, int64_t out_unit_stride, int64_t out_split_stride) {
+    constexpr int TPR = kScoreCols / VEC;     // threads along a row
+    constexpr int RPI = kThreads / TPR;       // rows per iteration
+    __shared__ double red[RPI][kScoreCols];
+
+    const int tid = threadIdx.x;
+    const int lane_col = (tid % TPR) * VEC;
+    const int row_off = tid / TPR;
+    const int64_t col0 = static_cast<int64_t>(blockIdx.x) * kScoreCols + lane_col;
+    const int64_t split = blockIdx.y;
+    const int64_t unit = blockIdx.z;
+    const int64_t r_begin = split * rows_per_split;
+    const int64_t r_end = min(M, r_begin + rows_per_split);
+    const T *base = X + unit * M * ldx;
+
+    double acc[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
+
+    if constexpr (VEC > 1) {
+        const bool full = col0 + VEC <= K;
+        int64_t r = r_begin + row_off;
+        // four rows in flight per thread
+        for (; r + 3 * RPI < r_end; r += 4 * RPI) {
+            uint4 q[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const T *p = base + (r + u * RPI) * ldx + col0;
+                if (full) {
+                    q[u] = *reinterpret_cast<const uint4 *>(p);
+                } else {
+                    T tmp[VEC];
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) tmp[v] = (col0 + v < K) ? p[v] : T(0);
+                    q[u] = *reinterpret_cast<const uint4 *>(tmp);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const T *t = reinterpret_cast<const T *>(&q[u]);
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    const double x = to_f64(t[v]);
+                    acc[v] = fma(x, x, acc[v]);
+                }
+            }
+        }
+        for (; r < r_end; r += RPI) {
+            const T *p = base + r * ldx + col0;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                const double x = (col0 + v < K) ? to_f64(p[v]) : 0.0;
+                acc[v] = fma(x, x, acc[v]);
+            }
+        }
+    } else {
+        if (col0 < K) {
+            for (int64_t r = r_begin + row_off; r < r_end; r += RPI) {
+                const double x = to_f64(base[r * ldx + col0]);
+                acc[0] = fma(x, x, acc[0]);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) red[row_off][lane_col + v] = acc[v];
+    __syncthreads();
+    if (tid < kScoreCols) {
+        double s = 0.0;
+#pragma unroll
+        for (int g = 0; g < RPI; ++g) s += red[g][tid];
+        const int64_t col = static_cast<int64_t>(blockIdx.x) * kScoreCols + tid;
+        if (col < K) out[unit * out_unit_stride + split * out_split_stride + col] = s;
+    }
+}
+
+// energy[b][j] = sum over splits s (in order) of partials[b][s][j]
+__global__ __launch_bounds__(kThreads) void score_finalize_kernel(
+    const double *__restrict__ partials, int64_t B, int64_t S, int64_t K,
+    double *__restrict__ energy) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    if (t >= B * K) return;
+    const int64_t b = t / K, j = t % K;
+    const double *p = partials + b * S * K + j;
+    double s = 0.0;
+    for (int64_t i = 0; i < S; ++i) s += p[i * K];
+    energy[t] = s;
+}
+
+template <typename T, int VEC>
+hipError_t launch_partial(const T *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                          int64_t S, double *out, int64_t unit_stride, int64_t split_stride,
+                          hipStream_t stream) {
+    const int64_t rps = (M + S - 1) / S;
+    dim3 grid(static_cast<unsigned>((K + kScoreCols - 1) / kScoreCols),
+              static_cast<unsigned>(S), static_cast<unsigned>(B));
+    hipLaunchKernelGGL((score_partial_kernel<T, VEC>), grid, dim3(kThreads), 0, stream,
+                       X, M, K, ldx, rps, out, unit_stride, split_stride);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t score_splits(int64_t B, int64_t M, int64_t K) {
+    const int64_t col_blocks = (K + kScoreCols - 1) / kScoreCols;
+    int64_t s = (kScoreTargetBlocks + B * col_blocks - 1) / (B * col_blocks);
+    const int64_t max_s = (M + kScoreMinRows - 1) / kScoreMinRows;
+    if (s > max_s) s = max_s;
+    if (s > 65535) s = 65535;
+    return s < 1 ? 1 : s;
+}
+
+size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K) {
+    const int64_t s = score_splits(B, M, K);
+    return s > 1 ? static_cast<size_t>(B * s * K) * sizeof(double) : 0;
+}
+
+hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t K,
+                        int64_t ldx, double *energy, double *partials, hipStream_t stream) {
+    const int64_t S = score_splits(B, M, K);
+    double *out = S > 1 ? partials : energy;
+    const int64_t unit_stride = S * K, split_stride = K;
+    const size_t esz = bf16 ? 2 : 4;
+    const bool aligned = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
+                         ((ldx * static_cast<int64_t>(esz)) % 16 == 0);
+    hipError_t err;
+    if (bf16) {
+        const uint16_t *x = static_cast<const uint16_t *>(X);
+        err = aligned ? launch_partial<uint16_t, 8>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream)
+                      : launch_partial<uint16_t, 1>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream);
+    } else {
+        const float *x = static_cast<const float *>(X);
+        err = aligned ? launch_partial<float, 4>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream)
+                      : launch_partial<float, 1>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream);
+    }
+    if (err != hipSuccess || S == 1) return err;
+    const int64_t n = B * K;
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(static_cast<unsigned>((n + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, stream, partials, B, S, K, energy);
+    return hipGetLastError();
+}
+
+}  // namespace rmm

@@ -1,0 +1,180 @@
+// TopK over each unit's energies (Sec. 3.2: I = TopK({s_j}, ceil(rho d))),
+// returned as an ascending index list.
+//
+// One workgroup per selection unit.  Each float64 energy is mapped to a
+// 64-bit key whose unsigned order is the order of the values (NaN above
+// +inf, -0 == +0), so the whole selection is integer work: an MSB-first
+// radix select with 8-bit digits finds the k-th largest key, using LDS
+// histograms with integer atomics (order-independent counts).  It stops as
+// soon as the bucket holding the k-th key is taken whole.  Keys tied with
+// the k-th key are taken lowest index first, and the kept indices are
+// compacted in ascending order with two workgroup prefix scans.  Each thread
+// owns a contiguous chunk of keys, kept in registers when it fits.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace rmm {
+
+namespace {
+
+__device__ __forceinline__ uint64_t order_key(double d) {
+    uint64_t u = __double_as_longlong(d);
+    if (d != d) u = 0x7ff8000000000000ull;          // every NaN -> one quiet NaN
+    if (u == 0x8000000000000000ull) u = 0;          // -0 ties with +0
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane) {
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+
+// Exclusive prefix sum of v over the workgroup in thread order.
+template <int NT>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *buf) {
+    constexpr int NW = NT / kWave;
+    const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+    const uint32_t incl = wave_inclusive_scan(v, lane);
+    if (lane == kWave - 1) buf[w] = incl;
+    __syncthreads();
+    if (w == 0) {
+        const uint32_t x = lane < NW ? buf[lane] : 0u;
+        const uint32_t xi = wave_inclusive_scan(x, lane);
+        if (lane < NW) buf[lane] = xi - x;
+    }
+    __syncthreads();
+    const uint32_t r = buf[w] + incl - v;
+    __syncthreads();
+    return r;
+}
+
+// NT threads; C keys per thread held in registers (REG) or re-read from
+// memory (REG == false, chunk size `cpt` at run time).
+template <int NT, int C, bool REG>
+__global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ energy,
+                                                    int64_t K, int64_t k, int cpt,
+                                                    int32_t *__restrict__ idx) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t scan_buf[NT / kWave];
+    __shared__ uint32_t s_digit, s_above, s_count;
+
+    const int tid = threadIdx.x;
+    const double *e = energy + static_cast<int64_t>(blockIdx.x) * K;
+    int32_t *out = idx + static_cast<int64_t>(blockIdx.x) * k;
+    const int chunk = REG ? C : cpt;
+    const int64_t c0 = static_cast<int64_t>(tid) * chunk;
+
+    if (k == K) {                       // everything is kept
+        for (int64_t j = tid; j < K; j += NT) out[j] = static_cast<int32_t>(j);
+        return;
+    }
+
+    uint64_t keys[REG ? C : 1];
+    if constexpr (REG) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t j = c0 + c;
+            keys[c] = j < K ? order_key(e[j]) : 0ull;
+        }
+    }
+    auto key_at = [&](int c) -> uint64_t {
+        if constexpr (REG) return keys[c];
+        else return order_key(e[c0 + c]);
+    };
+    const int n_own = static_cast<int>(max<int64_t>(0, min<int64_t>(chunk, K - c0)));
+
+    uint64_t prefix = 0, mask = 0;
+    uint32_t need = static_cast<uint32_t>(k);
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += NT) hist[i] = 0;
+        __syncthreads();
+        if constexpr (REG) {
+#pragma unroll
+            for (int c = 0; c < C; ++c)
+                if (c < n_own && (keys[c] & mask) == prefix)
+                    atomicAdd(&hist[(keys[c] >> shift) & 0xff], 1u);
+        } else {
+            for (int c = 0; c < n_own; ++c) {
+                const uint64_t u = key_at(c);
+                if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 0xff], 1u);
+            }
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            // lane L holds digits 255-4L .. 252-4L (descending value order)
+            uint32_t h[4], sum = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) { h[q] = hist[255 - 4 * tid - q]; sum += h[q]; }
+            const uint32_t incl = wave_inclusive_scan(sum, tid);
+            uint32_t run = incl - sum;
+            if (run < need && need <= incl) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (run + h[q] >= need) {
+                        s_digit = 255 - 4 * tid - q;
+                        s_above = run;
+                        s_count = h[q];
+                        break;
+                    }
+                    run += h[q];
+                }
+            }
+        }
+        __syncthreads();
+        need -= s_above;
+        prefix |= static_cast<uint64_t>(s_digit) << shift;
+        mask |= 0xffull << shift;
+        if (s_count == need) break;      // the whole bucket is kept
+    }
+
+    // candidates share the prefix; keep the first `need` of them by index
+    uint32_t n_cand = 0;
+    for (int c = 0; c < n_own; ++c) n_cand += ((key_at(c) & mask) == prefix);
+    uint32_t cand = block_exclusive_scan<NT>(n_cand, scan_buf);
+    uint32_t n_sel = 0;
+    {
+        uint32_t cc = cand;
+        for (int c = 0; c < n_own; ++c) {
+            const uint64_t p = key_at(c) & mask;
+            if (p > prefix) ++n_sel;
+            else if (p == prefix) { n_sel += (cc < need); ++cc; }
+        }
+    }
+    uint32_t pos = block_exclusive_scan<NT>(n_sel, scan_buf);
+    for (int c = 0; c < n_own; ++c) {
+        const uint64_t p = key_at(c) & mask;
+        bool keep = p > prefix;
+        if (p == prefix) { keep = cand < need; ++cand; }
+        if (keep) out[pos++] = static_cast<int32_t>(c0 + c);
+    }
+}
+
+template <int NT, int C, bool REG>
+hipError_t launch(const double *energy, int64_t B, int64_t K, int64_t k, int cpt,
+                  int32_t *idx, hipStream_t stream) {
+    hipLaunchKernelGGL((select_kernel<NT, C, REG>), dim3(static_cast<unsigned>(B)), dim3(NT), 0,
+                       stream, energy, K, k, cpt, idx);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
+                         int32_t *idx, hipStream_t stream) {
+    if (K <= 256) return launch<256, 1, true>(energy, B, K, k, 1, idx, stream);
+    if (K <= 512) return launch<256, 2, true>(energy, B, K, k, 2, idx, stream);
+    if (K <= 1024) return launch<256, 4, true>(energy, B, K, k, 4, idx, stream);
+    if (K <= 2048) return launch<256, 8, true>(energy, B, K, k, 8, idx, stream);
+    if (K <= 4096) return launch<1024, 4, true>(energy, B, K, k, 4, idx, stream);
+    if (K <= 8192) return launch<1024, 8, true>(energy, B, K, k, 8, idx, stream);
+    if (K <= 16384) return launch<1024, 16, true>(energy, B, K, k, 16, idx, stream);
+    if (K <= 32768) return launch<1024, 32, true>(energy, B, K, k, 32, idx, stream);
+    const int cpt = static_cast<int>((K + 1023) / 1024);
+    return launch<1024, 1, false>(energy, B, K, k, cpt, idx, stream);
+}
+
+}  // namespace rmm

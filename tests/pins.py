@@ -329,6 +329,9 @@ def check_qk(o):
     for h in range(2):
         assert np.array_equal(np.isneginf(S[h]), mask)
         assert np.all(np.isfinite(S[h][~mask]))
+    # rows computed one by one are the same rows of the full S, mask included
+    Sr = o.reduced_qk(Q, Kt, idx, causal=True, rows=[2, 0])
+    assert np.array_equal(Sr[:, 0], S[:, 2]) and np.array_equal(Sr[:, 1], S[:, 0])
     # r = 1 is the dense scaled product (exact dots)
     Q = _bf16(73, (2, 5, 16))
     Kt = _bf16(74, (1, 6, 16))

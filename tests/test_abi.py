@@ -1,0 +1,168 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and its host-side logic (k rule, workspace sizes, argument
+validation) behaves as documented.  Only calls that fail validation are made
+here; validation happens before any HIP call."""
+import ctypes
+import math
+import os
+import re
+from fractions import Fraction
+
+import pytest
+
+import paper_2608_13426_amd as rmm
+from oracle import rmm_oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rmm.h")
+
+OK, INVALID, UNSUPPORTED, WS_SMALL, HIP = 0, 1, 2, 3, 4
+P = ctypes.c_void_p(0x100000)          # a non-null pointer that is never dereferenced
+NULL = None
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rmm_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_are_exported():
+    names = _declared()
+    assert names == sorted(rmm.EXPORTED_SYMBOLS)
+    for n in names:
+        assert hasattr(rmm.lib, n), n
+
+
+def test_library_is_gfx950_code_object():
+    data = open(rmm.LIB_PATH, "rb").read()
+    assert b"gfx950" in data
+
+
+def test_retained_count_matches_rule():
+    for K in (1, 2, 7, 100, 128, 512, 4096, 14336, 28672):
+        for p in range(1, 101):
+            s = f"{p / 100:.2f}"
+            want = max(1, math.ceil(Fraction(s) * K))
+            assert rmm.rmm_retained_count(float(s), K) == want
+            assert rmm.rmm_retained_count(float(s), K) == rmm_oracle.retained_count(float(s), K)
+    assert rmm.rmm_retained_count(0.07, 100) == 7
+    assert rmm.rmm_retained_count(0.8, 128) == 103
+    for bad in (0.0, -1.0, 1.0000001, float("nan"), float("inf")):
+        assert rmm.rmm_retained_count(bad, 128) == -1
+    assert rmm.rmm_retained_count(0.5, 0) == -1
+    assert rmm.rmm_retained_count(0.5, 2 ** 31) == -1
+
+
+def test_workspace_sizes():
+    # score: one float64 partial per (unit, split, column); none when unsplit
+    ws = rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 1, 8192, 4096)
+    assert ws > 0 and ws % 8 == 0
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 1, 32, 512) == 0
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_SELECT, 4, 100, 4096, 10) == 0
+    lin = rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 8192, 4096, 2048)
+    assert lin >= ws + 4096 * 8 + 2048 * 4
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 8192, 4096, 0) == 0
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 0, 8192, 4096) == 0
+
+
+def test_status_strings():
+    for code in range(5):
+        s = rmm.rmm_status_string(code)
+        assert isinstance(s, str) and s
+    assert rmm.rmm_status_string(99) == "unknown status"
+
+
+def test_score_validation():
+    f = rmm.lib.rmm_score
+    assert f(NULL, 1, 1, 8, 8, 8, P, NULL, 0, NULL) == INVALID
+    assert f(P, 1, 1, 8, 8, 8, NULL, NULL, 0, NULL) == INVALID
+    assert f(P, 7, 1, 8, 8, 8, P, NULL, 0, NULL) == INVALID        # dtype
+    assert f(P, 1, 0, 8, 8, 8, P, NULL, 0, NULL) == INVALID        # B
+    assert f(P, 1, 1, 0, 8, 8, P, NULL, 0, NULL) == INVALID        # M
+    assert f(P, 1, 1, 8, 0, 8, P, NULL, 0, NULL) == INVALID        # K
+    assert f(P, 1, 1, 8, 8, 7, P, NULL, 0, NULL) == INVALID        # ldx < K
+    assert f(P, 1, 70000, 8, 8, 8, P, NULL, 0, NULL) == UNSUPPORTED
+    need = rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 1, 8192, 4096)
+    assert f(P, 1, 1, 8192, 4096, 4096, P, NULL, 0, NULL) == WS_SMALL
+    assert f(P, 1, 1, 8192, 4096, 4096, P, P, need - 8, NULL) == WS_SMALL
+    assert f(P, 1, 1, 8192, 4096, 4096, P, ctypes.c_void_p(0x100004), need, NULL) == INVALID
+
+
+def test_select_validation():
+    f = rmm.lib.rmm_select
+    assert f(NULL, 1, 8, 2, P, NULL) == INVALID
+    assert f(P, 1, 8, 2, NULL, NULL) == INVALID
+    assert f(P, 0, 8, 2, P, NULL) == INVALID
+    assert f(P, 1, 8, 0, P, NULL) == INVALID
+    assert f(P, 1, 8, 9, P, NULL) == INVALID
+    assert f(P, 1, 0, 1, P, NULL) == INVALID
+    assert f(P, 1, 2 ** 31, 1, P, NULL) == INVALID
+
+
+def test_gemm_validation():
+    f = rmm.lib.rmm_reduced_gemm
+    args = dict(X=P, W=P, idx=P, dt=1, B=1, M=16, N=16, K=32, k=8, ldx=32, ldw=16, Y=P, ldy=16)
+
+    def call(**kw):
+        a = {**args, **kw}
+        return f(a["X"], a["W"], a["idx"], a["dt"], a["B"], a["M"], a["N"], a["K"], a["k"],
+                 a["ldx"], a["ldw"], a["Y"], a["ldy"], NULL)
+
+    for name in ("X", "W", "idx", "Y"):
+        assert call(**{name: NULL}) == INVALID, name
+    assert call(dt=5) == INVALID
+    for name in ("B", "M", "N", "K"):
+        assert call(**{name: 0}) == INVALID, name
+    assert call(k=0) == INVALID
+    assert call(k=33) == INVALID
+    assert call(ldx=31) == INVALID
+    assert call(ldw=15) == INVALID
+    assert call(ldy=15) == INVALID
+    assert call(B=70000) == UNSUPPORTED
+
+
+def test_qk_validation():
+    f = rmm.lib.rmm_reduced_qk
+    base = [P, P, P, 1, 1, 32, 8, 64, 64, 128, 64, ctypes.c_float(0.088), 1, P, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 13):
+        assert call(i, NULL) == INVALID
+    assert call(3, 9) == INVALID           # dtype
+    assert call(4, 0) == INVALID           # batch
+    assert call(6, 5) == INVALID           # H % Hkv
+    assert call(10, 0) == INVALID          # k
+    assert call(10, 129) == INVALID        # k > D
+    assert call(9, 512) == UNSUPPORTED     # D > 256
+
+
+def test_linear_validation():
+    f = rmm.lib.rmm_linear
+    need = rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 64, 128, 64)
+    base = [P, P, 0.5, 1, 1, 64, 32, 128, 128, 32, P, 32, NULL, P, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    assert call(2, 0.0) == INVALID
+    assert call(2, 1.5) == INVALID
+    assert call(2, float("nan")) == INVALID
+    assert call(0, NULL) == INVALID
+    assert call(13, NULL) == WS_SMALL
+    assert call(14, need - 1) == WS_SMALL
+    assert call(8, 100) == INVALID           # ldx < K
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    x = torch.zeros(4, 8, dtype=torch.bfloat16)
+    e = torch.zeros(8, dtype=torch.float64)
+    with pytest.raises(ValueError):
+        rmm.rmm_score(x, e)
