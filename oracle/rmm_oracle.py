@@ -172,25 +172,27 @@ def gqa_kv_head(h: int, H: int, Hkv: int) -> int:
 
 
 def reduced_qk(Q: np.ndarray, K: np.ndarray, idx: np.ndarray,
-               causal: bool) -> np.ndarray:
+               causal: bool, rows=None) -> np.ndarray:
     """S[h] = (1/sqrt(D)) Q[h][:, I_h] K[g(h)][:, I_h]^T, masked (Sec. 3.3).
 
     Q [H x Lq x D], K [Hkv x Lk x D], idx [H x k] -> S [H x Lq x Lk] float64
-    with -inf at masked entries (t > i + Lk - Lq) when ``causal``.
+    with -inf at masked entries (t > i + Lk - Lq) when ``causal``.  With
+    ``rows`` (query positions i), only those rows of S are computed.
     """
     Q = np.asarray(Q, dtype=np.float64)
     K = np.asarray(K, dtype=np.float64)
     H, Lq, D = Q.shape
     Hkv, Lk, _ = K.shape
+    rows = np.arange(Lq) if rows is None else np.asarray(rows, dtype=np.int64)
     scale = 1.0 / math.sqrt(D)
-    S = np.empty((H, Lq, Lk), dtype=np.float64)
+    S = np.empty((H, rows.shape[0], Lk), dtype=np.float64)
+    i = rows[:, None]
+    t = np.arange(Lk)[None, :]
     for h in range(H):
         g = gqa_kv_head(h, H, Hkv)
         I = np.asarray(idx[h], dtype=np.int64)
-        S[h] = scale * (Q[h][:, I] @ K[g][:, I].T)
+        S[h] = scale * (Q[h][rows][:, I] @ K[g][:, I].T)
         if causal:
-            i = np.arange(Lq)[:, None]
-            t = np.arange(Lk)[None, :]
             S[h][t > i + (Lk - Lq)] = -np.inf
     return S
 
