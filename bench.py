@@ -1,0 +1,264 @@
+"""Benchmark of the RMM hot path on one MI355X.
+
+One step = one pass of the whole reduced path of an 8B-class decoder layer
+(seq 8192, hidden 4096, 32 query / 8 kv heads of dim 128, MLP 14336) at
+retention ratio r, on synthetic bf16 inputs already resident in HBM:
+
+  * q/k/v  : energies of the attention input, TopK, three gathered GEMMs
+             (the three projections read one input, so they share one set)
+  * o      : energies, TopK, gathered GEMM
+  * gate/up: energies of the MLP input, TopK, two gathered GEMMs
+  * down   : energies, TopK, gathered GEMM
+  * QK^T   : per-head energies of Q, TopK per head, reduced QK^T (causal)
+
+The headline is retained TFLOP/s (2*M*N*k per projection plus 2*k per
+computed causal score) at r = 0.5, with the speedup of the same pipeline
+over its own r = 1 run.  Each r is timed separately: W warm-up steps, then
+K timed steps bracketed by device synchronisation.
+
+  python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--ratios 0.25,0.5,0.75,1.0]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "reduced-GEMM TFLOP/s (retained FLOPs) + speedup vs dense r=1, 8B shapes, seq 8192"
+HEADLINE_R = 0.5
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (no sparsity)
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--ratios", default="0.25,0.5,0.75,1.0")
+    p.add_argument("--workload", default="layer_8b")
+    p.add_argument("--cpu-tokens", type=int, default=4096,
+                   help="tokens of the bounded CPU-oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+# ---------------------------------------------------------------- inputs
+
+class Layer:
+    """Device-resident inputs, weights and outputs of one decoder layer."""
+
+    def __init__(self, wk, dev):
+        import torch
+        import workloads as wl
+        self.wk, self.dev = wk, dev
+        self.M = wk.M
+
+        def put(f32):
+            bits = wl.f32_to_bf16_bits(f32)
+            return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+
+        self.X = {name: put(wl.workload_input(wk, name)) for name in wk.inputs}
+        self.W = {p.name: put(wl.workload_weight(wk, p)) for p in wk.projections}
+        self.Y = {p.name: torch.empty((self.M, p.N), dtype=torch.bfloat16, device=dev)
+                  for p in wk.projections}
+        a = wk.attention
+        q, k = wl.workload_qk(wk)
+        self.Q = put(q).reshape(1, a.H, a.L, a.D)
+        self.Kc = put(k).reshape(1, a.Hkv, a.L, a.D)
+        self.S = torch.empty((1, a.H, a.L, a.L), dtype=torch.bfloat16, device=dev)
+        # groups of projections that read one input
+        self.groups = {}
+        for p in wk.projections:
+            self.groups.setdefault(p.input_name, []).append(p)
+        Kmax = max(v[0] for v in wk.inputs.values())
+        import paper_2608_13426_amd as rmm
+        ws = max(rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 1, self.M, Kmax),
+                 rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, a.H, a.L, a.D), 1)
+        self.ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.energy = torch.empty(max(Kmax, a.H * a.D), dtype=torch.float64, device=dev)
+        self.idx = {name: None for name in wk.inputs}
+        self.qidx = None
+
+
+def flops(wk, r):
+    """Retained FLOPs of one step at ratio r."""
+    import paper_2608_13426_amd as rmm
+    proj = sum(2 * wk.M * p.N * rmm.rmm_retained_count(r, p.K) for p in wk.projections)
+    a = wk.attention
+    pairs = a.L * (a.L + 1) // 2
+    qk = 2 * a.H * pairs * rmm.rmm_retained_count(r, a.D)
+    return proj, qk
+
+
+def run_step(L, r, gemm_events=None):
+    """Enqueue one full step on the current stream."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    wk = L.wk
+    for name, projs in L.groups.items():
+        K = wk.inputs[name][0]
+        k = rmm.rmm_retained_count(r, K)
+        X = L.X[name]
+        e = L.energy[:K]
+        rmm.rmm_score(X, e, L.ws)
+        if L.idx[name] is None or L.idx[name].numel() != k:
+            L.idx[name] = torch.empty(k, dtype=torch.int32, device=L.dev)
+        rmm.rmm_select(e, k, L.idx[name])
+        for p in projs:
+            if gemm_events is not None:
+                ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ev0.record()
+            rmm.rmm_reduced_gemm(X, L.W[p.name], L.idx[name].view(1, k), L.Y[p.name])
+            if gemm_events is not None:
+                ev1.record()
+                gemm_events.append((ev0, ev1, 2 * wk.M * p.N * k))
+    a = wk.attention
+    kq = rmm.rmm_retained_count(r, a.D)
+    e = L.energy[:a.H * a.D]
+    rmm.rmm_score(L.Q.reshape(a.H, a.L, a.D), e, L.ws)
+    if L.qidx is None or L.qidx.numel() != a.H * kq:
+        L.qidx = torch.empty(a.H * kq, dtype=torch.int32, device=L.dev)
+    rmm.rmm_select(e, kq, L.qidx)
+    rmm.rmm_reduced_qk(L.Q, L.Kc, L.qidx.view(1, a.H, kq), L.S, causal=True)
+
+
+def time_ratio(L, r, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        run_step(L, r)
+    torch.cuda.synchronize()
+    events = []
+    t0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        run_step(L, r, gemm_events=events)
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / steps
+    gemm_ms = sum(a.elapsed_time(b) for a, b, _ in events)
+    gemm_flop = sum(f for _, _, f in events)
+    proj, qk = flops(L.wk, r)
+    return {
+        "r": r, "ms_per_step": ms, "wall_s": wall,
+        "tflops": (proj + qk) / (ms * 1e-3) / 1e12,
+        "retained_gflop": (proj + qk) / 1e9,
+        "gemm_launches": len(events), "gemm_ms_total": gemm_ms,
+        "gemm_tflops": gemm_flop / (gemm_ms * 1e-3) / 1e12,
+        "gemm_avg_us": gemm_ms * 1e3 / max(len(events), 1),
+        "gemm_avg_gflop": gemm_flop / max(len(events), 1) / 1e9,
+    }
+
+
+# ---------------------------------------------------------- CPU baseline
+
+def cpu_baseline(wk, tokens, r):
+    """The CPU oracle on the first `tokens` tokens of the same workload."""
+    import oracle.rmm_oracle as ro
+    import workloads as wl
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:                                  # threadpoolctl missing
+        blas_threads = os.cpu_count() or 1
+    X = {n: wl.decode(wl.f32_to_bf16_bits(wl.workload_input(wk, n, M=tokens)), "bf16")
+         for n in wk.inputs}
+    W = {p.name: wl.decode(wl.f32_to_bf16_bits(wl.workload_weight(wk, p)), "bf16")
+         for p in wk.projections}
+    q, k = wl.workload_qk(wk, L=tokens)
+    Q = wl.decode(wl.f32_to_bf16_bits(q), "bf16")
+    Kc = wl.decode(wl.f32_to_bf16_bits(k), "bf16")
+    a = wk.attention
+    flop = 0
+    t0 = time.perf_counter()
+    for p in wk.projections:
+        Y, idx, _ = ro.rmm(X[p.input_name], W[p.name], r)
+        flop += 2 * tokens * p.N * len(idx)
+    H, Hkv = a.H, a.Hkv
+    S, qidx, _ = ro.rmm_qk(Q, Kc, r, True)
+    flop += 2 * H * (tokens * (tokens + 1) // 2) * qidx.shape[1]
+    dt = time.perf_counter() - t0
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(blas_threads),
+            "kind": "oracle",
+            "sample": (f"first {tokens} of {wk.M} tokens of the same layer (all 7 projections "
+                       f"+ per-head QK^T, r={r}); {flop / 1e9:.1f} retained GFLOP in {dt:.1f} s; "
+                       f"float64, BLAS threads={blas_threads}, host cpus={os.cpu_count()}")}
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_13426_amd  # noqa: F401  (fails loudly without librmm.so)
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    wk = wl.WORKLOADS[args.workload]
+    ratios = [float(x) for x in args.ratios.split(",")]
+    if HEADLINE_R not in ratios:
+        ratios.append(HEADLINE_R)
+    t_gen = time.perf_counter()
+    L = Layer(wk, dev)
+    torch.cuda.synchronize()
+    print(f"# inputs resident in HBM ({time.perf_counter() - t_gen:.1f} s)", file=sys.stderr,
+          flush=True)
+    sweep = {}
+    for r in ratios:
+        sweep[r] = time_ratio(L, r, args.steps, args.warmup)
+        print(f"# r={r}: {sweep[r]['ms_per_step']:.3f} ms/step, "
+              f"{sweep[r]['tflops']:.1f} TFLOP/s, GEMM {sweep[r]['gemm_tflops']:.1f} TFLOP/s",
+              file=sys.stderr, flush=True)
+    head = sweep[HEADLINE_R]
+    base = sweep.get(1.0)
+    for r, rec in sweep.items():
+        rec["speedup_vs_r1"] = (base["ms_per_step"] / rec["ms_per_step"]) if base else None
+    roof_ach = head["gemm_tflops"]
+    out = {
+        "metric": METRIC,
+        "value": round(head["tflops"], 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wk.name}: {wk.description}", "seq_len": wk.M, "batch": 1,
+                   "r": HEADLINE_R, "projections": [p.name for p in wk.projections],
+                   "attention": "per-head reduced QK^T, causal, 32 q / 8 kv heads, d=128"},
+        "speedup_vs_r1": round(head["speedup_vs_r1"], 3) if base else None,
+        "sweep": {str(r): {k: (round(v, 4) if isinstance(v, float) else v)
+                           for k, v in rec.items()} for r, rec in sweep.items()},
+        "roofline": {"bound": "mfma", "kernel": "gemm_gather_bf16_kernel",
+                     "achieved": round(roof_ach, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(roof_ach / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None,
+                     "avg_launch_us": round(head["gemm_avg_us"], 2),
+                     "avg_launch_gflop": round(head["gemm_avg_gflop"], 3)},
+    }
+    if not args.no_cpu_baseline:
+        print(f"# CPU oracle on {args.cpu_tokens} tokens ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wk, args.cpu_tokens, HEADLINE_R)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -206,9 +206,8 @@ def test_reduced_gemm_strided_operands():
 ])
 def test_reduced_qk(dtype, batch, H, Hkv, Lq, Lk, D, r, causal, seed):
     dev = require_gpu()
-    rng = wl.rng_for(seed, 300)
-    Qf = wl.heavy_tailed_heads(rng, batch * H, Lq, D)
-    Kf = wl.heavy_tailed_heads(rng, batch * Hkv, Lk, D)
+    Qf = wl.heavy_tailed_heads((seed, 300), batch * H, Lq, D)
+    Kf = wl.heavy_tailed_heads((seed, 301), batch * Hkv, Lk, D)
     Qs, Ks = wl.encode(Qf, dtype), wl.encode(Kf, dtype)
     Q = wl.decode(Qs, dtype).astype(np.float64).reshape(batch, H, Lq, D)
     Kv = wl.decode(Ks, dtype).astype(np.float64).reshape(batch, Hkv, Lk, D)

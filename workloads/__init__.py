@@ -22,7 +22,10 @@ samples by round-to-nearest-even.
 """
 from __future__ import annotations
 
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
+import os
+
 import numpy as np
 
 __all__ = [
@@ -30,6 +33,9 @@ __all__ = [
     "Workload", "WORKLOADS", "rng_for", "activation", "weight",
     "heavy_tailed_heads", "outlier_heads", "encode", "decode",
 ]
+
+
+_POOL = ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1))
 
 
 # ---------------------------------------------------------------------------
@@ -42,12 +48,22 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     NaN inputs map to a quiet NaN; infinities stay infinities.
     """
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    out = rounded.astype(np.uint16)
-    nan = np.isnan(x)
-    if nan.any():
-        out[nan] = ((u[nan] >> 16) | 0x0040).astype(np.uint16)
+    out = np.empty(x.shape, dtype=np.uint16)
+    xf, of = x.reshape(-1), out.reshape(-1)
+
+    def part(lo_hi):
+        lo, hi = lo_hi
+        u = xf[lo:hi].view(np.uint32)
+        # no uint32 overflow: the largest non-NaN pattern is -inf (0xff800000)
+        r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+        o = r.astype(np.uint16)
+        nan = np.isnan(xf[lo:hi])
+        if nan.any():
+            o[nan] = ((u[nan] >> np.uint32(16)) | np.uint32(0x0040)).astype(np.uint16)
+        of[lo:hi] = o
+
+    n, step = xf.shape[0], 1 << 22
+    list(_POOL.map(part, [(i, min(n, i + step)) for i in range(0, n, step)]))
     return out
 
 
@@ -84,45 +100,67 @@ def rng_for(seed: int, tensor_id: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64([seed, tensor_id]))
 
 
-def activation(rng: np.random.Generator, shape, n_outlier: int,
-               outlier_scale: float) -> np.ndarray:
-    """N(0,1) activations [..., K] with ``n_outlier`` channels scaled.
+_BLOCK_ROWS = 64
 
-    The outlier channels are the same for every leading index (they are
-    channels of the hidden state, i.e. columns of the activation matrix).
+
+def normal_blocks(key, shape) -> np.ndarray:
+    """N(0,1) float32 array of ``shape`` (at least 2-D: [..., rows, cols]).
+
+    Rows are drawn in fixed blocks of 64, each from its own PCG64 stream
+    keyed by (key, leading index, block), in parallel threads.  A draw with
+    fewer rows is therefore exactly the leading rows of a longer one.
     """
-    x = rng.standard_normal(size=shape, dtype=np.float32)
+    shape = tuple(int(v) for v in shape)
+    out = np.empty(shape, dtype=np.float32)
+    lead, R, C = shape[:-2], shape[-2], shape[-1]
+    jobs = [(li, b) for li in np.ndindex(*lead) for b in range(-(-R // _BLOCK_ROWS))]
+
+    def fill(job):
+        li, b = job
+        r0, r1 = b * _BLOCK_ROWS, min(R, (b + 1) * _BLOCK_ROWS)
+        g = np.random.Generator(np.random.PCG64([*key, *li, b]))
+        out[li + (slice(r0, r1),)] = g.standard_normal(size=(r1 - r0, C), dtype=np.float32)
+
+    list(_POOL.map(fill, jobs))
+    return out
+
+
+def activation(key, shape, n_outlier: int, outlier_scale: float) -> np.ndarray:
+    """N(0,1) activations [..., M, K] with ``n_outlier`` channels scaled.
+
+    ``key`` = (seed, tensor id).  The outlier channels are the same for every
+    row (they are channels of the hidden state, i.e. columns of the
+    activation matrix), chosen from the stream of ``key``.
+    """
     K = shape[-1]
+    x = normal_blocks(key, shape)
     if n_outlier > 0:
-        cols = rng.choice(K, size=n_outlier, replace=False)
+        cols = rng_for(*key).choice(K, size=n_outlier, replace=False)
         x[..., cols] *= np.float32(outlier_scale)
     return x
 
 
-def weight(rng: np.random.Generator, K: int, N: int, std: float = 0.02) -> np.ndarray:
+def weight(key, K: int, N: int, std: float = 0.02) -> np.ndarray:
     """Weights [K x N] ~ N(0, std^2) (row k = contraction index k)."""
-    w = rng.standard_normal(size=(K, N), dtype=np.float32)
+    w = normal_blocks(key, (K, N))
     w *= np.float32(std)
     return w
 
 
-def heavy_tailed_heads(rng: np.random.Generator, H: int, L: int, D: int,
-                       nu: float = 3.0) -> np.ndarray:
+def heavy_tailed_heads(key, H: int, L: int, D: int, nu: float = 3.0) -> np.ndarray:
     """[H x L x D]: entry c[h,j]*z, z ~ N(0,1), c[h,j] = |Student-t(nu)|."""
-    c = np.abs(rng.standard_t(nu, size=(H, 1, D))).astype(np.float32)
-    z = rng.standard_normal(size=(H, L, D), dtype=np.float32)
+    c = np.abs(rng_for(*key).standard_t(nu, size=(H, 1, D))).astype(np.float32)
+    z = normal_blocks(key, (H, L, D))
     z *= c
     return z
 
 
-def outlier_heads(rng: np.random.Generator, H: int, L: int, D: int,
-                  frac: float, scale: float) -> np.ndarray:
+def outlier_heads(key, H: int, L: int, D: int, frac: float, scale: float) -> np.ndarray:
     """[H x L x D] N(0,1) with ``round(frac*H*D)`` of the H*D channels scaled."""
-    z = rng.standard_normal(size=(H, L, D), dtype=np.float32)
+    z = normal_blocks(key, (H, L, D))
     n_out = int(round(frac * H * D))
     if n_out > 0:
-        ch = rng.choice(H * D, size=n_out, replace=False)
-        for c in ch:
+        for c in rng_for(*key).choice(H * D, size=n_out, replace=False):
             z[c // D, :, c % D] *= np.float32(scale)
     return z
 
@@ -228,32 +266,31 @@ def workload_input(wl: Workload, name: str, M: int | None = None) -> np.ndarray:
     same draw's distribution (a fresh draw of M rows from the same stream).
     """
     K, n_out, scale = wl.inputs[name]
-    rng = rng_for(wl.seed, _INPUT_IDS[name])
-    return activation(rng, (wl.M if M is None else M, K), n_out, scale)
+    return activation((wl.seed, _INPUT_IDS[name]), (wl.M if M is None else M, K), n_out, scale)
 
 
 def workload_weight(wl: Workload, proj: Projection) -> np.ndarray:
-    rng = rng_for(wl.seed, _WEIGHT_IDS[proj.name])
-    return weight(rng, proj.K, proj.N)
+    return weight((wl.seed, _WEIGHT_IDS[proj.name]), proj.K, proj.N)
 
 
 def workload_qk(wl: Workload, L: int | None = None):
     """fp32 samples of (Q [H x L x D], K [Hkv x L x D])."""
     a = wl.attention
     L = a.L if L is None else L
-    rq, rk = rng_for(wl.seed, 200), rng_for(wl.seed, 201)
+    kq, kk = (wl.seed, 200), (wl.seed, 201)
     if a.recipe == "heavy_tailed":
-        return (heavy_tailed_heads(rq, a.H, L, a.D),
-                heavy_tailed_heads(rk, a.Hkv, L, a.D))
-    return (outlier_heads(rq, a.H, L, a.D, 0.01, 20.0),
-            outlier_heads(rk, a.Hkv, L, a.D, 0.01, 20.0))
+        return (heavy_tailed_heads(kq, a.H, L, a.D),
+                heavy_tailed_heads(kk, a.Hkv, L, a.D))
+    return (outlier_heads(kq, a.H, L, a.D, 0.01, 20.0),
+            outlier_heads(kk, a.Hkv, L, a.D, 0.01, 20.0))
 
 
 def random_case(seed: int, shape, dtype: str, n_outlier: int = 0,
                 outlier_scale: float = 10.0, std: float = 1.0) -> np.ndarray:
     """Stored bytes of a generic random tensor for parity/edge-case tests."""
-    rng = rng_for(seed, 1000 + len(shape))
-    x = activation(rng, tuple(shape), n_outlier, outlier_scale)
+    shape = tuple(shape)
+    x = activation((seed, 1000 + len(shape)), shape if len(shape) > 1 else (1,) + shape,
+                   n_outlier, outlier_scale).reshape(shape)
     if std != 1.0:
         x *= np.float32(std)
     return encode(x, dtype)
