@@ -171,6 +171,31 @@ def test_reduced_gemm(dtype, B, M, N, K, k, seed):
         check_product(Y[b], ref, absprod, k, dtype)
 
 
+@pytest.mark.parametrize("B,M,N,K,k,ldw_pad,seed", [
+    (1, 2100, 4100, 3000, 1111, 0, 50),     # ragged M, N and k tails in 256x256 tiles
+    (2, 2048, 2048, 4096, 2048, 0, 51),     # two selection units
+    (1, 2048, 4098, 700, 300, 0, 52),       # W rows not 16-byte multiples
+    (1, 4096, 2048, 1024, 1, 0, 53),        # k = 1
+    (1, 2048, 4096, 1024, 1024, 8, 54),     # identity list, padded W rows
+])
+def test_reduced_gemm_large_tiles(B, M, N, K, k, ldw_pad, seed):
+    dev = require_gpu()
+    Xs = wl.random_case(seed, (B, M, K), "bf16", n_outlier=max(1, K // 100))
+    Ws = wl.random_case(seed + 100, (K, N + ldw_pad), "bf16", std=0.02)
+    idx = _ascending(seed, B, K, k)
+    Xd = to_device(Xs, "bf16", dev)
+    Wd = to_device(Ws, "bf16", dev)[:, :N]
+    Yd = torch.empty((B, M, N), dtype=torch.bfloat16, device=dev)
+    rmm.rmm_reduced_gemm(Xd, Wd, torch.from_numpy(idx.astype(np.int32)).to(dev), Yd)
+    Y = from_device(Yd)
+    X = wl.decode(Xs, "bf16").astype(np.float64)
+    W = wl.decode(Ws, "bf16").astype(np.float64)[:, :N]
+    for b in range(B):
+        ref = ro.reduced_matmul(X[b], W, idx[b])
+        absprod = np.abs(X[b][:, idx[b]]) @ np.abs(W[idx[b], :])
+        check_product(Y[b], ref, absprod, k, "bf16")
+
+
 def test_reduced_gemm_strided_operands():
     """Leading dimensions larger than the logical widths."""
     dev = require_gpu()
