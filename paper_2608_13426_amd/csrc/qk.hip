@@ -123,6 +123,192 @@ __global__ __launch_bounds__(WM *WN *kWave) void qk_bf16_kernel(
         }
 }
 
+// ------------------------------------------------------- row-streaming kernel
+// One workgroup per (head, 128-query tile) walks the key tiles of its rows.
+// Q and K rows (D values, 16-byte chunks) are read whole and staged in LDS
+// with an odd row stride of D/2+1 words, so 32 rows read at one column hit
+// 32 distinct banks; the MFMA operands are gathered from the staged rows at
+// the retained dims (a zeroed pad word stands in for padding positions).
+// Q's fragments are gathered once and kept in registers.  The product is
+// formed transposed (keys x queries), so each lane holds 4 consecutive keys
+// of one query; tiles are staged through LDS and written as coalesced
+// 16-byte non-temporal stores.  Key tiles wholly above the diagonal are
+// streamed as -inf.
+namespace rowk {
+constexpr int BQ = 128, BT = 128, NT = 256;
+constexpr int OS = BT + 8;    // staged output row: 272 bytes (16-byte aligned)
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+}  // namespace rowk
+
+template <int D>
+__global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
+    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Kc,
+    const int32_t *__restrict__ idx, uint16_t *__restrict__ S, int H, int Hkv, int Lq, int Lk,
+    int k, float scale, int causal) {
+    using namespace rowk;
+    constexpr int RW = D / 2 + 1;          // words per staged row (odd)
+    constexpr int CH = D / 8;              // 16-byte chunks per row
+    constexpr int PER_T = BT * CH / NT;    // chunks staged per thread
+    constexpr int KSMAX = D / 16;
+    static_assert(D % 16 == 0 && BQ == BT && (BT * CH) % NT == 0, "shape");
+
+    __shared__ uint32_t rows_lds[BT * RW];
+    __shared__ __attribute__((aligned(16))) uint16_t out_lds[BQ * OS];
+    __shared__ __attribute__((aligned(16))) uint16_t col_off[D + 16];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bh = blockIdx.y, b = bh / H, h = bh % H, g = h / (H / Hkv);
+    const int q0 = blockIdx.x * BQ;
+    const int off = Lk - Lq;
+    const int32_t *I = idx + static_cast<int64_t>(bh) * k;
+    uint16_t *Sh = S + static_cast<int64_t>(bh) * Lq * Lk;
+    const int n_tiles = (Lk + BT - 1) / BT;
+    int n_compute = n_tiles;
+    if (causal) {
+        const int limit = min(q0 + BQ, Lq) - 1 + off;   // largest key any row keeps
+        n_compute = limit < 0 ? 0 : min(n_tiles, limit / BT + 1);
+    }
+    const int r16 = tid >> 4, c16 = tid & 15;           // store role: rows r16 + 16i, chunk c16
+
+    if (n_compute > 0) {
+        const int kp = (k + 15) & ~15;
+        const int KS = kp / 16;
+        for (int t = tid; t < D + 16; t += NT) col_off[t] = static_cast<uint16_t>((t < k ? I[t] : D) * 2);
+        for (int r = tid; r < BT; r += NT) rows_lds[r * RW + D / 2] = 0u;
+
+        const __amdgpu_buffer_rsrc_t qr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(Q + (static_cast<int64_t>(bh) * Lq + q0) * D), 0,
+            static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
+        const uint16_t *Kh = Kc + (static_cast<int64_t>(b) * Hkv + g) * Lk * D;
+
+        uint4 regs[PER_T];
+        auto load_rows = [&](__amdgpu_buffer_rsrc_t rs) {
+#pragma unroll
+            for (int i = 0; i < PER_T; ++i) {
+                const int v = tid + NT * i;
+                const auto x = __builtin_amdgcn_raw_buffer_load_b128(
+                    rs, static_cast<uint32_t>(((v / CH) * D + (v % CH) * 8) * 2), 0, 0);
+                regs[i] = make_uint4(x[0], x[1], x[2], x[3]);
+            }
+        };
+        auto store_rows = [&]() {
+#pragma unroll
+            for (int i = 0; i < PER_T; ++i) {
+                const int v = tid + NT * i;
+                uint32_t *dst = rows_lds + (v / CH) * RW + (v % CH) * 4;
+                dst[0] = regs[i].x; dst[1] = regs[i].y; dst[2] = regs[i].z; dst[3] = regs[i].w;
+            }
+        };
+        auto key_rsrc = [&](int kt) {
+            const int t0 = kt * BT;
+            return __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<uint16_t *>(Kh + static_cast<int64_t>(t0) * D), 0,
+                static_cast<uint32_t>(min(BT, Lk - t0) * D * 2), 0x00020000);
+        };
+        // 8 retained dims (k-step ks, lane half) of staged row `row`
+        auto frag = [&](int row, int ks) -> bf16x8_t {
+            const uint4 co = *reinterpret_cast<const uint4 *>(&col_off[ks * 16 + 8 * (lane >> 5)]);
+            const char *base = reinterpret_cast<const char *>(rows_lds + row * RW);
+            const uint32_t o[4] = {co.x, co.y, co.z, co.w};
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t lo = *reinterpret_cast<const uint16_t *>(base + (o[q] & 0xffffu));
+                const uint32_t hi = *reinterpret_cast<const uint16_t *>(base + (o[q] >> 16));
+                w[q] = lo | (hi << 16);
+            }
+            return __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+        };
+
+        const int wk = wave >> 1, wq = wave & 1;     // wave: 64 keys x 64 queries
+        const int lr = lane & 31, lh = lane >> 5;
+
+        load_rows(qr);
+        store_rows();
+        __syncthreads();
+        bf16x8_t qf[2][KSMAX];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int ks = 0; ks < KSMAX; ++ks)
+                if (ks < KS) qf[j][ks] = frag(wq * 64 + j * 32 + lr, ks);
+        load_rows(key_rsrc(0));
+        __syncthreads();
+        store_rows();
+        __syncthreads();
+
+        for (int kt = 0; kt < n_compute; ++kt) {
+            if (kt + 1 < n_compute) load_rows(key_rsrc(kt + 1));
+            f32x16_t acc[2][2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KSMAX; ++ks) {
+                if (ks < KS) {
+                    const bf16x8_t kf0 = frag(wk * 64 + lr, ks);
+                    const bf16x8_t kf1 = frag(wk * 64 + 32 + lr, ks);
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) {
+                        acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[j][ks], acc[0][j], 0, 0, 0);
+                        acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[j][ks], acc[1][j], 0, 0, 0);
+                    }
+                }
+            }
+            // acc[i][j][4*gq + r]: key wk*64 + i*32 + 8*gq + 4*lh + r, query wq*64 + j*32 + lr
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const int ql = wq * 64 + j * 32 + lr;
+                    const int qg = q0 + ql;
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        const int kl = wk * 64 + i * 32 + 8 * gq + 4 * lh;
+                        const int kg = kt * BT + kl;
+                        uint16_t o4[4];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const bool masked = causal && (kg + r > qg + off);
+                            o4[r] = masked ? kBf16NegInf : f32_to_bf16(acc[i][j][4 * gq + r] * scale);
+                        }
+                        *reinterpret_cast<uint2 *>(&out_lds[ql * OS + kl]) =
+                            make_uint2(o4[0] | (static_cast<uint32_t>(o4[1]) << 16),
+                                       o4[2] | (static_cast<uint32_t>(o4[3]) << 16));
+                    }
+                }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < BQ / 16; ++i) {
+                const int r = r16 + 16 * i;
+                const int col = kt * BT + c16 * 8;
+                if (q0 + r < Lq && col < Lk) {
+                    const uint4 v = *reinterpret_cast<const uint4 *>(&out_lds[r * OS + c16 * 8]);
+                    __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w},
+                        reinterpret_cast<u32x4_t *>(Sh + static_cast<int64_t>(q0 + r) * Lk + col));
+                }
+            }
+            if (kt + 1 < n_compute) store_rows();
+            __syncthreads();
+        }
+    }
+    // key tiles wholly above the diagonal
+    const uint32_t ninf2 = 0xff80ff80u;
+    for (int kt = n_compute; kt < n_tiles; ++kt) {
+#pragma unroll
+        for (int i = 0; i < BQ / 16; ++i) {
+            const int r = r16 + 16 * i;
+            const int col = kt * BT + c16 * 8;
+            if (q0 + r < Lq && col < Lk)
+                __builtin_nontemporal_store(u32x4_t{ninf2, ninf2, ninf2, ninf2},
+                    reinterpret_cast<u32x4_t *>(Sh + static_cast<int64_t>(q0 + r) * Lk + col));
+        }
+    }
+}
+
 template <int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void qk_f32_kernel(
     const float *__restrict__ Q, const float *__restrict__ Kc, const int32_t *__restrict__ idx,
@@ -190,6 +376,21 @@ hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *
                           int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
                           int64_t D, int64_t k, float scale, bool causal, uint16_t *S,
                           hipStream_t stream) {
+    const bool rows_ok = (D == 64 || D == 128) && Lk % 8 == 0 &&
+                         reinterpret_cast<uintptr_t>(S) % 16 == 0;
+    if (rows_ok) {
+        dim3 grid(static_cast<unsigned>((Lq + rowk::BQ - 1) / rowk::BQ),
+                  static_cast<unsigned>(batch * H));
+        if (D == 128)
+            hipLaunchKernelGGL(qk_bf16_rows_kernel<128>, grid, dim3(rowk::NT), 0, stream, Q, Kc, idx,
+                               S, static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
+                               static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
+        else
+            hipLaunchKernelGGL(qk_bf16_rows_kernel<64>, grid, dim3(rowk::NT), 0, stream, Q, Kc, idx,
+                               S, static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
+                               static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
+        return hipGetLastError();
+    }
     constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2;
     dim3 grid(static_cast<unsigned>((Lk + BN - 1) / BN), static_cast<unsigned>((Lq + BM - 1) / BM),
               static_cast<unsigned>(batch * H));
