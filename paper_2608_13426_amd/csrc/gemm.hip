@@ -145,24 +145,32 @@ __global__ __launch_bounds__(WM *WN *kWave) void gemm_gather_bf16_kernel(
 }
 
 // ------------------------------------------------------ bf16, large tiles
-// 256x256 output tile, 64 retained indices per k-tile, 4 waves of 128x128
-// (16 MFMAs per 16-deep k-step per wave), LDS double-buffered (128 KB).
-// Each LDS row holds the 64 k-values of one output row (A) or column (B)
-// as eight 16-byte chunks; chunk c of row r is stored at c ^ swz(r), which
-// spreads the operand reads of 8 consecutive rows, the gathered-X writes
-// and the transposed-W writes of rows 8 apart over distinct bank groups.
+// 256x256 output tile, 64 retained indices per k-tile, NW waves in a 2 x NW/2
+// grid (each wave 128 x 512/NW), LDS double-buffered (128 KB).  Each LDS row
+// holds the 64 k-values of one output row (A) or column (B) as eight 16-byte
+// chunks; chunk c of row r is stored at c ^ swz(r), which spreads the operand
+// reads of 8 consecutive rows, the gathered-X writes and the transposed-W
+// writes of rows 8 apart over distinct bank groups.
 namespace big {
-constexpr int BM = 256, BN = 256, BK = 64, NT = 256;
+constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int GROUP_M = 4;
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int at(int row, int chunk) { return row * BK + ((chunk ^ swz(row)) << 3); }
 }  // namespace big
 
-__global__ __launch_bounds__(big::NT, 1) void gemm_gather_bf16_big_kernel(
+template <int NW>
+__global__ __launch_bounds__(NW * 64, NW / 4) void gemm_gather_bf16_big_kernel(
     const uint16_t *__restrict__ X, const uint16_t *__restrict__ W,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int k,
     int64_t ldx, int64_t ldw, int64_t ldy, int64_t w_bytes, int tiles_m, int tiles_n) {
     using namespace big;
+    constexpr int NT = NW * 64;
+    constexpr int WN = NW / 2;            // waves along N (2 along M)
+    constexpr int TN = BN / WN;           // wave tile: 128 x TN
+    constexpr int FN = TN / 32;
+    constexpr int XR = BM / (2 * NW);     // X rows gathered per thread (pairs)
+    constexpr int WR = BK * BN / 8 / NT;  // W rows per thread block (8 columns wide)
+    static_assert(WR == 4 || WR == 8, "W block");
     __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (BM + BN) * BK];
     // buffer b: A tile at lds + b*BM*BK, B tile at lds + 2*BM*BK + b*BN*BK
 
@@ -183,13 +191,13 @@ __global__ __launch_bounds__(big::NT, 1) void gemm_gather_bf16_big_kernel(
     idx += unit * k;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // X gather: lane pair p takes retained positions 2p, 2p+1 of rows ra + 8i
+    // X gather: lane pair p takes retained positions 2p, 2p+1 of rows ra + 2*NW*i
     const int p = lane & 31, ra = wave * 2 + (lane >> 5);
-    // W gather: an 8 x 8 block, rows 8*t8.. of the k-tile, columns 8*c..
-    const int t8 = tid >> 5, c = tid & 31;
+    // W gather: a WR x 8 block, rows WR*tq.. of the k-tile, columns 8*c..
+    const int tq = tid >> 5, c = tid & 31;
 
-    uint32_t xlo[BM / 8], xhi[BM / 8];
-    uint4 wv[8];
+    uint32_t xlo[XR], xhi[XR];
+    uint4 wv[WR];
 
     // Branch-free gathers through buffer descriptors: a lane whose retained
     // position is past k, or whose row is past M, reads at an offset beyond
@@ -211,64 +219,68 @@ __global__ __launch_bounds__(big::NT, 1) void gemm_gather_bf16_big_kernel(
 
     // Index values are fetched one k-tile ahead of the gathers that use them
     // (raw[]), then turned into byte offsets (off[]) once they have landed.
-    uint32_t raw[10], off[10];
+    uint32_t raw[2 + WR], off[2 + WR];
     auto fetch_idx = [&](int t0) {
         raw[0] = __builtin_amdgcn_raw_buffer_load_b32(ir, static_cast<uint32_t>(t0 + 2 * p) * 4u, 0, 0);
         raw[1] = __builtin_amdgcn_raw_buffer_load_b32(ir, static_cast<uint32_t>(t0 + 2 * p + 1) * 4u, 0, 0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < WR; ++i)
             raw[2 + i] = __builtin_amdgcn_raw_buffer_load_b32(
-                ir, static_cast<uint32_t>(t0 + 8 * t8 + i) * 4u, 0, 0);
+                ir, static_cast<uint32_t>(t0 + WR * tq + i) * 4u, 0, 0);
     };
     auto make_offsets = [&](int t0) {
         off[0] = t0 + 2 * p < k ? raw[0] * 2u : kOut;
         off[1] = t0 + 2 * p + 1 < k ? raw[1] * 2u : kOut;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) off[2 + i] = t0 + 8 * t8 + i < k ? raw[2 + i] * wrow + wcol : kOut;
+        for (int i = 0; i < WR; ++i) off[2 + i] = t0 + WR * tq + i < k ? raw[2 + i] * wrow + wcol : kOut;
     };
     auto gather = [&]() {
 #pragma unroll
-        for (int i = 0; i < BM / 8; ++i) {
-            const uint32_t row = xlane + static_cast<uint32_t>(8 * i) * xrow;
+        for (int i = 0; i < XR; ++i) {
+            const uint32_t row = xlane + static_cast<uint32_t>(2 * NW * i) * xrow;
             // packed into pairs only at stash time, so no wait sits between loads
             xlo[i] = __builtin_amdgcn_raw_buffer_load_b16(xr, row + off[0], 0, 0);
             xhi[i] = __builtin_amdgcn_raw_buffer_load_b16(xr, row + off[1], 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < WR; ++i) {
             const auto v = __builtin_amdgcn_raw_buffer_load_b128(wr, off[2 + i], 0, 0);
             wv[i] = make_uint4(v[0], v[1], v[2], v[3]);
         }
     };
     auto stash = [&](uint16_t *as, uint16_t *bs) {
 #pragma unroll
-        for (int i = 0; i < BM / 8; ++i) {
-            const int row = ra + 8 * i;
+        for (int i = 0; i < XR; ++i) {
+            const int row = ra + 2 * NW * i;
             *reinterpret_cast<uint32_t *>(&as[at(row, p >> 2) + 2 * (p & 3)]) = xlo[i] | (xhi[i] << 16);
         }
-        // 8x8 transpose: column jj of the block becomes 8 consecutive k of B row n
+        // WR x 8 transpose: column jj of the block becomes WR consecutive k of B row n
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
-            uint32_t d[4];
+            uint32_t d[WR / 2];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
+            for (int q = 0; q < WR / 2; ++q) {
                 const uint32_t a = reinterpret_cast<const uint32_t *>(&wv[2 * q])[jj >> 1];
                 const uint32_t b = reinterpret_cast<const uint32_t *>(&wv[2 * q + 1])[jj >> 1];
                 d[q] = (jj & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
             }
-            *reinterpret_cast<uint4 *>(&bs[at(8 * c + jj, t8)]) = make_uint4(d[0], d[1], d[2], d[3]);
+            if constexpr (WR == 8) {
+                *reinterpret_cast<uint4 *>(&bs[at(8 * c + jj, tq)]) = make_uint4(d[0], d[1], d[2], d[3]);
+            } else {
+                *reinterpret_cast<uint2 *>(&bs[at(8 * c + jj, tq >> 1) + 4 * (tq & 1)]) = make_uint2(d[0], d[1]);
+            }
         }
     };
 
-    f32x16_t acc[4][4];
+    f32x16_t acc[4][FN];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int lr = lane & 31, lh = lane >> 5;
     const int nT = (k + BK - 1) / BK;
     fetch_idx(0);
@@ -287,17 +299,17 @@ __global__ __launch_bounds__(big::NT, 1) void gemm_gather_bf16_big_kernel(
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             const int chunk = 2 * ks + lh;
-            bf16x8_t a[4], b[4];
+            bf16x8_t a[4], b[FN];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 a[i] = *reinterpret_cast<const bf16x8_t *>(&as[at(wm * 128 + i * 32 + lr, chunk)]);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                b[j] = *reinterpret_cast<const bf16x8_t *>(&bs[at(wn * 128 + j * 32 + lr, chunk)]);
+            for (int j = 0; j < FN; ++j)
+                b[j] = *reinterpret_cast<const bf16x8_t *>(&bs[at(wn * TN + j * 32 + lr, chunk)]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         if (t + 1 < nT) stash(lds + (cur ^ 1) * BM * BK, lds + 2 * BM * BK + (cur ^ 1) * BN * BK);
@@ -308,8 +320,8 @@ __global__ __launch_bounds__(big::NT, 1) void gemm_gather_bf16_big_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = n0 + wn * 128 + j * 32 + lr;
+        for (int j = 0; j < FN; ++j) {
+            const int n = n0 + wn * TN + j * 32 + lr;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int m = m0 + wm * 128 + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
@@ -378,6 +390,8 @@ __global__ __launch_bounds__(256) void gemm_gather_f32_kernel(
 
 }  // namespace
 
+constexpr int kBigWaves = 4;
+
 hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx,
                             int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                             int64_t ldx, int64_t ldw, uint16_t *Y, int64_t ldy,
@@ -392,9 +406,9 @@ hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t 
         const int tm = static_cast<int>((M + big::BM - 1) / big::BM);
         const int tn = static_cast<int>((N + big::BN - 1) / big::BN);
         dim3 grid(static_cast<unsigned>(tm * tn), static_cast<unsigned>(B));
-        hipLaunchKernelGGL(gemm_gather_bf16_big_kernel, grid, dim3(big::NT), 0, stream, X, W, idx, Y,
-                           static_cast<int>(M), static_cast<int>(N), static_cast<int>(k), ldx, ldw,
-                           ldy, w_bytes, tm, tn);
+        hipLaunchKernelGGL(gemm_gather_bf16_big_kernel<kBigWaves>, grid, dim3(kBigWaves * 64), 0,
+                           stream, X, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
+                           static_cast<int>(k), ldx, ldw, ldy, w_bytes, tm, tn);
         return hipGetLastError();
     }
     constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2;
