@@ -4,8 +4,9 @@ One step = one pass of the whole reduced path of an 8B-class decoder layer
 (seq 8192, hidden 4096, 32 query / 8 kv heads of dim 128, MLP 14336) at
 retention ratio r, on synthetic bf16 inputs already resident in HBM:
 
-  * q/k/v  : energies of the attention input, TopK, three gathered GEMMs
-             (the three projections read one input, so they share one set)
+  * q/k/v  : energies of the attention input (the scoring pass also writes
+             its K-major copy), TopK, three gathered GEMMs (the three
+             projections read one input, so they share one set)
   * o      : energies, TopK, gathered GEMM
   * gate/up: energies of the MLP input, TopK, two gathered GEMMs
   * down   : energies, TopK, gathered GEMM
@@ -67,6 +68,9 @@ class Layer:
             return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
 
         self.X = {name: put(wl.workload_input(wk, name)) for name in wk.inputs}
+        # K-major copies written by the scoring pass
+        self.Xt = {name: torch.empty((v[0], self.M), dtype=torch.bfloat16, device=dev)
+                   for name, v in wk.inputs.items()}
         self.W = {p.name: put(wl.workload_weight(wk, p)) for p in wk.projections}
         self.Y = {p.name: torch.empty((self.M, p.N), dtype=torch.bfloat16, device=dev)
                   for p in wk.projections}
@@ -109,7 +113,7 @@ def run_step(L, r, gemm_events=None):
         k = rmm.rmm_retained_count(r, K)
         X = L.X[name]
         e = L.energy[:K]
-        rmm.rmm_score(X, e, L.ws)
+        rmm.rmm_score_kmajor(X, e, L.Xt[name], L.ws)
         if L.idx[name] is None or L.idx[name].numel() != k:
             L.idx[name] = torch.empty(k, dtype=torch.int32, device=L.dev)
         rmm.rmm_select(e, k, L.idx[name])
@@ -117,7 +121,8 @@ def run_step(L, r, gemm_events=None):
             if gemm_events is not None:
                 ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 ev0.record()
-            rmm.rmm_reduced_gemm(X, L.W[p.name], L.idx[name].view(1, k), L.Y[p.name])
+            rmm.rmm_reduced_gemm_kmajor(L.Xt[name], L.W[p.name], L.idx[name].view(1, k),
+                                        L.Y[p.name])
             if gemm_events is not None:
                 ev1.record()
                 gemm_events.append((ev0, ev1, 2 * wk.M * p.N * k))
@@ -247,7 +252,7 @@ def main():
         "speedup_vs_r1": round(head["speedup_vs_r1"], 3) if base else None,
         "sweep": {str(r): {k: (round(v, 4) if isinstance(v, float) else v)
                            for k, v in rec.items()} for r, rec in sweep.items()},
-        "roofline": {"bound": "mfma", "kernel": "gemm_gather_bf16_kernel",
+        "roofline": {"bound": "mfma", "kernel": "gemm_kmajor_bf16_kernel",
                      "achieved": round(roof_ach, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(roof_ach / PEAK_BF16_TFLOPS, 4),
                      "traffic": None,

@@ -74,7 +74,8 @@ int64_t rmm_retained_count(double r, int64_t K);
  * Bytes of workspace a call needs (0 if none).  Arguments as in the call:
  *   RMM_OP_SCORE : B, M, K        (k ignored)
  *   RMM_OP_SELECT: always 0
- *   RMM_OP_LINEAR: B, M, K, k     (k = rmm_retained_count(r, K))
+ *   RMM_OP_LINEAR: B, M, K, k     (k = rmm_retained_count(r, K); includes
+ *                  room for the K-major copy of X, B*K*round_up(M, 8) bf16)
  * Returns 0 for non-positive sizes.  Host-only.
  */
 size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t k);
@@ -100,6 +101,25 @@ size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t 
 rmm_status_t rmm_score(const void *X, rmm_dtype_t dtype, int64_t B, int64_t M,
                        int64_t K, int64_t ldx, double *energy,
                        void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Column energies plus a K-major copy of the activations   (Sec. 3.2 score;
+ * the copy feeds rmm_reduced_gemm_kmajor).
+ *
+ * Computes exactly what rmm_score computes for bf16 (bit-identical energies)
+ * and, in the same pass over X, writes Xt[b][j][m] = X[b][m][j]: unit b's
+ * K x M transpose, row stride ldxt (ldxt >= M).  A retained index j is then
+ * one contiguous row of Xt.  bf16 only.
+ *
+ * X        : [B][M][ldx] bf16, 16-byte aligned, ldx % 8 == 0.
+ * Xt       : [B][K][ldxt] bf16, written; 16-byte aligned, ldxt % 8 == 0.
+ * energy, workspace: as rmm_score (same workspace size).
+ * Errors   : as rmm_score; INVALID_ARGUMENT for a null Xt or ldxt < M;
+ *            UNSUPPORTED for misaligned X/Xt or ldx, ldxt not multiples of 8.
+ */
+rmm_status_t rmm_score_kmajor(const void *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                              double *energy, void *Xt, int64_t ldxt,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * TopK selection   (Sec. 3.2: I = TopK({s_j}, ceil(rho d))).
@@ -142,6 +162,27 @@ rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx,
                               void *Y, int64_t ldy, hipStream_t stream);
 
 /*
+ * Gathered reduced product from K-major activations   (Sec. 3.2 definition
+ * of RMM; Sec. 3.3 projections) -- the same Y as rmm_reduced_gemm, reading
+ * X[:, I] as rows I of Xt (the copy written by rmm_score_kmajor).
+ *
+ *   Y[b][m][n] = sum_{t < k} Xt[b][idx[b*k + t]][m] * W[idx[b*k + t]][n]
+ *
+ * Xt  : [B][K][ldxt] bf16, ldxt >= M.     W : [K][ldw] bf16, ldw >= N.
+ * idx : int32 [B*k], ascending per unit, values in [0, K).
+ * Y   : [B][M][ldy] bf16, ldy >= N, written.
+ * Retained rows of Xt and W are read as 16-byte vectors and staged through
+ * LDS; no compacted operand is written to memory.  bf16 only.
+ * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, k outside [1, K],
+ *         ld too small; UNSUPPORTED for Xt/W not 16-byte aligned, ldxt or ldw
+ *         not multiples of 8, or K*ldxt or K*ldw of 2^30 elements or more.
+ */
+rmm_status_t rmm_reduced_gemm_kmajor(const void *Xt, const void *W, const int32_t *idx,
+                                     int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                                     int64_t ldxt, int64_t ldw, void *Y, int64_t ldy,
+                                     hipStream_t stream);
+
+/*
  * Reduced attention scores over head-dim slices   (Sec. 3.3, Attention:
  * S~ = (1/sqrt(d_h)) Q[:, I] K[:, I]^T, then the optional causal mask M).
  *
@@ -167,9 +208,12 @@ rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx,
 /*
  * Fused RMM projection   (Sec. 3.2 + Sec. 3.3 "MLP and linear projections").
  *
- * k = rmm_retained_count(r, K); then rmm_score -> rmm_select ->
- * rmm_reduced_gemm on `stream`, with no host synchronisation (k depends
- * only on r and K).  Each of the B units selects from its own M rows.
+ * k = rmm_retained_count(r, K); then score -> rmm_select -> gathered GEMM
+ * on `stream`, with no host synchronisation (k depends only on r and K).
+ * Each of the B units selects from its own M rows.  For bf16 with 16-byte
+ * aligned X rows and W (ldx, ldw multiples of 8) the K-major path is taken
+ * (rmm_score_kmajor with the copy in the workspace, then
+ * rmm_reduced_gemm_kmajor); otherwise rmm_score + rmm_reduced_gemm.
  *
  * idx_out   : int32 [B*k] receiving the index sets, or NULL (kept in the
  *             workspace).

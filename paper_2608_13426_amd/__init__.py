@@ -5,7 +5,7 @@ sizes and strides off torch tensors, passes raw device pointers and the
 current HIP stream, and raises ``RmmError`` on a non-zero status.  Every
 step of the computation runs in librmm's gfx950 kernels; torch only owns the
 device memory and the stream.  Importing this package fails loudly when
-``librmm.so`` has not been built (``python -m paper_2608_13426_amd.build``).
+``librmm.so`` has not been built (``python paper_2608_13426_amd/build.py``).
 """
 from __future__ import annotations
 
@@ -18,7 +18,8 @@ __all__ = [
     "RmmError", "LIB_PATH", "lib", "RMM_F32", "RMM_BF16", "RMM_OP_SCORE",
     "RMM_OP_SELECT", "RMM_OP_LINEAR", "rmm_retained_count", "rmm_workspace_size",
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
-    "rmm_reduced_qk", "rmm_linear", "EXPORTED_SYMBOLS",
+    "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
+    "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -41,6 +42,10 @@ _SIGS = {
     "rmm_linear": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
                                   _i64, _i64, _i64, _p, _i64, _p, _p, ctypes.c_size_t, _p]),
     "rmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "rmm_score_kmajor": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _p, _i64, _p,
+                                        ctypes.c_size_t, _p]),
+    "rmm_reduced_gemm_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64,
+                                               _i64, _p, _i64, _p]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -54,7 +59,7 @@ class RmmError(RuntimeError):
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"librmm.so is missing at {LIB_PATH}; build it with "
-                          "`python -m paper_2608_13426_amd.build`")
+                          "`python paper_2608_13426_amd/build.py`")
     handle = ctypes.CDLL(LIB_PATH)
     for name, (res, args) in _SIGS.items():
         fn = getattr(handle, name)
@@ -146,6 +151,23 @@ def rmm_score(X: torch.Tensor, energy: torch.Tensor, workspace: torch.Tensor | N
     return energy
 
 
+def rmm_score_kmajor(X: torch.Tensor, energy: torch.Tensor, Xt: torch.Tensor,
+                     workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Energies of each unit of bf16 X [B, M, K] plus its K-major copy Xt [B, K, ldxt]."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, energy, Xt)
+    if energy.dtype != torch.float64 or energy.numel() != B * K or not energy.is_contiguous():
+        raise ValueError("energy must be a contiguous float64 tensor of B*K elements")
+    Bt, Kt, Mt, ldxt = _rows(Xt, "Xt")
+    if (Bt, Kt, Mt) != (B, K, M) or Xt.dtype != X.dtype:
+        raise ValueError("Xt must be [B, K, M] (a view with row stride ldxt) of X's dtype")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("rmm_score_kmajor", lib.rmm_score_kmajor(
+        X.data_ptr(), B, M, K, ldx, energy.data_ptr(), Xt.data_ptr(), ldxt, _ptr(workspace),
+        ws_bytes, _stream(d, stream)))
+    return energy
+
+
 def rmm_select(energy: torch.Tensor, k: int, idx: torch.Tensor, stream=None) -> torch.Tensor:
     """TopK (ascending int32 indices) of each unit's energies.
 
@@ -186,6 +208,28 @@ def rmm_reduced_gemm(X: torch.Tensor, W: torch.Tensor, idx: torch.Tensor, Y: tor
     _check("rmm_reduced_gemm", lib.rmm_reduced_gemm(
         X.data_ptr(), W.data_ptr(), idx.data_ptr(), _dtype_code(X), B, M, N, K, k, ldx, ldw,
         Y.data_ptr(), ldy, _stream(d, stream)))
+    return Y
+
+
+def rmm_reduced_gemm_kmajor(Xt: torch.Tensor, W: torch.Tensor, idx: torch.Tensor,
+                            Y: torch.Tensor, stream=None) -> torch.Tensor:
+    """Y[b] = X[b][:, I_b] @ W[I_b, :] from the K-major copy Xt [B, K, M]."""
+    B, K, M, ldxt = _rows(Xt, "Xt")
+    d = _dev(Xt, W, idx, Y)
+    if W.dim() != 2 or W.shape[0] != K or W.stride(1) != 1:
+        raise ValueError("W must be [K, N] with contiguous rows")
+    N, ldw = W.shape[1], W.stride(0)
+    By, My, Ny, ldy = _rows(Y, "Y")
+    if (By, My, Ny) != (B, M, N):
+        raise ValueError("Y must be [B, M, N]")
+    if not (Xt.dtype == W.dtype == Y.dtype == torch.bfloat16):
+        raise TypeError("Xt, W and Y must be bfloat16")
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.numel() % B:
+        raise ValueError("idx must be contiguous int32 [B, k]")
+    k = idx.numel() // B
+    _check("rmm_reduced_gemm_kmajor", lib.rmm_reduced_gemm_kmajor(
+        Xt.data_ptr(), W.data_ptr(), idx.data_ptr(), B, M, N, K, k, ldxt, ldw, Y.data_ptr(),
+        ldy, _stream(d, stream)))
     return Y
 
 

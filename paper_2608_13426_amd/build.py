@@ -1,6 +1,7 @@
 """Build librmm.so (gfx950) in-tree with hipcc.
 
-Usage: ``python -m paper_2608_13426_amd.build`` or ``build()`` from Python.
+Usage: ``python paper_2608_13426_amd/build.py [-v]`` (run as a script: the
+package itself refuses to import without a built library).
 Objects go to ``_build/`` at the repository root; the shared library is
 written next to this file, where the Python binding loads it.
 """

@@ -43,6 +43,24 @@ rmm_status_t check_gemm_shapes(const void *X, const void *W, rmm_dtype_t dt, int
     return RMM_OK;
 }
 
+inline bool aligned16(const void *p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+// The K-major GEMM reads 16-byte vectors through buffer descriptors whose
+// byte offsets must stay below 2^31.
+bool kmajor_ok(const void *Xt, const void *W, int64_t B, int64_t M, int64_t K, int64_t ldxt,
+               int64_t ldw) {
+    if (!aligned16(Xt) || !aligned16(W) || ldxt % 8 || ldw % 8) return false;
+    const int64_t lim = int64_t(1) << 31;
+    if (K * ldxt * 2 + ldxt * 2 >= lim || K * ldw * 2 + ldw * 2 >= lim) return false;
+    return B <= kGridYZMax && M <= kInt32Max;
+}
+
+// K-major copy of the activations held in rmm_linear's workspace
+inline int64_t xt_ld(int64_t M) { return (M + 7) / 8 * 8; }
+inline size_t xt_bytes(int64_t B, int64_t M, int64_t K) {
+    return static_cast<size_t>(B * K * xt_ld(M)) * 2;
+}
+
 }  // namespace
 
 extern "C" {
@@ -73,7 +91,7 @@ size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t 
         if (M < 1 || k < 1 || k > K) return 0;
         return align256(rmm::score_workspace_bytes(B, M, K)) +
                align256(static_cast<size_t>(B * K) * sizeof(double)) +
-               align256(static_cast<size_t>(B * k) * sizeof(int32_t));
+               align256(static_cast<size_t>(B * k) * sizeof(int32_t)) + align256(xt_bytes(B, M, K));
     }
     return 0;
 }
@@ -89,7 +107,23 @@ rmm_status_t rmm_score(const void *X, rmm_dtype_t dtype, int64_t B, int64_t M, i
         if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
     }
     return from_hip(rmm::launch_score(X, dtype == RMM_BF16, B, M, K, ldx, energy,
-                                      static_cast<double *>(workspace), stream));
+                                      static_cast<double *>(workspace), nullptr, 0, stream));
+}
+
+rmm_status_t rmm_score_kmajor(const void *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                              double *energy, void *Xt, int64_t ldxt, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+    rmm_status_t st = check_score(X, RMM_BF16, B, M, K, ldx, energy);
+    if (st != RMM_OK) return st;
+    if (!Xt || ldxt < M) return RMM_ERR_INVALID_ARGUMENT;
+    if (!aligned16(X) || ldx % 8 || !aligned16(Xt) || ldxt % 8) return RMM_ERR_UNSUPPORTED;
+    const size_t need = rmm::score_workspace_bytes(B, M, K);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+        if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
+    }
+    return from_hip(rmm::launch_score(X, true, B, M, K, ldx, energy, static_cast<double *>(workspace),
+                                      static_cast<uint16_t *>(Xt), ldxt, stream));
 }
 
 rmm_status_t rmm_select(const double *energy, int64_t B, int64_t K, int64_t k, int32_t *idx,
@@ -113,6 +147,19 @@ rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx, 
     return from_hip(rmm::launch_gemm_f32(static_cast<const float *>(X),
                                          static_cast<const float *>(W), idx, B, M, N, K, k, ldx,
                                          ldw, static_cast<float *>(Y), ldy, stream));
+}
+
+rmm_status_t rmm_reduced_gemm_kmajor(const void *Xt, const void *W, const int32_t *idx, int64_t B,
+                                     int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldxt,
+                                     int64_t ldw, void *Y, int64_t ldy, hipStream_t stream) {
+    if (!Xt || !W || !idx || !Y) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || M < 1 || N < 1 || K < 1 || k < 1 || k > K) return RMM_ERR_INVALID_ARGUMENT;
+    if (ldxt < M || ldw < N || ldy < N) return RMM_ERR_INVALID_ARGUMENT;
+    if (K > kInt32Max || M > kInt32Max || N > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (!kmajor_ok(Xt, W, B, M, K, ldxt, ldw)) return RMM_ERR_UNSUPPORTED;
+    return from_hip(rmm::launch_gemm_kmajor_bf16(static_cast<const uint16_t *>(Xt),
+                                                 static_cast<const uint16_t *>(W), idx, B, M, N, K, k,
+                                                 ldxt, ldw, static_cast<uint16_t *>(Y), ldy, stream));
 }
 
 rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx, rmm_dtype_t dtype,
@@ -155,12 +202,22 @@ rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtyp
     double *energy = reinterpret_cast<double *>(ws);
     ws += align256(static_cast<size_t>(B * K) * sizeof(double));
     int32_t *idx = idx_out ? idx_out : reinterpret_cast<int32_t *>(ws);
+    ws += align256(static_cast<size_t>(B * k) * sizeof(int32_t));
+    uint16_t *Xt = reinterpret_cast<uint16_t *>(ws);
 
-    hipError_t e = rmm::launch_score(X, dtype == RMM_BF16, B, M, K, ldx, energy, partials, stream);
+    // bf16 with 16-byte aligned rows: the scoring pass also writes the K-major
+    // copy that the K-major GEMM gathers rows from
+    const bool kmajor = dtype == RMM_BF16 && aligned16(X) && ldx % 8 == 0 && aligned16(Xt) &&
+                        kmajor_ok(Xt, W, B, M, K, xt_ld(M), ldw);
+    hipError_t e = rmm::launch_score(X, dtype == RMM_BF16, B, M, K, ldx, energy, partials,
+                                     kmajor ? Xt : nullptr, xt_ld(M), stream);
     if (e != hipSuccess) return RMM_ERR_HIP;
     e = rmm::launch_select(energy, B, K, k, idx, stream);
     if (e != hipSuccess) return RMM_ERR_HIP;
-    if (dtype == RMM_BF16)
+    if (kmajor)
+        e = rmm::launch_gemm_kmajor_bf16(Xt, static_cast<const uint16_t *>(W), idx, B, M, N, K, k,
+                                         xt_ld(M), ldw, static_cast<uint16_t *>(Y), ldy, stream);
+    else if (dtype == RMM_BF16)
         e = rmm::launch_gemm_bf16(static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(W),
                                   idx, B, M, N, K, k, ldx, ldw, static_cast<uint16_t *>(Y), ldy,
                                   stream);

@@ -330,6 +330,166 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_gather_bf16_big_kernel(
         }
 }
 
+// ------------------------------------------- bf16, K-major activations
+// Xt[j][m] holds X[m][j] (written by the scoring pass), so a retained index
+// is one contiguous row of Xt, just as it is one contiguous row of W.  Both
+// operands are gathered as 16-byte row vectors: each thread loads an R x 8
+// block (R retained rows, 8 consecutive m or n), transposes it in registers
+// and writes 8 LDS rows of R consecutive k -- the swizzled layout of the
+// large-tile kernel above.  Square tiles of BT = 256 (four waves of 128x128)
+// or 128 (four waves of 64x64); 64 retained indices per k-tile.
+template <int BT>
+__global__ __launch_bounds__(256, 1) void gemm_kmajor_bf16_kernel(
+    const uint16_t *__restrict__ Xt, const uint16_t *__restrict__ W,
+    const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int K, int k,
+    int64_t ldxt, int64_t ldw, int64_t ldy, int64_t xt_bytes, int64_t w_bytes, int tiles_m,
+    int tiles_n) {
+    using big::at;
+    constexpr int BK = big::BK, NT = 256;
+    constexpr int G = BT / 8;             // 8-wide column groups per tile row
+    constexpr int R = BK * G / NT;        // retained rows per thread block
+    constexpr int TW = BT / 2;            // wave tile TW x TW (2 x 2 waves)
+    constexpr int F = TW / 32;            // 32x32 fragments per wave side
+    static_assert(R == 4 || R == 8, "thread block");
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * 2 * BT * BK];
+
+    const int T = tiles_m * tiles_n;
+    const int bid = blockIdx.x;
+    const int lin = (T % 8 == 0) ? (bid % 8) * (T / 8) + bid / 8 : bid;
+    const int gsz = big::GROUP_M * tiles_n;
+    const int first_m = (lin / gsz) * big::GROUP_M;
+    const int gm = min(big::GROUP_M, tiles_m - first_m);
+    const int m0 = (first_m + (lin % gsz) % gm) * BT;
+    const int n0 = ((lin % gsz) / gm) * BT;
+    const int64_t unit = blockIdx.y;
+    Xt += unit * static_cast<int64_t>(K) * ldxt;
+    Y += unit * static_cast<int64_t>(M) * ldy;
+    idx += unit * k;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = tid % G, tq = tid / G;   // columns 8c.., retained rows R*tq..
+
+    // Rows past k read out of range (zero); columns past M or N read
+    // neighbouring data that only reaches outputs never stored.
+    constexpr uint32_t kOut = 0x80000000u;
+    const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(Xt), 0, static_cast<uint32_t>(xt_bytes), 0x00020000);
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(W), 0, static_cast<uint32_t>(w_bytes), 0x00020000);
+    const __amdgpu_buffer_rsrc_t ir = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(idx), 0, static_cast<uint32_t>(k) * 4u, 0x00020000);
+    const uint32_t arow = static_cast<uint32_t>(ldxt) * 2u, brow = static_cast<uint32_t>(ldw) * 2u;
+    const uint32_t acol = static_cast<uint32_t>(m0 + 8 * c) * 2u;
+    const uint32_t bcol = static_cast<uint32_t>(n0 + 8 * c) * 2u;
+
+    uint32_t raw[R], ao[R], bo[R];
+    uint4 av[R], bv[R];
+    auto fetch_idx = [&](int t0) {
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            raw[i] = __builtin_amdgcn_raw_buffer_load_b32(ir, static_cast<uint32_t>(t0 + R * tq + i) * 4u, 0, 0);
+    };
+    auto make_offsets = [&](int t0) {
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const bool in = t0 + R * tq + i < k;
+            ao[i] = in ? raw[i] * arow + acol : kOut;
+            bo[i] = in ? raw[i] * brow + bcol : kOut;
+        }
+    };
+    auto gather = [&]() {
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const auto a = __builtin_amdgcn_raw_buffer_load_b128(ar, ao[i], 0, 0);
+            av[i] = make_uint4(a[0], a[1], a[2], a[3]);
+        }
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const auto b = __builtin_amdgcn_raw_buffer_load_b128(br, bo[i], 0, 0);
+            bv[i] = make_uint4(b[0], b[1], b[2], b[3]);
+        }
+    };
+    // R x 8 block -> 8 LDS rows (8c + jj) of R consecutive k
+    auto put = [&](uint16_t *dst, const uint4 *v) {
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+            uint32_t d[R / 2];
+#pragma unroll
+            for (int q = 0; q < R / 2; ++q) {
+                const uint32_t a = reinterpret_cast<const uint32_t *>(&v[2 * q])[jj >> 1];
+                const uint32_t b = reinterpret_cast<const uint32_t *>(&v[2 * q + 1])[jj >> 1];
+                d[q] = (jj & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+            }
+            if constexpr (R == 8)
+                *reinterpret_cast<uint4 *>(&dst[at(8 * c + jj, tq)]) = make_uint4(d[0], d[1], d[2], d[3]);
+            else
+                *reinterpret_cast<uint2 *>(&dst[at(8 * c + jj, tq >> 1) + 4 * (tq & 1)]) = make_uint2(d[0], d[1]);
+        }
+    };
+
+    f32x16_t acc[F][F];
+#pragma unroll
+    for (int i = 0; i < F; ++i)
+#pragma unroll
+        for (int j = 0; j < F; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 31, lh = lane >> 5;
+    const int nT = (k + BK - 1) / BK;
+    // buffer b: A at lds + b*BT*BK, B at lds + (2 + b)*BT*BK
+    fetch_idx(0);
+    make_offsets(0);
+    gather();
+    if (nT > 1) fetch_idx(BK);
+    put(lds, av);
+    put(lds + 2 * BT * BK, bv);
+    if (nT > 1) make_offsets(BK);
+    __syncthreads();
+    for (int t = 0; t < nT; ++t) {
+        const int cur = t & 1;
+        const uint16_t *as = lds + cur * BT * BK;
+        const uint16_t *bs = lds + (2 + cur) * BT * BK;
+        if (t + 2 < nT) fetch_idx((t + 2) * BK);
+        if (t + 1 < nT) gather();
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            const int chunk = 2 * ks + lh;
+            bf16x8_t a[F], b[F];
+#pragma unroll
+            for (int i = 0; i < F; ++i)
+                a[i] = *reinterpret_cast<const bf16x8_t *>(&as[at(wm * TW + i * 32 + lr, chunk)]);
+#pragma unroll
+            for (int j = 0; j < F; ++j)
+                b[j] = *reinterpret_cast<const bf16x8_t *>(&bs[at(wn * TW + j * 32 + lr, chunk)]);
+#pragma unroll
+            for (int i = 0; i < F; ++i)
+#pragma unroll
+                for (int j = 0; j < F; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        if (t + 1 < nT) {
+            put(lds + (cur ^ 1) * BT * BK, av);
+            put(lds + (2 + (cur ^ 1)) * BT * BK, bv);
+        }
+        if (t + 2 < nT) make_offsets((t + 2) * BK);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int i = 0; i < F; ++i)
+#pragma unroll
+        for (int j = 0; j < F; ++j) {
+            const int n = n0 + wn * TW + j * 32 + lr;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + wm * TW + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
+                if (m < M && n < N) Y[static_cast<int64_t>(m) * ldy + n] = f32_to_bf16(acc[i][j][v]);
+            }
+        }
+}
+
 // ------------------------------------------------------------------ fp32
 template <int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void gemm_gather_f32_kernel(
@@ -422,6 +582,28 @@ hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t 
         hipLaunchKernelGGL((gemm_gather_bf16_kernel<BM, BN, BK, WM, WN, false>), grid,
                            dim3(WM * WN * kWave), 0, stream, X, W, idx, Y, static_cast<int>(M),
                            static_cast<int>(N), static_cast<int>(k), ldx, ldw, ldy);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
+                                  int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                                  int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
+                                  hipStream_t stream) {
+    const int64_t xt_bytes = K * ldxt * 2, w_bytes = K * ldw * 2;
+    const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+    if (t256 * B >= 128) {
+        const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
+        hipLaunchKernelGGL(gemm_kmajor_bf16_kernel<256>, dim3(tm * tn, static_cast<unsigned>(B)),
+                           dim3(256), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
+                           static_cast<int>(N), static_cast<int>(K), static_cast<int>(k), ldxt,
+                           ldw, ldy, xt_bytes, w_bytes, tm, tn);
+    } else {
+        const int tm = static_cast<int>((M + 127) / 128), tn = static_cast<int>((N + 127) / 128);
+        hipLaunchKernelGGL(gemm_kmajor_bf16_kernel<128>, dim3(tm * tn, static_cast<unsigned>(B)),
+                           dim3(256), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
+                           static_cast<int>(N), static_cast<int>(K), static_cast<int>(k), ldxt,
+                           ldw, ldy, xt_bytes, w_bytes, tm, tn);
+    }
     return hipGetLastError();
 }
 

@@ -15,12 +15,15 @@ constexpr int kScoreCols = 128;        // columns per workgroup
 constexpr int kScoreMinRows = 64;      // fewest rows per split
 constexpr int kScoreTargetBlocks = 1024;
 
+int64_t score_rows_per_split(int64_t B, int64_t M, int64_t K);
 int64_t score_splits(int64_t B, int64_t M, int64_t K);
 size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K);
 
+// Xt (nullable): also write the K-major copy Xt[b][j][m] (bf16 only, X rows
+// 16-byte aligned, Xt 16-byte aligned with ldxt % 8 == 0).
 hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t K,
-                        int64_t ldx, double *energy, double *partials,
-                        hipStream_t stream);
+                        int64_t ldx, double *energy, double *partials, uint16_t *Xt,
+                        int64_t ldxt, hipStream_t stream);
 
 // -------------------------------------------------------------- selection
 hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
@@ -31,6 +34,12 @@ hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t 
                             int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                             int64_t ldx, int64_t ldw, uint16_t *Y, int64_t ldy,
                             hipStream_t stream);
+// Xt: K-major activations [B][K][ldxt]; 16-byte aligned, ldxt % 8 == 0,
+// K*ldxt*2 and K*ldw*2 below 2^31 (checked by the caller).
+hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
+                                  int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                                  int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
+                                  hipStream_t stream);
 hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx,
                            int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                            int64_t ldx, int64_t ldw, float *Y, int64_t ldy,

@@ -7,6 +7,11 @@
 // float64 and accumulated in float64 in a fixed order: per thread over its
 // rows, then the row groups of the workgroup in order, then the splits in
 // order (second kernel).  No atomics, so results are bit-reproducible.
+//
+// Optionally the same pass writes a K-major copy Xt[b][j][m] = X[b][m][j]
+// (bf16): each 64-row slab is staged in LDS and written out as whole
+// 128-byte segments of Xt rows.  The gathered GEMM then reads a retained
+// index as one contiguous Xt row.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -21,13 +26,24 @@ __device__ __forceinline__ double to_f64(float v) { return static_cast<double>(v
 
 // VEC = elements per 16-byte load, or 1 for the element-wise path used when
 // rows are not 16-byte aligned.
-template <typename T, int VEC>
+// Slab layout for the transposed copy: 64 rows x 128 columns of bf16, row
+// stride 136; column c of row r is stored at c ^ (8 * ((r >> 3) & 7)), so the
+// column-wise reads of 8 rows 8 apart fall on distinct banks.
+constexpr int kSlabRows = 64, kSlabStride = kScoreCols + 8;
+__device__ __forceinline__ int slab_at(int r, int c) {
+    return r * kSlabStride + (c ^ (8 * ((r >> 3) & 7)));
+}
+
+template <typename T, int VEC, bool XT>
 __global__ __launch_bounds__(kThreads) void score_partial_kernel(
     const T *__restrict__ X, int64_t M, int64_t K, int64_t ldx, int64_t rows_per_split,
-    double *__restrict__ out, int64_t out_unit_stride, int64_t out_split_stride) {
+    double *__restrict__ out, int64_t out_unit_stride, int64_t out_split_stride,
+    uint16_t *__restrict__ Xt, int64_t ldxt) {
     constexpr int TPR = kScoreCols / VEC;     // threads along a row
     constexpr int RPI = kThreads / TPR;       // rows per iteration
+    static_assert(!XT || (VEC == 8 && 4 * RPI == kSlabRows), "transposed copy: bf16 vector path");
     __shared__ double red[RPI][kScoreCols];
+    __shared__ __attribute__((aligned(16))) uint16_t slab[XT ? kSlabRows * kSlabStride : 1];
 
     const int tid = threadIdx.x;
     const int lane_col = (tid % TPR) * VEC;
@@ -45,9 +61,11 @@ __global__ __launch_bounds__(kThreads) void score_partial_kernel(
 
     if constexpr (VEC > 1) {
         const bool full = col0 + VEC <= K;
+        // whole 64-row slabs (a trip count uniform across the workgroup, as
+        // the slab loop below synchronises), four rows in flight per thread
+        const int64_t n_slabs = (r_end - r_begin) / (4 * RPI);
         int64_t r = r_begin + row_off;
-        // four rows in flight per thread
-        for (; r + 3 * RPI < r_end; r += 4 * RPI) {
+        for (int64_t sl = 0; sl < n_slabs; ++sl, r += 4 * RPI) {
             uint4 q[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
@@ -70,6 +88,29 @@ __global__ __launch_bounds__(kThreads) void score_partial_kernel(
                     acc[v] = fma(x, x, acc[v]);
                 }
             }
+            if constexpr (XT) {
+                // stage the 64-row slab, then write 8 lanes per 128-byte Xt segment
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    *reinterpret_cast<uint4 *>(&slab[slab_at(row_off + u * RPI, lane_col)]) = q[u];
+                __syncthreads();
+                const int64_t slab_row0 = r - row_off;
+                const int rq = (threadIdx.x & 7) * 8;          // 8 rows of the slab
+#pragma unroll
+                for (int pass = 0; pass < kScoreCols / 32; ++pass) {
+                    const int c = pass * 32 + (threadIdx.x >> 3);
+                    const int64_t col = static_cast<int64_t>(blockIdx.x) * kScoreCols + c;
+                    uint32_t w[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        w[e] = static_cast<uint32_t>(slab[slab_at(rq + 2 * e, c)]) |
+                               (static_cast<uint32_t>(slab[slab_at(rq + 2 * e + 1, c)]) << 16);
+                    if (col < K)
+                        *reinterpret_cast<uint4 *>(Xt + unit * K * ldxt + col * ldxt + slab_row0 + rq) =
+                            make_uint4(w[0], w[1], w[2], w[3]);
+                }
+                __syncthreads();
+            }
         }
         for (; r < r_end; r += RPI) {
             const T *p = base + r * ldx + col0;
@@ -77,6 +118,9 @@ __global__ __launch_bounds__(kThreads) void score_partial_kernel(
             for (int v = 0; v < VEC; ++v) {
                 const double x = (col0 + v < K) ? to_f64(p[v]) : 0.0;
                 acc[v] = fma(x, x, acc[v]);
+                if constexpr (XT) {
+                    if (col0 + v < K) Xt[unit * K * ldxt + (col0 + v) * ldxt + r] = p[v];
+                }
             }
         }
     } else {
@@ -113,27 +157,37 @@ __global__ __launch_bounds__(kThreads) void score_finalize_kernel(
     energy[t] = s;
 }
 
-template <typename T, int VEC>
+template <typename T, int VEC, bool XT>
 hipError_t launch_partial(const T *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
                           int64_t S, double *out, int64_t unit_stride, int64_t split_stride,
-                          hipStream_t stream) {
-    const int64_t rps = (M + S - 1) / S;
+                          uint16_t *Xt, int64_t ldxt, hipStream_t stream) {
+    const int64_t rps = score_rows_per_split(B, M, K);
     dim3 grid(static_cast<unsigned>((K + kScoreCols - 1) / kScoreCols),
               static_cast<unsigned>(S), static_cast<unsigned>(B));
-    hipLaunchKernelGGL((score_partial_kernel<T, VEC>), grid, dim3(kThreads), 0, stream,
-                       X, M, K, ldx, rps, out, unit_stride, split_stride);
+    hipLaunchKernelGGL((score_partial_kernel<T, VEC, XT>), grid, dim3(kThreads), 0, stream,
+                       X, M, K, ldx, rps, out, unit_stride, split_stride, Xt, ldxt);
     return hipGetLastError();
 }
 
 }  // namespace
 
-int64_t score_splits(int64_t B, int64_t M, int64_t K) {
+// Rows per split: a whole number of 64-row slabs, chosen so that the grid
+// has about kScoreTargetBlocks workgroups.
+int64_t score_rows_per_split(int64_t B, int64_t M, int64_t K) {
     const int64_t col_blocks = (K + kScoreCols - 1) / kScoreCols;
     int64_t s = (kScoreTargetBlocks + B * col_blocks - 1) / (B * col_blocks);
     const int64_t max_s = (M + kScoreMinRows - 1) / kScoreMinRows;
     if (s > max_s) s = max_s;
-    if (s > 65535) s = 65535;
-    return s < 1 ? 1 : s;
+    if (s < 1) s = 1;
+    int64_t rps = (M + s - 1) / s;
+    rps = (rps + kScoreMinRows - 1) / kScoreMinRows * kScoreMinRows;
+    if ((M + rps - 1) / rps > 65535) rps = (M + 65534) / 65535;
+    return rps;
+}
+
+int64_t score_splits(int64_t B, int64_t M, int64_t K) {
+    const int64_t rps = score_rows_per_split(B, M, K);
+    return (M + rps - 1) / rps;
 }
 
 size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K) {
@@ -142,7 +196,8 @@ size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K) {
 }
 
 hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t K,
-                        int64_t ldx, double *energy, double *partials, hipStream_t stream) {
+                        int64_t ldx, double *energy, double *partials, uint16_t *Xt,
+                        int64_t ldxt, hipStream_t stream) {
     const int64_t S = score_splits(B, M, K);
     double *out = S > 1 ? partials : energy;
     const int64_t unit_stride = S * K, split_stride = K;
@@ -150,14 +205,21 @@ hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t 
     const bool aligned = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                          ((ldx * static_cast<int64_t>(esz)) % 16 == 0);
     hipError_t err;
-    if (bf16) {
+    if (Xt) {   // bf16, 16-byte aligned rows (checked by the caller)
+        err = launch_partial<uint16_t, 8, true>(static_cast<const uint16_t *>(X), B, M, K, ldx, S, out,
+                                                unit_stride, split_stride, Xt, ldxt, stream);
+    } else if (bf16) {
         const uint16_t *x = static_cast<const uint16_t *>(X);
-        err = aligned ? launch_partial<uint16_t, 8>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream)
-                      : launch_partial<uint16_t, 1>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream);
+        err = aligned ? launch_partial<uint16_t, 8, false>(x, B, M, K, ldx, S, out, unit_stride,
+                                                           split_stride, nullptr, 0, stream)
+                      : launch_partial<uint16_t, 1, false>(x, B, M, K, ldx, S, out, unit_stride,
+                                                           split_stride, nullptr, 0, stream);
     } else {
         const float *x = static_cast<const float *>(X);
-        err = aligned ? launch_partial<float, 4>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream)
-                      : launch_partial<float, 1>(x, B, M, K, ldx, S, out, unit_stride, split_stride, stream);
+        err = aligned ? launch_partial<float, 4, false>(x, B, M, K, ldx, S, out, unit_stride,
+                                                        split_stride, nullptr, 0, stream)
+                      : launch_partial<float, 1, false>(x, B, M, K, ldx, S, out, unit_stride,
+                                                        split_stride, nullptr, 0, stream);
     }
     if (err != hipSuccess || S == 1) return err;
     const int64_t n = B * K;

@@ -89,6 +89,38 @@ def test_score_validation():
     assert f(P, 1, 1, 8192, 4096, 4096, P, ctypes.c_void_p(0x100004), need, NULL) == INVALID
 
 
+def test_score_kmajor_validation():
+    f = rmm.lib.rmm_score_kmajor
+    A = ctypes.c_void_p(0x100000)       # 16-byte aligned, never dereferenced
+    assert f(A, 1, 64, 128, 128, P, NULL, 64, NULL, 0, NULL) == INVALID        # no Xt
+    assert f(A, 1, 64, 128, 128, P, A, 60, NULL, 0, NULL) == INVALID          # ldxt < M
+    assert f(A, 1, 64, 130, 130, P, A, 64, NULL, 0, NULL) == UNSUPPORTED      # ldx % 8
+    assert f(A, 1, 64, 128, 128, P, A, 68, NULL, 0, NULL) == UNSUPPORTED      # ldxt % 8
+    assert f(ctypes.c_void_p(0x100002), 1, 64, 128, 128, P, A, 64, NULL, 0, NULL) == UNSUPPORTED
+    assert f(NULL, 1, 64, 128, 128, P, A, 64, NULL, 0, NULL) == INVALID
+
+
+def test_gemm_kmajor_validation():
+    f = rmm.lib.rmm_reduced_gemm_kmajor
+    A = ctypes.c_void_p(0x100000)
+    ok = [A, A, P, 1, 64, 64, 128, 32, 64, 64, A, 64, NULL]
+
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 10):
+        assert call(i, NULL) == INVALID
+    assert call(7, 0) == INVALID            # k
+    assert call(7, 129) == INVALID          # k > K
+    assert call(8, 63) == INVALID           # ldxt < M
+    assert call(8, 68) == UNSUPPORTED       # ldxt % 8
+    assert call(9, 60) == INVALID           # ldw < N
+    assert call(0, ctypes.c_void_p(0x100008)) == UNSUPPORTED
+    assert call(6, 2 ** 24) == UNSUPPORTED  # K * ldxt * 2 bytes beyond 2^31
+
+
 def test_select_validation():
     f = rmm.lib.rmm_select
     assert f(NULL, 1, 8, 2, P, NULL) == INVALID

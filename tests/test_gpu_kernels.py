@@ -83,6 +83,33 @@ def test_score_is_deterministic():
     assert all(np.array_equal(runs[0], r) for r in runs[1:])
 
 
+def _ld8(n):
+    return (n + 7) // 8 * 8
+
+
+@pytest.mark.parametrize("B,M,K,seed", [
+    (1, 128, 512, 0), (2, 1000, 296, 1), (1, 8192, 1024, 2), (3, 37, 8, 3), (1, 64, 136, 4),
+    (2, 200, 2048, 5),
+])
+def test_score_kmajor(B, M, K, seed):
+    """Energies bit-identical to rmm_score; Xt an exact transpose of X."""
+    dev = require_gpu()
+    stored = wl.random_case(60 + seed, (B, M, K), "bf16", n_outlier=max(1, K // 50))
+    Xd = to_device(stored, "bf16", dev)
+    e1 = _energies_gpu(Xd, B, M, K, dev)
+    ldxt = _ld8(M)
+    Xt_full = torch.full((B, K, ldxt), -1.0, dtype=torch.bfloat16, device=dev)
+    Xt = Xt_full[:, :, :M]
+    e2 = torch.empty(B * K, dtype=torch.float64, device=dev)
+    rmm.rmm_score_kmajor(Xd, e2, Xt, _score_ws(B, M, K, dev))
+    assert torch.equal(e1, e2)
+    got = Xt_full.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got[:, :, :M], np.ascontiguousarray(stored.transpose(0, 2, 1)))
+    assert np.all(got[:, :, M:] == 0xbf80)          # padding columns untouched
+    e_ref = ro.column_energies(wl.decode(stored, "bf16")[0].astype(np.float64))
+    check_energies(e2.cpu().numpy()[:K], e_ref, M)
+
+
 # ----------------------------------------------------------------- select
 
 def _energy_case(seed, B, K):
@@ -196,6 +223,41 @@ def test_reduced_gemm_large_tiles(B, M, N, K, k, ldw_pad, seed):
         check_product(Y[b], ref, absprod, k, "bf16")
 
 
+@pytest.mark.parametrize("B,M,N,K,k,seed", [
+    (1, 200, 72, 300, 37, 0),        # 128-wide tiles, ragged everything
+    (2, 129, 104, 64, 64, 1),
+    (1, 1, 8, 1, 1, 3),
+    (3, 300, 520, 700, 333, 5),
+    (1, 513, 264, 2048, 1, 6),
+    (1, 2100, 4104, 3000, 1111, 50),  # 256-wide tiles, ragged M/N/k tails
+    (2, 2048, 2048, 4096, 2048, 51),
+    (1, 4096, 2048, 1024, 1, 53),
+    (1, 2048, 4096, 1024, 1024, 54),
+])
+def test_reduced_gemm_kmajor(B, M, N, K, k, seed):
+    """Oracle parity, and bit-identity with the row-major gather (same k order)."""
+    dev = require_gpu()
+    Xs = wl.random_case(seed, (B, M, K), "bf16", n_outlier=max(1, K // 40))
+    Ws = wl.random_case(seed + 100, (K, N), "bf16", std=0.02)
+    idx = _ascending(seed, B, K, k)
+    ldxt = _ld8(M)
+    Xt_host = np.zeros((B, K, ldxt), dtype=np.uint16)
+    Xt_host[:, :, :M] = Xs.transpose(0, 2, 1)
+    Xtd = to_device(Xt_host, "bf16", dev)[:, :, :M]
+    Wd = to_device(Ws, "bf16", dev)
+    idd = torch.from_numpy(idx.astype(np.int32)).to(dev)
+    Y = torch.empty((B, M, N), dtype=torch.bfloat16, device=dev)
+    rmm.rmm_reduced_gemm_kmajor(Xtd, Wd, idd, Y)
+    Y_row = torch.empty_like(Y)
+    rmm.rmm_reduced_gemm(to_device(Xs, "bf16", dev), Wd, idd, Y_row)
+    assert torch.equal(Y.view(torch.int16), Y_row.view(torch.int16))
+    Yn = from_device(Y)
+    X, W = wl.decode(Xs, "bf16").astype(np.float64), wl.decode(Ws, "bf16").astype(np.float64)
+    for b in range(B):
+        ref = ro.reduced_matmul(X[b], W, idx[b])
+        check_product(Yn[b], ref, np.abs(X[b][:, idx[b]]) @ np.abs(W[idx[b], :]), k, "bf16")
+
+
 def test_reduced_gemm_strided_operands():
     """Leading dimensions larger than the logical widths."""
     dev = require_gpu()
@@ -306,6 +368,20 @@ def test_linear_equals_separate_calls_bitwise():
     Y3 = torch.empty_like(Y1)
     rmm.rmm_linear(Xd, Wd, r, Y3)
     assert torch.equal(Y1.view(torch.int16), Y3.view(torch.int16))
+    # the K-major split calls (what rmm_linear runs for aligned bf16)
+    Xt = torch.empty((B, K, _ld8(M)), dtype=torch.bfloat16, device=dev)[:, :, :M]
+    e2 = torch.empty_like(e)
+    rmm.rmm_score_kmajor(Xd, e2, Xt, _score_ws(B, M, K, dev))
+    assert torch.equal(e, e2)
+    Y4 = torch.empty_like(Y1)
+    rmm.rmm_reduced_gemm_kmajor(Xt, Wd, i2.reshape(B, k), Y4)
+    assert torch.equal(Y1.view(torch.int16), Y4.view(torch.int16))
+    # rows that are not 16-byte multiples take the row-major path: same bits
+    Xpad = torch.zeros((B, M, K + 3), dtype=torch.bfloat16, device=dev)
+    Xpad[:, :, :K] = Xd
+    Y5 = torch.empty_like(Y1)
+    rmm.rmm_linear(Xpad[:, :, :K], Wd, r, Y5)
+    assert torch.equal(Y1.view(torch.int16), Y5.view(torch.int16))
 
 
 def test_linear_is_deterministic():
