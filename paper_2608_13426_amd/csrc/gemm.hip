@@ -338,18 +338,19 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_gather_bf16_big_kernel(
 // and writes 8 LDS rows of R consecutive k -- the swizzled layout of the
 // large-tile kernel above.  Square tiles of BT = 256 (four waves of 128x128)
 // or 128 (four waves of 64x64); 64 retained indices per k-tile.
-template <int BT>
-__global__ __launch_bounds__(256, 1) void gemm_kmajor_bf16_kernel(
+template <int BT, int NW>
+__global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_bf16_kernel(
     const uint16_t *__restrict__ Xt, const uint16_t *__restrict__ W,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int K, int k,
     int64_t ldxt, int64_t ldw, int64_t ldy, int64_t xt_bytes, int64_t w_bytes, int tiles_m,
     int tiles_n) {
     using big::at;
-    constexpr int BK = big::BK, NT = 256;
+    constexpr int BK = big::BK, NT = NW * 64;
     constexpr int G = BT / 8;             // 8-wide column groups per tile row
     constexpr int R = BK * G / NT;        // retained rows per thread block
-    constexpr int TW = BT / 2;            // wave tile TW x TW (2 x 2 waves)
-    constexpr int F = TW / 32;            // 32x32 fragments per wave side
+    constexpr int WN = NW / 2;            // waves: 2 along M, NW/2 along N
+    constexpr int TWM = BT / 2, TWN = BT / WN;
+    constexpr int FM = TWM / 32, FN = TWN / 32;
     static_assert(R == 4 || R == 8, "thread block");
     __shared__ __attribute__((aligned(16))) uint16_t lds[2 * 2 * BT * BK];
 
@@ -427,15 +428,15 @@ __global__ __launch_bounds__(256, 1) void gemm_kmajor_bf16_kernel(
         }
     };
 
-    f32x16_t acc[F][F];
+    f32x16_t acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < F; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < F; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int lr = lane & 31, lh = lane >> 5;
     const int nT = (k + BK - 1) / BK;
     // buffer b: A at lds + b*BT*BK, B at lds + (2 + b)*BT*BK
@@ -456,17 +457,17 @@ __global__ __launch_bounds__(256, 1) void gemm_kmajor_bf16_kernel(
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             const int chunk = 2 * ks + lh;
-            bf16x8_t a[F], b[F];
+            bf16x8_t a[FM], b[FN];
 #pragma unroll
-            for (int i = 0; i < F; ++i)
-                a[i] = *reinterpret_cast<const bf16x8_t *>(&as[at(wm * TW + i * 32 + lr, chunk)]);
+            for (int i = 0; i < FM; ++i)
+                a[i] = *reinterpret_cast<const bf16x8_t *>(&as[at(wm * TWM + i * 32 + lr, chunk)]);
 #pragma unroll
-            for (int j = 0; j < F; ++j)
-                b[j] = *reinterpret_cast<const bf16x8_t *>(&bs[at(wn * TW + j * 32 + lr, chunk)]);
+            for (int j = 0; j < FN; ++j)
+                b[j] = *reinterpret_cast<const bf16x8_t *>(&bs[at(wn * TWN + j * 32 + lr, chunk)]);
 #pragma unroll
-            for (int i = 0; i < F; ++i)
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < F; ++j)
+                for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         if (t + 1 < nT) {
@@ -478,13 +479,13 @@ __global__ __launch_bounds__(256, 1) void gemm_kmajor_bf16_kernel(
     }
 
 #pragma unroll
-    for (int i = 0; i < F; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < F; ++j) {
-            const int n = n0 + wn * TW + j * 32 + lr;
+        for (int j = 0; j < FN; ++j) {
+            const int n = n0 + wn * TWN + j * 32 + lr;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int m = m0 + wm * TW + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
+                const int m = m0 + wm * TWM + i * 32 + 8 * (v / 4) + 4 * lh + (v % 4);
                 if (m < M && n < N) Y[static_cast<int64_t>(m) * ldy + n] = f32_to_bf16(acc[i][j][v]);
             }
         }
@@ -585,6 +586,8 @@ hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t 
     return hipGetLastError();
 }
 
+constexpr int kKmajorWaves = 8;
+
 hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
                                   int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                                   int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
@@ -593,14 +596,14 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
     const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
     if (t256 * B >= 128) {
         const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
-        hipLaunchKernelGGL(gemm_kmajor_bf16_kernel<256>, dim3(tm * tn, static_cast<unsigned>(B)),
-                           dim3(256), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
+        hipLaunchKernelGGL((gemm_kmajor_bf16_kernel<256, kKmajorWaves>),
+                           dim3(tm * tn, static_cast<unsigned>(B)), dim3(kKmajorWaves * 64), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
                            static_cast<int>(N), static_cast<int>(K), static_cast<int>(k), ldxt,
                            ldw, ldy, xt_bytes, w_bytes, tm, tn);
     } else {
         const int tm = static_cast<int>((M + 127) / 128), tn = static_cast<int>((N + 127) / 128);
-        hipLaunchKernelGGL(gemm_kmajor_bf16_kernel<128>, dim3(tm * tn, static_cast<unsigned>(B)),
-                           dim3(256), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
+        hipLaunchKernelGGL((gemm_kmajor_bf16_kernel<128, 4>),
+                           dim3(tm * tn, static_cast<unsigned>(B)), dim3(256), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
                            static_cast<int>(N), static_cast<int>(K), static_cast<int>(k), ldxt,
                            ldw, ldy, xt_bytes, w_bytes, tm, tn);
     }
