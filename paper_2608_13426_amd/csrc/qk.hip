@@ -129,7 +129,11 @@ __global__ __launch_bounds__(WM *WN *kWave) void qk_bf16_kernel(
 // with an odd row stride of D/2+1 words, so 32 rows read at one column hit
 // 32 distinct banks; the MFMA operands are gathered from the staged rows at
 // the retained dims (a zeroed pad word stands in for padding positions).
-// Q's fragments are gathered once and kept in registers.  The product is
+// Q's fragments are gathered once and kept in registers.  The four waves
+// split the 128x128 tile into KW = 4/WQ key strips and WQ query strips: with
+// few retained dims (KSMAX k-steps) one strip of 32 keys per wave against all
+// 128 queries, so no K fragment is gathered twice; with more, 2x2 strips keep
+// Q's register footprint in bounds.  The product is
 // formed transposed (keys x queries), so each lane holds 4 consecutive keys
 // of one query; tiles are staged through LDS and written as coalesced
 // 16-byte non-temporal stores.  Key tiles wholly above the diagonal are
@@ -138,9 +142,12 @@ namespace rowk {
 constexpr int BQ = 128, BT = 128, NT = 256;
 constexpr int OS = BT + 8;    // staged output row: 272 bytes (16-byte aligned)
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+// cache policy of the score stores (sc1).  Streaming (nt) stores measured
+// about 25% slower for this pattern of 256-byte row pieces 2*Lk bytes apart.
+constexpr int kStoreAux = 16;
 }  // namespace rowk
 
-template <int D>
+template <int D, int KSMAX, int WQ>
 __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Kc,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ S, int H, int Hkv, int Lq, int Lk,
@@ -149,8 +156,11 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
     constexpr int RW = D / 2 + 1;          // words per staged row (odd)
     constexpr int CH = D / 8;              // 16-byte chunks per row
     constexpr int PER_T = BT * CH / NT;    // chunks staged per thread
-    constexpr int KSMAX = D / 16;
+    constexpr int KW = 4 / WQ;             // waves along keys
+    constexpr int FI = BT / KW / 32;       // 32-key fragments per wave
+    constexpr int FJ = BQ / WQ / 32;       // 32-query fragments per wave
     static_assert(D % 16 == 0 && BQ == BT && (BT * CH) % NT == 0, "shape");
+    static_assert(KSMAX * 16 <= D && (WQ == 1 || WQ == 2), "shape");
 
     __shared__ uint32_t rows_lds[BT * RW];
     __shared__ __attribute__((aligned(16))) uint16_t out_lds[BQ * OS];
@@ -169,6 +179,10 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
         n_compute = limit < 0 ? 0 : min(n_tiles, limit / BT + 1);
     }
     const int r16 = tid >> 4, c16 = tid & 15;           // store role: rows r16 + 16i, chunk c16
+    // the block's rows of S; rows at or past Lq fall outside the range and are dropped
+    const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
+        Sh + static_cast<int64_t>(q0) * Lk, 0, static_cast<uint32_t>(min(BQ, Lq - q0) * Lk * 2),
+        0x00020000);
 
     if (n_compute > 0) {
         const int kp = (k + 15) & ~15;
@@ -220,18 +234,18 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
             return __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
         };
 
-        const int wk = wave >> 1, wq = wave & 1;     // wave: 64 keys x 64 queries
+        const int wk = wave / WQ, wq = wave % WQ;   // wave: BT/KW keys x BQ/WQ queries
         const int lr = lane & 31, lh = lane >> 5;
 
         load_rows(qr);
         store_rows();
         __syncthreads();
-        bf16x8_t qf[2][KSMAX];
+        bf16x8_t qf[FJ][KSMAX];
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < FJ; ++j)
 #pragma unroll
             for (int ks = 0; ks < KSMAX; ++ks)
-                if (ks < KS) qf[j][ks] = frag(wq * 64 + j * 32 + lr, ks);
+                if (ks < KS) qf[j][ks] = frag((wq * FJ + j) * 32 + lr, ks);
         load_rows(key_rsrc(0));
         __syncthreads();
         store_rows();
@@ -239,45 +253,47 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
 
         for (int kt = 0; kt < n_compute; ++kt) {
             if (kt + 1 < n_compute) load_rows(key_rsrc(kt + 1));
-            f32x16_t acc[2][2];
+            f32x16_t acc[FI][FJ];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < FI; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < FJ; ++j)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 #pragma unroll
             for (int ks = 0; ks < KSMAX; ++ks) {
                 if (ks < KS) {
-                    const bf16x8_t kf0 = frag(wk * 64 + lr, ks);
-                    const bf16x8_t kf1 = frag(wk * 64 + 32 + lr, ks);
 #pragma unroll
-                    for (int j = 0; j < 2; ++j) {
-                        acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[j][ks], acc[0][j], 0, 0, 0);
-                        acc[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[j][ks], acc[1][j], 0, 0, 0);
+                    for (int i = 0; i < FI; ++i) {
+                        const bf16x8_t kf = frag((wk * FI + i) * 32 + lr, ks);
+#pragma unroll
+                        for (int j = 0; j < FJ; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[j][ks], acc[i][j], 0, 0, 0);
                     }
                 }
             }
-            // acc[i][j][4*gq + r]: key wk*64 + i*32 + 8*gq + 4*lh + r, query wq*64 + j*32 + lr
+            // acc[i][j][4*gq + r]: key (wk*FI + i)*32 + 8*gq + 4*lh + r, query (wq*FJ + j)*32 + lr
+            // a tile whose last key is at most its first query + off has no masked entry
+            const bool tile_open = !causal || kt * BT + BT - 1 <= q0 + off;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < FI; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    const int ql = wq * 64 + j * 32 + lr;
+                for (int j = 0; j < FJ; ++j) {
+                    const int ql = (wq * FJ + j) * 32 + lr;
                     const int qg = q0 + ql;
 #pragma unroll
                     for (int gq = 0; gq < 4; ++gq) {
-                        const int kl = wk * 64 + i * 32 + 8 * gq + 4 * lh;
-                        const int kg = kt * BT + kl;
-                        uint16_t o4[4];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const bool masked = causal && (kg + r > qg + off);
-                            o4[r] = masked ? kBf16NegInf : f32_to_bf16(acc[i][j][4 * gq + r] * scale);
+                        const int kl = (wk * FI + i) * 32 + 8 * gq + 4 * lh;
+                        uint32_t w0 = pack_bf16x2(acc[i][j][4 * gq] * scale, acc[i][j][4 * gq + 1] * scale);
+                        uint32_t w1 = pack_bf16x2(acc[i][j][4 * gq + 2] * scale, acc[i][j][4 * gq + 3] * scale);
+                        if (!tile_open) {
+                            const int lim = qg + off - (kt * BT + kl);   // keys kl + r kept iff r <= lim
+                            if (lim < 0) w0 = (w0 & 0xffff0000u) | kBf16NegInf;
+                            if (lim < 1) w0 = (w0 & 0x0000ffffu) | (static_cast<uint32_t>(kBf16NegInf) << 16);
+                            if (lim < 2) w1 = (w1 & 0xffff0000u) | kBf16NegInf;
+                            if (lim < 3) w1 = (w1 & 0x0000ffffu) | (static_cast<uint32_t>(kBf16NegInf) << 16);
                         }
-                        *reinterpret_cast<uint2 *>(&out_lds[ql * OS + kl]) =
-                            make_uint2(o4[0] | (static_cast<uint32_t>(o4[1]) << 16),
-                                       o4[2] | (static_cast<uint32_t>(o4[3]) << 16));
+                        *reinterpret_cast<uint2 *>(&out_lds[ql * OS + kl]) = make_uint2(w0, w1);
                     }
                 }
             __syncthreads();
@@ -285,10 +301,10 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
             for (int i = 0; i < BQ / 16; ++i) {
                 const int r = r16 + 16 * i;
                 const int col = kt * BT + c16 * 8;
-                if (q0 + r < Lq && col < Lk) {
+                if (col < Lk) {
                     const uint4 v = *reinterpret_cast<const uint4 *>(&out_lds[r * OS + c16 * 8]);
-                    __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w},
-                        reinterpret_cast<u32x4_t *>(Sh + static_cast<int64_t>(q0 + r) * Lk + col));
+                    __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{v.x, v.y, v.z, v.w}, sr,
+                        static_cast<uint32_t>((r * Lk + col) * 2), 0, kStoreAux);
                 }
             }
             if (kt + 1 < n_compute) store_rows();
@@ -302,9 +318,9 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
         for (int i = 0; i < BQ / 16; ++i) {
             const int r = r16 + 16 * i;
             const int col = kt * BT + c16 * 8;
-            if (q0 + r < Lq && col < Lk)
-                __builtin_nontemporal_store(u32x4_t{ninf2, ninf2, ninf2, ninf2},
-                    reinterpret_cast<u32x4_t *>(Sh + static_cast<int64_t>(q0 + r) * Lk + col));
+            if (col < Lk)
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{ninf2, ninf2, ninf2, ninf2}, sr,
+                    static_cast<uint32_t>((r * Lk + col) * 2), 0, kStoreAux);
         }
     }
 }
@@ -376,19 +392,18 @@ hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *
                           int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
                           int64_t D, int64_t k, float scale, bool causal, uint16_t *S,
                           hipStream_t stream) {
-    const bool rows_ok = (D == 64 || D == 128) && Lk % 8 == 0 &&
+    // Lk bound: a block's 128 rows of S are addressed with 32-bit byte offsets
+    const bool rows_ok = (D == 64 || D == 128) && Lk % 8 == 0 && Lk <= (1 << 22) &&
                          reinterpret_cast<uintptr_t>(S) % 16 == 0;
     if (rows_ok) {
         dim3 grid(static_cast<unsigned>((Lq + rowk::BQ - 1) / rowk::BQ),
                   static_cast<unsigned>(batch * H));
-        if (D == 128)
-            hipLaunchKernelGGL(qk_bf16_rows_kernel<128>, grid, dim3(rowk::NT), 0, stream, Q, Kc, idx,
-                               S, static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
-                               static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
-        else
-            hipLaunchKernelGGL(qk_bf16_rows_kernel<64>, grid, dim3(rowk::NT), 0, stream, Q, Kc, idx,
-                               S, static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
-                               static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
+        // up to 64 retained dims: one key strip per wave; more: 2x2 strips
+        auto kern = D == 64 ? qk_bf16_rows_kernel<64, 4, 1>
+                  : k <= 64 ? qk_bf16_rows_kernel<128, 4, 1> : qk_bf16_rows_kernel<128, 8, 2>;
+        hipLaunchKernelGGL(kern, grid, dim3(rowk::NT), 0, stream, Q, Kc, idx, S,
+                           static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
+                           static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
         return hipGetLastError();
     }
     constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2;

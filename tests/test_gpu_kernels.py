@@ -288,6 +288,12 @@ def test_reduced_gemm_strided_operands():
     ("bf16", 1, 4, 4, 200, 300, 128, 0.5, False, 3),
     ("bf16", 1, 2, 2, 257, 257, 128, 0.75, True, 4),
     ("bf16", 1, 2, 1, 33, 40, 128, 0.001, True, 5),    # k = 1
+    # Lk % 8 == 0: the row-streaming kernel, each register layout it has
+    ("bf16", 1, 4, 2, 200, 264, 128, 0.75, True, 8),   # k = 96: 2x2 wave strips
+    ("bf16", 2, 2, 1, 136, 256, 128, 1.0, True, 9),    # k = 128, Lk > Lq
+    ("bf16", 1, 4, 1, 130, 136, 128, 0.5, False, 10),  # k = 64: one key strip per wave
+    ("bf16", 1, 2, 2, 300, 320, 64, 0.5, True, 11),
+    ("bf16", 1, 2, 2, 256, 128, 128, 0.3, True, 12),   # Lq > Lk: leading rows fully masked
     ("f32", 1, 4, 2, 100, 130, 128, 0.5, True, 6),
     ("f32", 1, 2, 2, 70, 70, 64, 1.0, False, 7),
 ])
