@@ -33,4 +33,34 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 constexpr int kWave = 64;
 
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+// The two gfx950 LDS instructions below exist only in the device pass; the
+// host pass of a kernel that names them directly drops the kernel's launch
+// stub, so they are wrapped here.
+
+// ds_read_b64_tr_b16 at LDS byte address `lds`: within each 16-lane group,
+// lane l receives element l%4 of the 8-byte words addressed by lanes
+// 4v + (l%16)/4, v = 0..3 of its group (a 4x4 transpose of 16-bit values).
+__device__ __forceinline__ s16x4_t lds_read_tr16(const void *lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t *)(lds));
+#else
+    (void)lds;
+    return s16x4_t{};
+#endif
+}
+
+// 16-byte buffer load straight into LDS: lane i's data lands at lds + 16*i
+// (`lds` must be the same for the whole wave).  Offsets past the
+// descriptor's range stage zeros.
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rsrc, void *lds, uint32_t voffset) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void *)(lds), 16,
+                                             voffset, 0, 0, 0);
+#else
+    (void)rsrc; (void)lds; (void)voffset;
+#endif
+}
+
 }  // namespace rmm

@@ -13,6 +13,8 @@
 // filled; no compacted copy of either operand is ever written to memory.
 //
 // fp32 path: the same gather into LDS with a VALU FMA tile (fp32 accumulate).
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -491,6 +493,260 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_bf16_kernel(
         }
 }
 
+// ---------------------- bf16, K-major activations, DMA + transposing reads
+// Same operands as above (rows I(t) of Xt and of W), but nothing passes
+// through registers on the way in: each wave issues 16-byte buffer loads
+// that land directly in LDS (a wave fills 1 KiB = two 512-byte staged rows
+// of one operand), and the MFMA fragments are read back with the gfx950
+// transposing LDS read, which hands each lane four consecutive k of one m
+// (or n) from a K-major tile.  Within a staged row the 16-byte chunk c is
+// stored at position c ^ 4*(row % 4), so that the four rows one 16-lane
+// group reads together land in distinct banks.  Retained rows past k read
+// out of range and stage zeros.
+//
+// The K loop is a ring of S stages of BKS retained rows; loads run S-1
+// stages ahead of the MFMAs, so a gather has S-1 stage times to arrive.  The
+// retained indices are read with scalar loads (a wave's rows are
+// contiguous in the index list), which keeps them off the vector-memory
+// counter: waiting for the stage about to be consumed never waits for the
+// younger stages still in flight.
+//
+// The product is formed as Y^T tiles (W fragment as the MFMA's first
+// operand), so each lane ends with four consecutive n of one m and stores
+// them as one 8-byte vector.
+namespace trk {
+constexpr int BT = 256;
+constexpr int ROWB = BT * 2;             // bytes per staged row
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt unconstrained
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_le() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+}  // namespace trk
+
+template <int NW, int BKS, int S>
+__global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
+    const uint16_t *__restrict__ Xt, const uint16_t *__restrict__ W,
+    const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int k,
+    int64_t ldxt, int64_t ldw, int64_t ldy, int64_t xt_bytes, int64_t w_bytes, int tiles_m,
+    int tiles_n, int vec_y) {
+    using namespace trk;
+    constexpr int ASZ = BKS * ROWB;      // one operand, one stage
+    constexpr int PPW = BKS / 2 / NW;    // staged row pairs per wave per operand
+    constexpr int WN = NW / 2;           // waves: 2 along m, NW/2 along n
+    constexpr int TWN = BT / WN;
+    constexpr int FM = 4, FN = TWN / 32;
+    constexpr int D = S - 1;             // stages in flight ahead of the MFMAs
+    constexpr int PER_STAGE = 2 * PPW;   // loads per wave per stage
+    static_assert((NW == 4 || NW == 8) && PPW * NW * 2 == BKS && PPW % 2 == 0, "wave layout");
+    static_assert(BKS % 16 == 0 && S >= 2 && S <= 4 && 2 * S * ASZ <= 160 * 1024, "stages");
+    static_assert((D - 1) * PER_STAGE < 64, "vmcnt range");
+    // One LDS object per stage and operand: the compiler then sees that a
+    // fragment read of one stage cannot alias the loads still landing in the
+    // others, and waits only for the loads of the stage it reads.
+    __shared__ __attribute__((aligned(1024))) char sA0[ASZ], sA1[ASZ], sA2[ASZ], sA3[ASZ];
+    __shared__ __attribute__((aligned(1024))) char sB0[ASZ], sB1[ASZ], sB2[ASZ], sB3[ASZ];
+    auto stage_a = [&](auto I) -> char * {
+        constexpr int i = decltype(I)::value;
+        if constexpr (i == 0) return sA0;
+        else if constexpr (i == 1) return sA1;
+        else if constexpr (i == 2) return sA2;
+        else return sA3;
+    };
+    auto stage_b = [&](auto I) -> char * {
+        constexpr int i = decltype(I)::value;
+        if constexpr (i == 0) return sB0;
+        else if constexpr (i == 1) return sB1;
+        else if constexpr (i == 2) return sB2;
+        else return sB3;
+    };
+
+    const int T = tiles_m * tiles_n;
+    const int bid = blockIdx.x;
+    const int lin = (T % 8 == 0) ? (bid % 8) * (T / 8) + bid / 8 : bid;
+    const int gsz = big::GROUP_M * tiles_n;
+    const int first_m = (lin / gsz) * big::GROUP_M;
+    const int gm = min(big::GROUP_M, tiles_m - first_m);
+    const int m0 = (first_m + (lin % gsz) % gm) * BT;
+    const int n0 = ((lin % gsz) / gm) * BT;
+    const int64_t unit = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t *I = idx + unit * k;
+
+    constexpr uint32_t kOut = 0x80000000u;
+    const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(Xt + unit * (xt_bytes / 2)), 0, static_cast<uint32_t>(xt_bytes),
+        0x00020000);
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(W), 0, static_cast<uint32_t>(w_bytes), 0x00020000);
+    const uint32_t arow = static_cast<uint32_t>(ldxt) * 2u, brow = static_cast<uint32_t>(ldw) * 2u;
+
+    // DMA role: row pair P = wave*PPW + q of a stage holds retained rows
+    // 2P + h; this lane fills chunk position p of its row with source chunk
+    // p ^ 4*(row % 4), and row % 4 = (2q + h) % 4.
+    const int h = lane >> 5, p = lane & 31;
+    uint32_t acol[2], bcol[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const int src = p ^ (4 * ((2 * e + h) & 3));
+        acol[e] = static_cast<uint32_t>(m0 + 8 * src) * 2u;
+        bcol[e] = static_cast<uint32_t>(n0 + 8 * src) * 2u;
+    }
+    // the wave's 2*PPW retained positions of stage st, read as scalars
+    // (clamped into the list; positions past k are masked below)
+    auto stage_idx = [&](int st, int32_t (&r)[2 * PPW]) {
+        const int base = st * BKS + 2 * wave * PPW;
+#pragma unroll
+        for (int e = 0; e < 2 * PPW; ++e) r[e] = I[min(base + e, k - 1)];
+    };
+    auto dma = [&](auto slot, int st, const int32_t (&r)[2 * PPW]) {
+        char *la = stage_a(slot), *lb = stage_b(slot);
+        const int base = st * BKS + 2 * wave * PPW;
+#pragma unroll
+        for (int q = 0; q < PPW; ++q) {
+            const bool in = base + 2 * q + h < k;
+            const uint32_t j = static_cast<uint32_t>(h ? r[2 * q + 1] : r[2 * q]);
+            const uint32_t ao = in ? j * arow + acol[q & 1] : kOut;
+            const uint32_t bo = in ? j * brow + bcol[q & 1] : kOut;
+            const int P = wave * PPW + q;
+            lds_load16(ar, la + P * 1024, ao);
+            lds_load16(br, lb + P * 1024, bo);
+        }
+    };
+
+    // Fragment role: 16-lane group g reads rows 8*(g/2) + s/4 (+4) of a
+    // 16-row k-step, columns 16*(g%2) + 4*(s%4) .. +3 of a 32-wide block.
+    const int wm = wave / WN, wn = wave % WN;
+    const int g = lane >> 4, s16 = lane & 15;
+    const int f4 = (s16 >> 2) & 3;
+    const int lane_off = (8 * (g >> 1) + (s16 >> 2)) * ROWB + (2 * (g & 1) + ((s16 & 3) >> 1)) * 16 +
+                         8 * (s16 & 1);
+    int aoff[FM], boff[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) aoff[i] = lane_off + 64 * (4 * wm + (i ^ f4));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int q = (wn * TWN) / 32 + j;
+        boff[j] = lane_off + 64 * ((q & ~3) + ((q & 3) ^ f4));
+    }
+    auto frag = [&](const char *base) -> bf16x8_t {
+        const s16x4_t lo = lds_read_tr16(base);
+        const s16x4_t hi = lds_read_tr16(base + 4 * ROWB);
+        typedef short s16x8_t __attribute__((ext_vector_type(8)));
+        const s16x8_t v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(bf16x8_t, v);
+    };
+
+    f32x16_t acc[FN][FM];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.f;
+
+    const int nT = (k + BKS - 1) / BKS;
+    int32_t r[2 * PPW];
+    // a barrier that orders this wave's LDS accesses around it but, unlike
+    // __syncthreads(), does not wait for the loads still landing in LDS
+    auto barrier = []() { asm volatile("s_barrier" ::: "memory"); };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    // Every step issues one stage of loads (stages past the last one read
+    // out of range: no memory traffic, zeros into a slot nobody reads), so
+    // the count of loads younger than a given stage is the same at every
+    // step and the wait before each barrier is a fixed vmcnt.
+    auto prologue = [&](auto I) {
+        constexpr int st = decltype(I)::value;
+        if constexpr (st < D) {
+            stage_idx(st, r);
+            dma(I, st, r);
+        }
+    };
+    prologue(I0{});
+    prologue(I1{});
+    prologue(I2{});
+    prologue(I3{});
+    stage_idx(D, r);
+    wait_vmcnt_le<(D - 1) * PER_STAGE>();
+    barrier();
+    // stage t lives in slot t % S; the loop is unrolled by S so that every
+    // slot is a compile-time choice of LDS object
+    auto step = [&](auto I, int t) {
+        constexpr int slot = decltype(I)::value;
+        // refill the slot consumed in the previous stage (freed by the barrier)
+        dma(std::integral_constant<int, (slot + D) % S>{}, t + D, r);
+        stage_idx(t + D + 1, r);
+        const char *la = stage_a(I), *lb = stage_b(I);
+#pragma unroll
+        for (int ks = 0; ks < BKS / 16; ++ks) {
+            bf16x8_t a[FM], b[FN];
+            const int kb = ks * 16 * ROWB;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) a[i] = frag(la + aoff[i] + kb);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) b[j] = frag(lb + boff[j] + kb);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[j][i], 0, 0, 0);
+        }
+        // stage t+1 must have landed for every wave before the barrier;
+        // stages t+2 .. t+D may stay in flight
+        wait_vmcnt_le<(D - 1) * PER_STAGE>();
+        barrier();
+    };
+    int t0 = 0;
+    for (; t0 + S <= nT; t0 += S) {
+        step(I0{}, t0);
+        step(I1{}, t0 + 1);
+        if constexpr (S > 2) step(I2{}, t0 + 2);
+        if constexpr (S > 3) step(I3{}, t0 + 3);
+    }
+    if (t0 < nT) step(I0{}, t0);
+    if (t0 + 1 < nT) step(I1{}, t0 + 1);
+    if constexpr (S > 2) { if (t0 + 2 < nT) step(I2{}, t0 + 2); }
+    wait_vmcnt_le<0>();   // the out-of-range tail loads, before the block can exit
+
+    // acc[j][i][4*gq + r]: n = n0 + wn*TWN + 32j + 8gq + 4*(lane/32) + r,
+    //                      m = m0 + wm*128 + 32i + lane%32
+    const int lr = lane & 31, lh = lane >> 5;
+    uint16_t *Yu = Y + unit * static_cast<int64_t>(M) * ldy;
+    const int rows = min(BT, M - m0);
+    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+        Yu + static_cast<int64_t>(m0) * ldy, 0, static_cast<uint32_t>(rows * ldy * 2), 0x00020000);
+    const bool full_n = vec_y && n0 + BT <= N;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int ml = wm * 128 + 32 * i + lr;      // rows past M fall outside yr
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                const int n = n0 + wn * TWN + 32 * j + 8 * gq + 4 * lh;
+                const uint32_t w0 = pack_bf16x2(acc[j][i][4 * gq], acc[j][i][4 * gq + 1]);
+                const uint32_t w1 = pack_bf16x2(acc[j][i][4 * gq + 2], acc[j][i][4 * gq + 3]);
+                const uint32_t off = static_cast<uint32_t>((ml * ldy + n) * 2);
+                if (full_n) {
+                    typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{w0, w1}, yr, off, 0, 0);
+                } else {
+                    const uint16_t e[4] = {static_cast<uint16_t>(w0), static_cast<uint16_t>(w0 >> 16),
+                                           static_cast<uint16_t>(w1), static_cast<uint16_t>(w1 >> 16)};
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr)
+                        if (n + rr < N)
+                            __builtin_amdgcn_raw_buffer_store_b16(e[rr], yr, off + 2 * rr, 0, 0);
+                }
+            }
+        }
+}
+
 // ------------------------------------------------------------------ fp32
 template <int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void gemm_gather_f32_kernel(
@@ -587,6 +843,7 @@ hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t 
 }
 
 constexpr int kKmajorWaves = 8;
+constexpr int kTrWaves = 8, kTrRows = 32, kTrStages = 3;
 
 hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
                                   int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
@@ -594,7 +851,15 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                                   hipStream_t stream) {
     const int64_t xt_bytes = K * ldxt * 2, w_bytes = K * ldw * 2;
     const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
-    if (t256 * B >= 128) {
+    // Y rows of one 256-row tile are addressed with 32-bit byte offsets
+    if (t256 * B >= 128 && ldy < (int64_t(1) << 23)) {
+        const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
+        const int vec_y = reinterpret_cast<uintptr_t>(Y) % 8 == 0 && ldy % 4 == 0;
+        hipLaunchKernelGGL((gemm_kmajor_tr_kernel<kTrWaves, kTrRows, kTrStages>),
+                           dim3(tm * tn, static_cast<unsigned>(B)), dim3(kTrWaves * 64), 0, stream,
+                           Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
+                           static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, tn, vec_y);
+    } else if (t256 * B >= 128) {
         const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
         hipLaunchKernelGGL((gemm_kmajor_bf16_kernel<256, kKmajorWaves>),
                            dim3(tm * tn, static_cast<unsigned>(B)), dim3(kKmajorWaves * 64), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
