@@ -13,7 +13,7 @@ namespace rmm {
 // adds the splits in a fixed order.  Splits depend only on (B, M, K).
 constexpr int kScoreCols = 128;        // columns per workgroup
 constexpr int kScoreMinRows = 64;      // fewest rows per split
-constexpr int kScoreTargetBlocks = 1024;
+constexpr int kScoreTargetBlocks = 2048;
 
 int64_t score_rows_per_split(int64_t B, int64_t M, int64_t K);
 int64_t score_splits(int64_t B, int64_t M, int64_t K);

@@ -144,17 +144,130 @@ __global__ __launch_bounds__(kThreads) void score_partial_kernel(
     }
 }
 
+// bf16 rows with 16-byte aligned starts (ldx % 8 == 0): each wave reads a
+// 64-row x 64-column tile as eight 16-byte row vectors per lane (lanes
+// 8*mc + jc: rows 8*mc .. 8*mc+7, columns 8*jc .. 8*jc+7, so eight lanes
+// cover one 128-byte row segment), squares them into float64 column sums,
+// and, for the K-major copy, transposes its 8 x 8 block in registers and
+// stores eight 16-byte Xt vectors (eight lanes cover one 128-byte segment
+// of an Xt row).  The workgroup's four waves take tiles 64 rows apart;
+// their column sums are combined in a fixed order.
+constexpr int kStrip = 64;
+
+template <bool XT>
+__global__ __launch_bounds__(kThreads) void score_tile_kernel(
+    const uint16_t *__restrict__ X, int64_t M, int64_t K, int64_t ldx, int64_t rows_per_split,
+    double *__restrict__ out, int64_t out_unit_stride, int64_t out_split_stride,
+    uint16_t *__restrict__ Xt, int64_t ldxt) {
+    __shared__ double red[kThreads / 64][kStrip];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int jc = lane & 7, mc = lane >> 3;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * kStrip + 8 * jc;
+    const int64_t split = blockIdx.y, unit = blockIdx.z;
+    const int64_t r_begin = split * rows_per_split;
+    const int rows = static_cast<int>(min(M, r_begin + rows_per_split) - r_begin);
+    const int nvalid = static_cast<int>(max<int64_t>(0, min<int64_t>(8, K - j)));
+    // the split's rows as one buffer: rows past its end read zeros
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(X + (unit * M + r_begin) * ldx), 0,
+        static_cast<uint32_t>(rows * ldx * 2), 0x00020000);
+    constexpr uint32_t kOut = 0x80000000u;
+    const uint32_t col_off = nvalid > 0 ? static_cast<uint32_t>(j * 2) : kOut;
+    uint16_t *xt = XT ? Xt + (unit * K + j) * ldxt + r_begin : nullptr;
+
+    double acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    for (int m0 = wave * 64; m0 < rows; m0 += kThreads) {
+        uint4 v[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const uint32_t off = col_off == kOut ? kOut
+                               : static_cast<uint32_t>((m0 + 8 * mc + r) * ldx * 2) + col_off;
+            const auto q = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+            v[r] = make_uint4(q[0], q[1], q[2], q[3]);
+        }
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const uint32_t w[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const double x = e < nvalid
+                    ? static_cast<double>(__uint_as_float((e & 1) ? (w[e >> 1] & 0xffff0000u) : (w[e >> 1] << 16)))
+                    : 0.0;
+                acc[e] = fma(x, x, acc[e]);
+            }
+        }
+        if constexpr (XT) {
+            // column e of the 8 x 8 block becomes one 16-byte vector of Xt row j + e
+            const int mrow = m0 + 8 * mc;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+                uint32_t o[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t a = reinterpret_cast<const uint32_t *>(&v[2 * q])[e >> 1];
+                    const uint32_t b = reinterpret_cast<const uint32_t *>(&v[2 * q + 1])[e >> 1];
+                    o[q] = __builtin_amdgcn_perm(b, a, sel);
+                }
+                if (e < nvalid) {
+                    uint16_t *dst = xt + e * ldxt + mrow;
+                    if (mrow + 8 <= rows) {
+                        *reinterpret_cast<uint4 *>(dst) = make_uint4(o[0], o[1], o[2], o[3]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 8; ++r)
+                            if (mrow + r < rows) dst[r] = static_cast<uint16_t>(o[r >> 1] >> (16 * (r & 1)));
+                    }
+                }
+            }
+        }
+    }
+    // sum over the eight row groups of the wave (xor butterfly: every lane
+    // ends with the same, order-independent sum), then over the waves in order
+#pragma unroll
+    for (int sh = 8; sh < 64; sh <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], sh);
+    if (mc == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[wave][8 * jc + e] = acc[e];
+    }
+    __syncthreads();
+    if (threadIdx.x < kStrip) {
+        double s = red[0][threadIdx.x];
+#pragma unroll
+        for (int w = 1; w < kThreads / 64; ++w) s += red[w][threadIdx.x];
+        const int64_t col = static_cast<int64_t>(blockIdx.x) * kStrip + threadIdx.x;
+        if (col < K) out[unit * out_unit_stride + split * out_split_stride + col] = s;
+    }
+}
+
 // energy[b][j] = sum over splits s (in order) of partials[b][s][j]
-__global__ __launch_bounds__(kThreads) void score_finalize_kernel(
+__global__ __launch_bounds__(64) void score_finalize_kernel(
     const double *__restrict__ partials, int64_t B, int64_t S, int64_t K,
     double *__restrict__ energy) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * 64 + threadIdx.x;
     if (t >= B * K) return;
     const int64_t b = t / K, j = t % K;
     const double *p = partials + b * S * K + j;
     double s = 0.0;
+#pragma unroll 8
     for (int64_t i = 0; i < S; ++i) s += p[i * K];
     energy[t] = s;
+}
+
+template <bool XT>
+hipError_t launch_tiles(const uint16_t *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                        int64_t S, double *out, int64_t unit_stride, int64_t split_stride,
+                        uint16_t *Xt, int64_t ldxt, hipStream_t stream) {
+    const int64_t rps = score_rows_per_split(B, M, K);
+    dim3 grid(static_cast<unsigned>((K + kStrip - 1) / kStrip), static_cast<unsigned>(S),
+              static_cast<unsigned>(B));
+    hipLaunchKernelGGL((score_tile_kernel<XT>), grid, dim3(kThreads), 0, stream, X, M, K, ldx, rps,
+                       out, unit_stride, split_stride, Xt, ldxt);
+    return hipGetLastError();
 }
 
 template <typename T, int VEC, bool XT>
@@ -172,9 +285,9 @@ hipError_t launch_partial(const T *X, int64_t B, int64_t M, int64_t K, int64_t l
 }  // namespace
 
 // Rows per split: a whole number of 64-row slabs, chosen so that the grid
-// has about kScoreTargetBlocks workgroups.
+// of 64-column strips has about kScoreTargetBlocks workgroups.
 int64_t score_rows_per_split(int64_t B, int64_t M, int64_t K) {
-    const int64_t col_blocks = (K + kScoreCols - 1) / kScoreCols;
+    const int64_t col_blocks = (K + kStrip - 1) / kStrip;
     int64_t s = (kScoreTargetBlocks + B * col_blocks - 1) / (B * col_blocks);
     const int64_t max_s = (M + kScoreMinRows - 1) / kScoreMinRows;
     if (s > max_s) s = max_s;
@@ -204,13 +317,21 @@ hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t 
     const size_t esz = bf16 ? 2 : 4;
     const bool aligned = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                          ((ldx * static_cast<int64_t>(esz)) % 16 == 0);
+    // the tile kernel addresses one split's rows with 32-bit byte offsets
+    const bool tiles = bf16 && aligned &&
+                       score_rows_per_split(B, M, K) * ldx * 2 < (int64_t(1) << 31);
     hipError_t err;
-    if (Xt) {   // bf16, 16-byte aligned rows (checked by the caller)
+    if (Xt && tiles) {   // bf16, 16-byte aligned rows (checked by the caller)
+        err = launch_tiles<true>(static_cast<const uint16_t *>(X), B, M, K, ldx, S, out, unit_stride,
+                                 split_stride, Xt, ldxt, stream);
+    } else if (Xt) {
         err = launch_partial<uint16_t, 8, true>(static_cast<const uint16_t *>(X), B, M, K, ldx, S, out,
                                                 unit_stride, split_stride, Xt, ldxt, stream);
     } else if (bf16) {
         const uint16_t *x = static_cast<const uint16_t *>(X);
-        err = aligned ? launch_partial<uint16_t, 8, false>(x, B, M, K, ldx, S, out, unit_stride,
+        err = tiles ? launch_tiles<false>(x, B, M, K, ldx, S, out, unit_stride, split_stride, nullptr,
+                                          0, stream)
+            : aligned ? launch_partial<uint16_t, 8, false>(x, B, M, K, ldx, S, out, unit_stride,
                                                            split_stride, nullptr, 0, stream)
                       : launch_partial<uint16_t, 1, false>(x, B, M, K, ldx, S, out, unit_stride,
                                                            split_stride, nullptr, 0, stream);
@@ -223,8 +344,8 @@ hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t 
     }
     if (err != hipSuccess || S == 1) return err;
     const int64_t n = B * K;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(static_cast<unsigned>((n + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, stream, partials, B, S, K, energy);
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(static_cast<unsigned>((n + 63) / 64)), dim3(64), 0,
+                       stream, partials, B, S, K, energy);
     return hipGetLastError();
 }
 
