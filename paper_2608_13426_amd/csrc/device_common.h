@@ -35,6 +35,18 @@ constexpr int kWave = 64;
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
+// Workgroup barrier for LDS hand-offs.  __syncthreads() also waits for every
+// outstanding global load and store of the wave (its workgroup-scope fence),
+// which stalls a kernel that streams stores out while it computes; this one
+// waits only for the wave's own LDS accesses, and no instruction is
+// scheduled across it.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // The two gfx950 LDS instructions below exist only in the device pass; the
 // host pass of a kernel that names them directly drops the kernel's launch
 // stub, so they are wrapped here.

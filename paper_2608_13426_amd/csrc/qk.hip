@@ -296,33 +296,31 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
                         *reinterpret_cast<uint2 *>(&out_lds[ql * OS + kl]) = make_uint2(w0, w1);
                     }
                 }
-            __syncthreads();
+            lds_barrier();
 #pragma unroll
             for (int i = 0; i < BQ / 16; ++i) {
                 const int r = r16 + 16 * i;
                 const int col = kt * BT + c16 * 8;
-                if (col < Lk) {
-                    const uint4 v = *reinterpret_cast<const uint4 *>(&out_lds[r * OS + c16 * 8]);
-                    __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{v.x, v.y, v.z, v.w}, sr,
-                        static_cast<uint32_t>((r * Lk + col) * 2), 0, kStoreAux);
-                }
+                // unconditional (a column past Lk goes out of range): a branch
+                // here would make the compiler's wait for the next K rows also
+                // wait for these stores
+                const uint32_t off = col < Lk ? static_cast<uint32_t>((r * Lk + col) * 2) : 0x80000000u;
+                const uint4 v = *reinterpret_cast<const uint4 *>(&out_lds[r * OS + c16 * 8]);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{v.x, v.y, v.z, v.w}, sr, off, 0, kStoreAux);
             }
             if (kt + 1 < n_compute) store_rows();
-            __syncthreads();
+            lds_barrier();
         }
     }
-    // key tiles wholly above the diagonal
+    // key tiles wholly above the diagonal: one contiguous run per row, each
+    // wave writing whole rows with 1 KiB per store instruction
     const uint32_t ninf2 = 0xff80ff80u;
-    for (int kt = n_compute; kt < n_tiles; ++kt) {
-#pragma unroll
-        for (int i = 0; i < BQ / 16; ++i) {
-            const int r = r16 + 16 * i;
-            const int col = kt * BT + c16 * 8;
-            if (col < Lk)
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{ninf2, ninf2, ninf2, ninf2}, sr,
-                    static_cast<uint32_t>((r * Lk + col) * 2), 0, kStoreAux);
-        }
-    }
+    const int c0 = n_compute * BT;
+    const int nv = (Lk - c0) / 8;                 // 16-byte vectors per row (Lk % 8 == 0)
+    for (int r = wave; r < BQ; r += NT / 64)
+        for (int v = lane; v < nv; v += 64)
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{ninf2, ninf2, ninf2, ninf2}, sr,
+                static_cast<uint32_t>((r * Lk + c0 + 8 * v) * 2), 0, kStoreAux);
 }
 
 template <int BM, int BN, int BK>

@@ -258,6 +258,30 @@ def test_reduced_gemm_kmajor(B, M, N, K, k, seed):
         check_product(Yn[b], ref, np.abs(X[b][:, idx[b]]) @ np.abs(W[idx[b], :]), k, "bf16")
 
 
+@pytest.mark.parametrize("pad", [3, 8])
+def test_reduced_gemm_kmajor_strided_y(pad):
+    """256-wide tiles with Y rows longer than N: an odd row stride takes the
+    element-wise store path; nothing is written past column N."""
+    dev = require_gpu()
+    B, M, N, K, k = 3, 2050, 1030, 300, 150
+    Xs = wl.random_case(60 + pad, (B, M, K), "bf16", n_outlier=8)
+    Ws = wl.random_case(61 + pad, (K, N + 2), "bf16", std=0.02)     # W rows 16-byte aligned
+    idx = _ascending(62 + pad, B, K, k)
+    ldxt = _ld8(M)
+    Xt_host = np.zeros((B, K, ldxt), dtype=np.uint16)
+    Xt_host[:, :, :M] = Xs.transpose(0, 2, 1)
+    Xtd = to_device(Xt_host, "bf16", dev)[:, :, :M]
+    Yfull = torch.full((B, M, N + pad), 7.0, dtype=torch.bfloat16, device=dev)
+    rmm.rmm_reduced_gemm_kmajor(Xtd, to_device(Ws, "bf16", dev)[:, :N],
+                                torch.from_numpy(idx.astype(np.int32)).to(dev), Yfull[:, :, :N])
+    Y = from_device(Yfull)
+    assert np.all(Y[:, :, N:] == 7.0)
+    X, W = wl.decode(Xs, "bf16").astype(np.float64), wl.decode(Ws, "bf16").astype(np.float64)[:, :N]
+    for b in range(B):
+        ref = ro.reduced_matmul(X[b], W, idx[b])
+        check_product(Y[b, :, :N], ref, np.abs(X[b][:, idx[b]]) @ np.abs(W[idx[b], :]), k, "bf16")
+
+
 def test_reduced_gemm_strided_operands():
     """Leading dimensions larger than the logical widths."""
     dev = require_gpu()
