@@ -5,10 +5,11 @@ One step = one pass of the whole reduced path of an 8B-class decoder layer
 retention ratio r, on synthetic bf16 inputs already resident in HBM:
 
   * q/k/v  : energies of the attention input (the scoring pass also writes
-             its K-major copy), TopK, three gathered GEMMs (the three
-             projections read one input, so they share one set)
+             its K-major copy), TopK, one gathered GEMM over the q|k|v weights
+             stored concatenated along N (the three projections read one
+             input, so they share one set)
   * o      : energies, TopK, gathered GEMM
-  * gate/up: energies of the MLP input, TopK, two gathered GEMMs
+  * gate/up: energies of the MLP input, TopK, one gathered GEMM (gate|up)
   * down   : energies, TopK, gathered GEMM
   * QK^T   : per-head energies of Q, TopK per head, reduced QK^T (causal)
 
@@ -53,8 +54,7 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
 # dispatches, from two rocprofv3 --pmc runs (FETCH_SIZE x2.0, WRITE_SIZE x1.0:
 # the factors a 512 MiB device copy reads).  Valid for the gemm.hip whose
 # SHA-256 is recorded; None until measured.
-GEMM_TRAFFIC = {"gemm_hip_sha256": "72dbcdbafdde24c62b0e5bb8237c112b3aecc5b888cb5810092f0f2eba4b086b",
-                "bytes_per_launch": round((277646.72 * 2.0 + 130548.98) * 1024)}
+GEMM_TRAFFIC = None
 
 
 def parse():
@@ -102,18 +102,27 @@ class Layer:
         # K-major copies written by the scoring pass
         self.Xt = {name: torch.empty((v[0], self.M), dtype=torch.bfloat16, device=dev)
                    for name, v in wk.inputs.items()}
-        self.W = {p.name: put(wl.workload_weight(wk, p)) for p in wk.projections}
-        self.Y = {p.name: torch.empty((self.M, p.N), dtype=torch.bfloat16, device=dev)
-                  for p in wk.projections}
+        # groups of projections that read one input (q|k|v, gate|up): their
+        # weights are stored concatenated along N, so one GEMM launch per
+        # group computes all of them (the same retained rows serve each)
+        self.groups = {}
+        for p in wk.projections:
+            self.groups.setdefault(p.input_name, []).append(p)
+        self.Wcat, self.Ycat, self.W, self.Y = {}, {}, {}, {}
+        for name, projs in self.groups.items():
+            self.Wcat[name] = torch.cat([put(wl.workload_weight(wk, p)) for p in projs], dim=1)
+            self.Ycat[name] = torch.empty((self.M, sum(p.N for p in projs)), dtype=torch.bfloat16,
+                                          device=dev)
+            off = 0
+            for p in projs:
+                self.W[p.name] = self.Wcat[name][:, off:off + p.N]
+                self.Y[p.name] = self.Ycat[name][:, off:off + p.N]
+                off += p.N
         a = wk.attention
         q, k = wl.workload_qk(wk)
         self.Q = put(q).reshape(1, a.H, a.L, a.D)
         self.Kc = put(k).reshape(1, a.Hkv, a.L, a.D)
         self.S = torch.empty((1, a.H, a.L, a.L), dtype=torch.bfloat16, device=dev)
-        # groups of projections that read one input
-        self.groups = {}
-        for p in wk.projections:
-            self.groups.setdefault(p.input_name, []).append(p)
         Kmax = max(v[0] for v in wk.inputs.values())
         import paper_2608_13426_amd as rmm
         ws = max(rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 1, self.M, Kmax),
@@ -148,15 +157,13 @@ def run_step(L, r, gemm_events=None):
         if L.idx[name] is None or L.idx[name].numel() != k:
             L.idx[name] = torch.empty(k, dtype=torch.int32, device=L.dev)
         rmm.rmm_select(e, k, L.idx[name])
-        for p in projs:
-            if gemm_events is not None:
-                ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                ev0.record()
-            rmm.rmm_reduced_gemm_kmajor(L.Xt[name], L.W[p.name], L.idx[name].view(1, k),
-                                        L.Y[p.name])
-            if gemm_events is not None:
-                ev1.record()
-                gemm_events.append((ev0, ev1, 2 * wk.M * p.N * k))
+        if gemm_events is not None:
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ev0.record()
+        rmm.rmm_reduced_gemm_kmajor(L.Xt[name], L.Wcat[name], L.idx[name].view(1, k), L.Ycat[name])
+        if gemm_events is not None:
+            ev1.record()
+            gemm_events.append((ev0, ev1, 2 * wk.M * L.Ycat[name].shape[1] * k))
     a = wk.attention
     kq = rmm.rmm_retained_count(r, a.D)
     e = L.energy[:a.H * a.D]
