@@ -168,7 +168,10 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bh = blockIdx.y, b = bh / H, h = bh % H, g = h / (H / Hkv);
-    const int q0 = blockIdx.x * BQ;
+    // causal: the last query tiles carry the most key tiles, so they are
+    // dealt first (longest work first keeps the tail of the grid short)
+    const int qt = causal ? static_cast<int>(gridDim.x) - 1 - static_cast<int>(blockIdx.x) : blockIdx.x;
+    const int q0 = qt * BQ;
     const int off = Lk - Lq;
     const int32_t *I = idx + static_cast<int64_t>(bh) * k;
     uint16_t *Sh = S + static_cast<int64_t>(bh) * Lq * Lk;
