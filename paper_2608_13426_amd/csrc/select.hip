@@ -5,8 +5,9 @@
 // 64-bit key whose unsigned order is the order of the values (NaN above
 // +inf, -0 == +0), so the whole selection is integer work: an MSB-first
 // radix select with 8-bit digits finds the k-th largest key, using LDS
-// histograms with integer atomics (order-independent counts).  It stops as
-// soon as the bucket holding the k-th key is taken whole.  Keys tied with
+// histograms with integer atomics (order-independent counts).  It starts
+// below the leading bits every key shares and stops as soon as the bucket
+// holding the k-th key is taken whole.  Keys tied with
 // the k-th key are taken lowest index first, and the kept indices are
 // compacted in ascending order with two workgroup prefix scans.  Each thread
 // owns a contiguous chunk of keys, kept in registers when it fits.
@@ -87,20 +88,57 @@ __global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ e
     };
     const int n_own = static_cast<int>(max<int64_t>(0, min<int64_t>(chunk, K - c0)));
 
-    uint64_t prefix = 0, mask = 0;
+    // The leading bits shared by every key need no pass (energies of one
+    // unit usually share sign and most of the exponent): take the
+    // workgroup's smallest and largest key and start below their common
+    // prefix, so the first pass already spreads the keys over its buckets.
+    uint64_t kmin = ~0ull, kmax = 0;
+    for (int c = 0; c < n_own; ++c) {
+        const uint64_t u = key_at(c);
+        kmin = u < kmin ? u : kmin;
+        kmax = u > kmax ? u : kmax;
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint64_t a = __shfl_xor(kmin, o, kWave), b = __shfl_xor(kmax, o, kWave);
+        kmin = a < kmin ? a : kmin;
+        kmax = b > kmax ? b : kmax;
+    }
+    __shared__ uint64_t s_min[NT / kWave], s_max[NT / kWave];
+    if ((tid & (kWave - 1)) == 0) { s_min[tid / kWave] = kmin; s_max[tid / kWave] = kmax; }
+    __syncthreads();
+    kmin = s_min[0];
+    kmax = s_max[0];
+#pragma unroll
+    for (int w = 1; w < NT / kWave; ++w) {
+        kmin = s_min[w] < kmin ? s_min[w] : kmin;
+        kmax = s_max[w] > kmax ? s_max[w] : kmax;
+    }
+    uint64_t prefix, mask;
+    int top;                                        // highest bit not yet fixed
+    if (kmin == kmax) {
+        prefix = kmin; mask = ~0ull; top = -1;       // all keys equal: ties by index
+    } else {
+        top = 63 - __builtin_clzll(kmin ^ kmax);
+        mask = top == 63 ? 0ull : (~0ull << (top + 1));
+        prefix = kmax & mask;
+    }
     uint32_t need = static_cast<uint32_t>(k);
-    for (int shift = 56; shift >= 0; shift -= 8) {
+    while (top >= 0) {
+        // digit: bits top .. shift (up to 8 of them)
+        const int shift = max(0, top - 7);
+        const uint64_t dmask = (1ull << (top - shift + 1)) - 1;
         for (int i = tid; i < 256; i += NT) hist[i] = 0;
         __syncthreads();
         if constexpr (REG) {
 #pragma unroll
             for (int c = 0; c < C; ++c)
                 if (c < n_own && (keys[c] & mask) == prefix)
-                    atomicAdd(&hist[(keys[c] >> shift) & 0xff], 1u);
+                    atomicAdd(&hist[(keys[c] >> shift) & dmask], 1u);
         } else {
             for (int c = 0; c < n_own; ++c) {
                 const uint64_t u = key_at(c);
-                if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 0xff], 1u);
+                if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & dmask], 1u);
             }
         }
         __syncthreads();
@@ -127,7 +165,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ e
         __syncthreads();
         need -= s_above;
         prefix |= static_cast<uint64_t>(s_digit) << shift;
-        mask |= 0xffull << shift;
+        mask |= dmask << shift;
+        top = shift - 1;
         if (s_count == need) break;      // the whole bucket is kept
     }
 
