@@ -41,6 +41,8 @@ def _energies_gpu(Xd, B, M, K, dev):
     ("bf16", 1, 5000, 8, 0, 6),
     ("bf16", 4, 64, 2000, 8, 7),
     ("f32", 1, 3000, 1030, 2, 8),
+    ("bf16", 2, 1000, 300, 4, 9),      # 16-byte rows, K % 8 != 0: partial column group
+    ("bf16", 1, 70, 1030, 2, 10),      # a split shorter than one 64-row tile
 ])
 def test_score(dtype, B, M, K, pad, seed):
     dev = require_gpu()
@@ -108,6 +110,29 @@ def test_score_kmajor(B, M, K, seed):
     assert np.all(got[:, :, M:] == 0xbf80)          # padding columns untouched
     e_ref = ro.column_energies(wl.decode(stored, "bf16")[0].astype(np.float64))
     check_energies(e2.cpu().numpy()[:K], e_ref, M)
+
+
+@pytest.mark.parametrize("B,M,K,pad,seed", [(2, 1000, 300, 4, 0), (1, 333, 1030, 2, 1)])
+def test_score_kmajor_ragged_k(B, M, K, pad, seed):
+    """K not a multiple of 8 (rows padded to 16 bytes): the last column group
+    is partial; only the K real rows of Xt are written."""
+    dev = require_gpu()
+    stored = wl.random_case(80 + seed, (B, M, K + pad), "bf16", n_outlier=max(1, K // 50))
+    Xd = to_device(stored, "bf16", dev)[:, :, :K]
+    e1 = _energies_gpu(Xd, B, M, K, dev)
+    ldxt = _ld8(M)
+    Xt_flat = torch.full((B * K + 1, ldxt), -1.0, dtype=torch.bfloat16, device=dev)  # + sentinel row
+    Xt = Xt_flat[:B * K].view(B, K, ldxt)[:, :, :M]
+    e2 = torch.empty(B * K, dtype=torch.float64, device=dev)
+    rmm.rmm_score_kmajor(Xd, e2, Xt, _score_ws(B, M, K, dev))
+    assert torch.equal(e1, e2)
+    flat = Xt_flat.view(torch.int16).cpu().numpy().view(np.uint16)
+    got = flat[:B * K].reshape(B, K, ldxt)
+    assert np.array_equal(got[:, :, :M], np.ascontiguousarray(stored[:, :, :K].transpose(0, 2, 1)))
+    assert np.all(flat[B * K] == 0xbf80) and np.all(got[:, :, M:] == 0xbf80)
+    for b in range(B):
+        e_ref = ro.column_energies(wl.decode(stored[b, :, :K], "bf16").astype(np.float64))
+        check_energies(e2.cpu().numpy()[b * K:(b + 1) * K], e_ref, M)
 
 
 # ----------------------------------------------------------------- select
