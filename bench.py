@@ -53,8 +53,11 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
 # HBM bytes per launch of GEMM_KERNEL in the default command, averaged over its
 # dispatches, from two rocprofv3 --pmc runs (FETCH_SIZE x2.0, WRITE_SIZE x1.0:
 # the factors a 512 MiB device copy reads).  Valid for the gemm.hip whose
-# SHA-256 is recorded; None until measured.
-GEMM_TRAFFIC = None
+# SHA-256 is recorded and for the same launch mix (workload, ratios, one
+# launch per input group).
+GEMM_TRAFFIC = {"gemm_hip_sha256": "72dbcdbafdde24c62b0e5bb8237c112b3aecc5b888cb5810092f0f2eba4b086b",
+                "mix": "layer_8b r=0.5,1.0 grouped",
+                "bytes_per_launch": round((480461.50 * 2.0 + 227442.45) * 1024)}
 
 
 def parse():
@@ -73,9 +76,10 @@ def parse():
     return p.parse_args()
 
 
-def gemm_traffic():
-    """Recorded HBM bytes per launch of the GEMM, if its source is unchanged."""
-    if GEMM_TRAFFIC is None:
+def gemm_traffic(mix):
+    """Recorded HBM bytes per launch of the GEMM, if its source and launch mix
+    are the ones measured."""
+    if GEMM_TRAFFIC is None or GEMM_TRAFFIC["mix"] != mix:
         return None
     with open(GEMM_SOURCE, "rb") as f:
         if hashlib.sha256(f.read()).hexdigest() != GEMM_TRAFFIC["gemm_hip_sha256"]:
@@ -304,7 +308,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": GEMM_KERNEL,
                      "achieved": round(roof_ach, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(roof_ach / PEAK_BF16_TFLOPS, 4),
-                     "traffic": gemm_traffic(),
+                     "traffic": gemm_traffic(f"{wk.name} r={','.join(str(r) for r in sorted(sweep))} grouped"),
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE)",
                      "launches": g_n,
                      "avg_launch_us": round(g_ms * 1e3 / g_n, 2),
