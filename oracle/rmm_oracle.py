@@ -46,6 +46,9 @@ Readings where the paper is silent (each also listed in the design notes):
 * Causal mask: entry (i, t) is masked iff t > i + (Lk - Lq) (bottom-right
   aligned); masked entries are -inf, so softmax(S + M) is softmax of S with
   those entries removed.
+* Reduced attention block (softmax(S + M) V with the reduced S): a query row
+  whose keys are all masked (only when Lq > Lk) has no weights; its output
+  is 0.
 """
 from __future__ import annotations
 
@@ -55,7 +58,7 @@ import numpy as np
 
 __all__ = [
     "retained_count", "column_energies", "topk_indices", "reduced_matmul",
-    "rmm", "rmm_batched", "gqa_kv_head", "reduced_qk", "rmm_qk",
+    "rmm", "rmm_batched", "gqa_kv_head", "reduced_qk", "rmm_qk", "reduced_attention",
     "residual_energy", "retained_energy_fraction", "discarded_energy_ratio",
     "rank_one_bound", "factorized_bound", "normalized_bound",
     "selection_margin",
@@ -208,6 +211,36 @@ def rmm_qk(Q: np.ndarray, K: np.ndarray, r: float, causal: bool):
     e = np.stack([column_energies(Q[h]) for h in range(H)])
     idx = np.stack([topk_indices(e[h], k) for h in range(H)])
     return reduced_qk(Q, K, idx, causal), idx, e
+
+
+def reduced_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, idx: np.ndarray,
+                      causal: bool, rows=None) -> np.ndarray:
+    """O[h] = softmax(S[h] + M) V[g(h)] with the reduced scores S (Sec. 3.3).
+
+    The attention block the paper places RMM in: the reduced scores of
+    ``reduced_qk`` (the mask's -inf entries drop out of the softmax), then
+    each query row averages the value rows of its kv head with the softmax
+    weights.  Q [H x Lq x D], K [Hkv x Lk x D], V [Hkv x Lk x Dv], idx [H x k]
+    -> O [H x Lq x Dv] float64.  A query row with every key masked (only
+    possible when Lq > Lk) has no weights; its output is 0.  With ``rows``,
+    only those query rows are computed.
+    """
+    V = np.asarray(V, dtype=np.float64)
+    H = np.asarray(Q).shape[0]
+    Hkv = np.asarray(K).shape[0]
+    S = reduced_qk(Q, K, idx, causal, rows)
+    O = np.zeros((H, S.shape[1], V.shape[2]), dtype=np.float64)
+    for h in range(H):
+        g = gqa_kv_head(h, H, Hkv)
+        for i in range(S.shape[1]):
+            s = S[h, i]
+            keep = s != -np.inf                      # masked entries are -inf
+            if not keep.any():
+                continue
+            w = np.zeros_like(s)
+            w[keep] = np.exp(s[keep] - s[keep].max())
+            O[h, i] = (w / w.sum()) @ V[g]
+    return O
 
 
 # ---------------------------------------------------------------------------

@@ -353,6 +353,61 @@ def check_qk(o):
         assert np.allclose(S[h][~m], want[~m], rtol=0, atol=1e-14 * (1 + np.abs(want).max()))
 
 
+def check_attention(o):
+    """Reduced attention block (Sec. 3.3): softmax of the reduced, masked
+    scores, then the weighted average of the value rows."""
+    # two keys, one retained dim: weights 1/(1+e^(s1-s0)) with s_t = a*K[t,0]/sqrt(D);
+    # the other dims (5s) would change the result if they were not dropped
+    D, a = 4, 1.5
+    Q = np.zeros((1, 1, D)); Q[0, 0, 0] = a
+    K = np.array([[[1.0, 5, 5, 5], [2.0, 5, 5, 5]]])
+    V = np.array([[[1.0, -2.0], [3.0, 4.0]]])
+    O = o.reduced_attention(Q, K, V, np.array([[0]]), causal=False)
+    s0, s1 = a * 1.0 / math.sqrt(D), a * 2.0 / math.sqrt(D)
+    w0 = 1.0 / (1.0 + math.exp(s1 - s0))
+    assert np.allclose(O[0, 0], w0 * V[0, 0] + (1 - w0) * V[0, 1], rtol=1e-14, atol=0)
+    # all scores equal (Q = 0): the mean of the unmasked value rows (causal
+    # prefix means, bottom-right aligned); Lq > Lk leaves fully masked rows at 0
+    H, Hkv, Lq, Lk, D = 2, 1, 6, 4, 8
+    V = _bf16(80, (Hkv, Lk, 3))
+    O = o.reduced_attention(np.zeros((H, Lq, D)), _bf16(81, (Hkv, Lk, D)), V,
+                            np.stack([np.arange(4)] * H), causal=True)
+    for h in range(H):
+        for i in range(Lq):
+            n = i + (Lk - Lq) + 1
+            want = V[0][:n].mean(axis=0) if n > 0 else np.zeros(3)
+            assert np.allclose(O[h, i], want, rtol=1e-14, atol=1e-15)
+    # value rows of ones: every row with a key sums its weights to 1
+    Q, K = _bf16(82, (3, 5, 16)), _bf16(83, (1, 7, 16))
+    idx = np.stack([np.arange(0, 16, 3)] * 3)
+    O = o.reduced_attention(Q, K, np.ones((1, 7, 4)), idx, causal=True)
+    assert np.allclose(O, 1.0, rtol=1e-14, atol=0)
+    # causality: value and key rows past i + (Lk - Lq) do not reach row i
+    V = _bf16(84, (1, 7, 4))
+    O1 = o.reduced_attention(Q, K, V, idx, causal=True)
+    K2, V2 = K.copy(), V.copy()
+    K2[0, 6] += 7.0; V2[0, 6] -= 9.0                     # key 6: only row 4 sees it
+    O2 = o.reduced_attention(Q, K2, V2, idx, causal=True)
+    assert np.array_equal(O1[:, :4], O2[:, :4]) and not np.allclose(O1[:, 4], O2[:, 4])
+    # each output lies in the hull of the value rows it averages
+    assert np.all(O1 >= V[0].min(axis=0) - 1e-12) and np.all(O1 <= V[0].max(axis=0) + 1e-12)
+    # non-causal: permuting key and value rows together changes nothing
+    perm = np.array([3, 0, 6, 1, 5, 2, 4])
+    Oa = o.reduced_attention(Q, K, V, idx, causal=False)
+    Ob = o.reduced_attention(Q, K[:, perm], V[:, perm], idx, causal=False)
+    assert np.allclose(Oa, Ob, rtol=1e-13, atol=1e-15)
+    # GQA: a query head reads the value rows of kv head h // (H / Hkv)
+    V = np.stack([np.full((7, 2), g + 1.0) for g in range(2)])
+    O = o.reduced_attention(_bf16(85, (4, 5, 16)), _bf16(86, (2, 7, 16)), V,
+                            np.stack([np.arange(6)] * 4), causal=True)
+    for h in range(4):
+        assert np.allclose(O[h], h // 2 + 1.0, rtol=1e-14, atol=0)
+    # rows computed one by one are the same rows
+    Or = o.reduced_attention(Q, K, V[:1], idx, causal=True, rows=[4, 1])
+    Of = o.reduced_attention(Q, K, V[:1], idx, causal=True)
+    assert np.array_equal(Or[:, 0], Of[:, 4]) and np.array_equal(Or[:, 1], Of[:, 1])
+
+
 def check_margin(o):
     assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
     assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
@@ -361,4 +416,4 @@ def check_margin(o):
 
 
 ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
-              check_bounds, check_worked_example, check_qk, check_margin)
+              check_bounds, check_worked_example, check_qk, check_attention, check_margin)

@@ -149,7 +149,55 @@ def _rmm_qk_scores_k(Q, K, r, causal):
     return ro.reduced_qk(Q, K, idx, causal), idx, e
 
 
+def _attn_patch(weights, value_head):
+    """reduced_attention with the per-row weights or the value head replaced."""
+    def f(Q, K, V, idx, causal, rows=None):
+        V = np.asarray(V, dtype=np.float64)
+        H, Hkv = np.asarray(Q).shape[0], np.asarray(K).shape[0]
+        S = ro.reduced_qk(Q, K, idx, causal, rows)
+        O = np.zeros((H, S.shape[1], V.shape[2]))
+        for h in range(H):
+            W = weights(S[h])
+            O[h] = np.nan_to_num(W) @ V[value_head(h, H, Hkv)]
+        return O
+    return f
+
+
+def _w_softmax(S):
+    out = np.zeros_like(S)
+    for i, s in enumerate(S):
+        keep = s != -np.inf
+        if keep.any():
+            w = np.exp(s[keep] - s[keep].max())
+            out[i, keep] = w / w.sum()
+    return out
+
+
+def _w_over_queries(S):
+    E = np.where(S == -np.inf, 0.0, np.exp(np.where(S == -np.inf, 0.0, S)))
+    return E / np.maximum(E.sum(axis=0, keepdims=True), 1e-300)
+
+
+def _w_unnormalised(S):
+    return np.where(S == -np.inf, 0.0, np.exp(np.where(S == -np.inf, 0.0, S)))
+
+
+def _w_mask_as_zero(S):
+    return _w_softmax(np.where(S == -np.inf, 0.0, S))
+
+
+_gqa = lambda h, H, Hkv: h // (H // Hkv)
+_attn_over_queries = _attn_patch(_w_over_queries, _gqa)
+_attn_unnormalised = _attn_patch(_w_unnormalised, _gqa)
+_attn_mask_as_zero = _attn_patch(_w_mask_as_zero, _gqa)
+_attn_gqa_modulo = _attn_patch(_w_softmax, lambda h, H, Hkv: h % Hkv)
+
+
 MUTANTS = {
+    "attn_softmax_over_queries": ("reduced_attention", _attn_over_queries),
+    "attn_unnormalised": ("reduced_attention", _attn_unnormalised),
+    "attn_mask_as_zero_score": ("reduced_attention", _attn_mask_as_zero),
+    "attn_gqa_modulo": ("reduced_attention", _attn_gqa_modulo),
     "k_plain_ceil": ("retained_count", _k_plain_ceil),
     "k_round": ("retained_count", _k_round),
     "k_no_domain_check": ("retained_count", _k_no_domain),
