@@ -206,6 +206,29 @@ rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx,
                             hipStream_t stream);
 
 /*
+ * Reduced attention block   (Sec. 3.3 "Attention": the reduced scores feed
+ * the softmax of the attention block, which then weights the value rows).
+ *
+ * O[b,h,i,:] = sum_t P[i,t] V[b,g,t,:],  P[i,:] = softmax(S[b,h,i,:] + M[i,:]),
+ * with S the reduced scores of rmm_reduced_qk (same idx, scale, GQA map
+ * g = h / (H / Hkv) and causal mask); S is never written to memory.  A query
+ * row whose keys are all masked (only when Lq > Lk) gets O = 0.
+ *
+ * Q   : [batch][H][Lq][D]    Kc, V : [batch][Hkv][Lk][D]    O : [batch][H][Lq][D]
+ *       (contiguous; the value rows have the head dimension D).
+ * idx : int32 [batch*H*k], each head's list ascending (from rmm_select).
+ * Scores and the softmax are computed in fp32, the weights rounded to bf16
+ * for the value product, fp32 accumulation, bf16 output.
+ * Errors: INVALID_ARGUMENT as rmm_reduced_qk; UNSUPPORTED unless dtype is
+ *         RMM_BF16, D == 128 and Q, Kc, V, O are 16-byte aligned.
+ */
+rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
+                                   const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
+                                   int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
+                                   int64_t D, int64_t k, float scale, int causal, void *O,
+                                   hipStream_t stream);
+
+/*
  * Fused RMM projection   (Sec. 3.2 + Sec. 3.3 "MLP and linear projections").
  *
  * k = rmm_retained_count(r, K); then score -> rmm_select -> gathered GEMM

@@ -19,7 +19,7 @@ __all__ = [
     "RMM_OP_SELECT", "RMM_OP_LINEAR", "rmm_retained_count", "rmm_workspace_size",
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
-    "EXPORTED_SYMBOLS",
+    "rmm_reduced_attention", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -46,6 +46,9 @@ _SIGS = {
                                         ctypes.c_size_t, _p]),
     "rmm_reduced_gemm_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64,
                                                _i64, _p, _i64, _p]),
+    "rmm_reduced_attention": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64,
+                                             _i64, _i64, _i64, ctypes.c_float, ctypes.c_int, _p,
+                                             _p]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -259,6 +262,38 @@ def rmm_reduced_qk(Q: torch.Tensor, Kc: torch.Tensor, idx: torch.Tensor, S: torc
         Q.data_ptr(), Kc.data_ptr(), idx.data_ptr(), _dtype_code(Q), batch, H, Hkv, Lq, Lk, D,
         k, float(scale), 1 if causal else 0, S.data_ptr(), _stream(d, stream)))
     return S
+
+
+def rmm_reduced_attention(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor, idx: torch.Tensor,
+                          O: torch.Tensor, causal: bool = True, scale: float | None = None,
+                          stream=None) -> torch.Tensor:
+    """softmax(reduced scores + mask) V for Q [batch, H, Lq, D], Kc and V
+    [batch, Hkv, Lk, D], idx [batch, H, k]; writes O [batch, H, Lq, D]."""
+    if Q.dim() == 3:
+        Q, Kc, V, O = Q.unsqueeze(0), Kc.unsqueeze(0), V.unsqueeze(0), O.unsqueeze(0)
+    batch, H, Lq, D = Q.shape
+    bk, Hkv, Lk, Dk = Kc.shape
+    d = _dev(Q, Kc, V, idx, O)
+    if bk != batch or Dk != D:
+        raise ValueError("Kc must be [batch, Hkv, Lk, D]")
+    if tuple(V.shape) != (batch, Hkv, Lk, D):
+        raise ValueError("V must be [batch, Hkv, Lk, D]")
+    if tuple(O.shape) != (batch, H, Lq, D):
+        raise ValueError("O must be [batch, H, Lq, D]")
+    for t, n in ((Q, "Q"), (Kc, "Kc"), (V, "V"), (O, "O"), (idx, "idx")):
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    if not (Q.dtype == Kc.dtype == V.dtype == O.dtype):
+        raise TypeError("Q, Kc, V and O must share one dtype")
+    if idx.dtype != torch.int32 or idx.numel() % (batch * H):
+        raise ValueError("idx must be int32 [batch, H, k]")
+    k = idx.numel() // (batch * H)
+    if scale is None:
+        scale = D ** -0.5
+    _check("rmm_reduced_attention", lib.rmm_reduced_attention(
+        Q.data_ptr(), Kc.data_ptr(), V.data_ptr(), idx.data_ptr(), _dtype_code(Q), batch, H, Hkv,
+        Lq, Lk, D, k, float(scale), 1 if causal else 0, O.data_ptr(), _stream(d, stream)))
+    return O
 
 
 def rmm_linear(X: torch.Tensor, W: torch.Tensor, r: float, Y: torch.Tensor,

@@ -184,6 +184,26 @@ rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx, r
                                        static_cast<float *>(S), stream));
 }
 
+rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
+                                   const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
+                                   int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                                   int64_t k, float scale, int causal, void *O,
+                                   hipStream_t stream) {
+    if (!Q || !Kc || !V || !idx || !O) return RMM_ERR_INVALID_ARGUMENT;
+    if (!valid_dtype(dtype)) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (H % Hkv != 0) return RMM_ERR_INVALID_ARGUMENT;
+    if (k < 1 || k > D) return RMM_ERR_INVALID_ARGUMENT;
+    if (Lq > kInt32Max || Lk > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (dtype != RMM_BF16 || D != 128) return RMM_ERR_UNSUPPORTED;
+    if (!aligned16(Q) || !aligned16(Kc) || !aligned16(V) || !aligned16(O)) return RMM_ERR_UNSUPPORTED;
+    if (batch * H > kGridYZMax || Lq > kGridYZMax * 128) return RMM_ERR_UNSUPPORTED;
+    return from_hip(rmm::launch_attn_bf16(
+        static_cast<const uint16_t *>(Q), static_cast<const uint16_t *>(Kc),
+        static_cast<const uint16_t *>(V), idx, batch, H, Hkv, Lq, Lk, k, scale, causal != 0,
+        static_cast<uint16_t *>(O), stream));
+}
+
 rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtype, int64_t B,
                         int64_t M, int64_t N, int64_t K, int64_t ldx, int64_t ldw, void *Y,
                         int64_t ldy, int32_t *idx_out, void *workspace, size_t workspace_bytes,

@@ -173,6 +173,28 @@ def test_qk_validation():
     assert call(9, 512) == UNSUPPORTED     # D > 256
 
 
+def test_attention_validation():
+    f = rmm.lib.rmm_reduced_attention
+    A = ctypes.c_void_p(0x100000)
+    base = [A, A, A, P, 1, 1, 8, 2, 64, 64, 128, 64, ctypes.c_float(0.088), 1, A, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 3, 14):
+        assert call(i, NULL) == INVALID
+    assert call(4, 9) == INVALID            # dtype
+    assert call(5, 0) == INVALID            # batch
+    assert call(7, 3) == INVALID            # H % Hkv
+    assert call(11, 0) == INVALID           # k
+    assert call(11, 129) == INVALID         # k > D
+    assert call(4, 0) == UNSUPPORTED        # fp32
+    assert call(10, 64) == UNSUPPORTED      # D != 128
+    assert call(2, ctypes.c_void_p(0x100008)) == UNSUPPORTED   # V not 16-byte aligned
+
+
 def test_linear_validation():
     f = rmm.lib.rmm_linear
     need = rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 64, 128, 64)
