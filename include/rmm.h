@@ -57,7 +57,8 @@ typedef enum rmm_dtype {
 typedef enum rmm_op {
     RMM_OP_SCORE = 0,   /* rmm_score   */
     RMM_OP_SELECT = 1,  /* rmm_select  */
-    RMM_OP_LINEAR = 2   /* rmm_linear  */
+    RMM_OP_LINEAR = 2,  /* rmm_linear  */
+    RMM_OP_ATTENTION = 3 /* rmm_reduced_attention */
 } rmm_op_t;
 
 /*
@@ -76,6 +77,9 @@ int64_t rmm_retained_count(double r, int64_t K);
  *   RMM_OP_SELECT: always 0
  *   RMM_OP_LINEAR: B, M, K, k     (k = rmm_retained_count(r, K); includes
  *                  room for the K-major copy of X, B*K*round_up(M, 8) bf16)
+ *   RMM_OP_ATTENTION: B = batch*H, M = Lk, K = D, k  (each query head's
+ *                  retained key dims as rows: B*Lk*kp bf16, kp = k rounded
+ *                  up to 32, 64, 96 or 128)
  * Returns 0 for non-positive sizes.  Host-only.
  */
 size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t k);
@@ -217,15 +221,20 @@ rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx,
  * Q   : [batch][H][Lq][D]    Kc, V : [batch][Hkv][Lk][D]    O : [batch][H][Lq][D]
  *       (contiguous; the value rows have the head dimension D).
  * idx : int32 [batch*H*k], each head's list ascending (from rmm_select).
+ * workspace : rmm_workspace_size(RMM_OP_ATTENTION, batch*H, Lk, D, k) bytes,
+ *       16-byte aligned; receives each query head's retained key dims as
+ *       contiguous rows (overwritten by every call).
  * Scores and the softmax are computed in fp32, the weights rounded to bf16
  * for the value product, fp32 accumulation, bf16 output.
- * Errors: INVALID_ARGUMENT as rmm_reduced_qk; UNSUPPORTED unless dtype is
- *         RMM_BF16, D == 128 and Q, Kc, V, O are 16-byte aligned.
+ * Errors: INVALID_ARGUMENT as rmm_reduced_qk, or a misaligned workspace;
+ *         UNSUPPORTED unless dtype is RMM_BF16, D == 128 and Q, Kc, V, O
+ *         are 16-byte aligned; WORKSPACE_TOO_SMALL.
  */
 rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
                                    const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
                                    int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
                                    int64_t D, int64_t k, float scale, int causal, void *O,
+                                   void *workspace, size_t workspace_bytes,
                                    hipStream_t stream);
 
 /*

@@ -16,7 +16,7 @@ import torch
 
 __all__ = [
     "RmmError", "LIB_PATH", "lib", "RMM_F32", "RMM_BF16", "RMM_OP_SCORE",
-    "RMM_OP_SELECT", "RMM_OP_LINEAR", "rmm_retained_count", "rmm_workspace_size",
+    "RMM_OP_SELECT", "RMM_OP_LINEAR", "RMM_OP_ATTENTION", "rmm_retained_count", "rmm_workspace_size",
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
     "rmm_reduced_attention", "EXPORTED_SYMBOLS",
@@ -25,7 +25,7 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
 
 RMM_F32, RMM_BF16 = 0, 1
-RMM_OP_SCORE, RMM_OP_SELECT, RMM_OP_LINEAR = 0, 1, 2
+RMM_OP_SCORE, RMM_OP_SELECT, RMM_OP_LINEAR, RMM_OP_ATTENTION = 0, 1, 2, 3
 
 _p = ctypes.c_void_p
 _i64 = ctypes.c_int64
@@ -48,7 +48,7 @@ _SIGS = {
                                                _i64, _p, _i64, _p]),
     "rmm_reduced_attention": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64,
                                              _i64, _i64, _i64, ctypes.c_float, ctypes.c_int, _p,
-                                             _p]),
+                                             _p, ctypes.c_size_t, _p]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -266,9 +266,11 @@ def rmm_reduced_qk(Q: torch.Tensor, Kc: torch.Tensor, idx: torch.Tensor, S: torc
 
 def rmm_reduced_attention(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor, idx: torch.Tensor,
                           O: torch.Tensor, causal: bool = True, scale: float | None = None,
-                          stream=None) -> torch.Tensor:
+                          workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """softmax(reduced scores + mask) V for Q [batch, H, Lq, D], Kc and V
-    [batch, Hkv, Lk, D], idx [batch, H, k]; writes O [batch, H, Lq, D]."""
+    [batch, Hkv, Lk, D], idx [batch, H, k]; writes O [batch, H, Lq, D].
+    `workspace` (uint8, rmm_workspace_size(RMM_OP_ATTENTION, batch*H, Lk, D, k)
+    bytes) is allocated here when not given."""
     if Q.dim() == 3:
         Q, Kc, V, O = Q.unsqueeze(0), Kc.unsqueeze(0), V.unsqueeze(0), O.unsqueeze(0)
     batch, H, Lq, D = Q.shape
@@ -290,9 +292,14 @@ def rmm_reduced_attention(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor, id
     k = idx.numel() // (batch * H)
     if scale is None:
         scale = D ** -0.5
+    if workspace is None:
+        workspace = torch.empty(max(rmm_workspace_size(RMM_OP_ATTENTION, batch * H, Lk, D, k), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
     _check("rmm_reduced_attention", lib.rmm_reduced_attention(
         Q.data_ptr(), Kc.data_ptr(), V.data_ptr(), idx.data_ptr(), _dtype_code(Q), batch, H, Hkv,
-        Lq, Lk, D, k, float(scale), 1 if causal else 0, O.data_ptr(), _stream(d, stream)))
+        Lq, Lk, D, k, float(scale), 1 if causal else 0, O.data_ptr(), workspace.data_ptr(),
+        ws_bytes, _stream(d, stream)))
     return O
 
 

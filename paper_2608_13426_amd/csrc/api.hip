@@ -92,6 +92,9 @@ size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t 
         return align256(rmm::score_workspace_bytes(B, M, K)) +
                align256(static_cast<size_t>(B * K) * sizeof(double)) +
                align256(static_cast<size_t>(B * k) * sizeof(int32_t)) + align256(xt_bytes(B, M, K));
+    case RMM_OP_ATTENTION:
+        if (M < 1 || k < 1 || k > K) return 0;
+        return align256(rmm::attn_workspace_bytes(B, M, k));
     }
     return 0;
 }
@@ -188,7 +191,7 @@ rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
                                    const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
                                    int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
                                    int64_t k, float scale, int causal, void *O,
-                                   hipStream_t stream) {
+                                   void *workspace, size_t workspace_bytes, hipStream_t stream) {
     if (!Q || !Kc || !V || !idx || !O) return RMM_ERR_INVALID_ARGUMENT;
     if (!valid_dtype(dtype)) return RMM_ERR_INVALID_ARGUMENT;
     if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
@@ -197,11 +200,14 @@ rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
     if (Lq > kInt32Max || Lk > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
     if (dtype != RMM_BF16 || D != 128) return RMM_ERR_UNSUPPORTED;
     if (!aligned16(Q) || !aligned16(Kc) || !aligned16(V) || !aligned16(O)) return RMM_ERR_UNSUPPORTED;
-    if (batch * H > kGridYZMax || Lq > kGridYZMax * 128) return RMM_ERR_UNSUPPORTED;
+    if (batch * H > kGridYZMax || (Lq + 255) / 256 * batch * H > kInt32Max) return RMM_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < rmm::attn_workspace_bytes(batch * H, Lk, k))
+        return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (!aligned16(workspace)) return RMM_ERR_INVALID_ARGUMENT;
     return from_hip(rmm::launch_attn_bf16(
         static_cast<const uint16_t *>(Q), static_cast<const uint16_t *>(Kc),
         static_cast<const uint16_t *>(V), idx, batch, H, Hkv, Lq, Lk, k, scale, causal != 0,
-        static_cast<uint16_t *>(O), stream));
+        static_cast<uint16_t *>(O), workspace, stream));
 }
 
 rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtype, int64_t B,

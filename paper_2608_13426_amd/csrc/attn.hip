@@ -1,23 +1,31 @@
 // Reduced attention block: O = softmax(S + M) V with the reduced scores
 // S[h] = scale * Q[h][:, I_h] K[g(h)][:, I_h]^T of Sec. 3.3 (GQA: query head h
-// reads kv head h / (H / Hkv)), computed tile by tile with an online softmax
-// so that S never reaches memory.
+// reads kv head h / (H / Hkv)); S never reaches memory.
 //
-// One workgroup per (head, 128 queries); each of its four waves owns 32
-// queries and walks the key tiles (64 keys) the causal mask leaves it:
-//   * Q rows are staged once in LDS (odd row stride) and each wave gathers its
-//     queries' retained dims into registers; K rows are staged per tile the
-//     same way and gathered at the retained dims;
-//   * the scores are formed transposed (keys x queries, v_mfma_f32_32x32x16_bf16),
-//     so a lane holds 16 keys of one query: the row max and row sum need one
-//     exchange with the partner lane 32 away, and the lane's probabilities,
-//     rounded to bf16, are directly the second MFMA operand of O^T += V^T P^T;
-//   * V rows are staged with their 16-byte chunks at c ^ 4*(row % 4) and
-//     read with the gfx950 transposing LDS read, which yields the
-//     4-consecutive-keys-per-lane layout the probabilities are in;
-//   * O^T is accumulated in fp32 (a lane holds 16 output dims of one query),
-//     rescaled by its own query's exp(m_old - m_new), and divided by the row
-//     sum at the end.  A query with no unmasked key gets 0.
+// Two kernels on the caller's stream:
+//   1. attn_compact_k_kernel writes, for every query head, its retained key
+//      dims as contiguous rows: Ki[b][h][t][0..kp) = K[b][g(h)][t][I_h], zero
+//      past k (kp = 16 * KS >= k).  This is H*Lk*kp bf16 of workspace, read
+//      back once per query tile; it turns the per-tile key gather into plain
+//      16-byte rows.
+//   2. attn_fwd_kernel: one workgroup per (head, 256 queries), four waves of
+//      64 queries (two 32-query blocks sharing every K and V fragment), a
+//      three-slot LDS ring of 64-key tiles filled by LDS DMA two tiles ahead:
+//        * S^T = Ki Q_I^T per tile (v_mfma_f32_32x32x16_bf16; Q's retained
+//          dims gathered once into registers), so a lane holds 16 keys of
+//          one query and the row max needs one exchange with the lane 32
+//          away (v_permlane32_swap);
+//        * online softmax in log2 units, exp2(fma(s, c, -m)) with
+//          c = |scale| log2(e) (Q is negated exactly when scale < 0); the
+//          causal mask is applied only on tiles that cross a row's limit;
+//          the running max is raised (and O^T, l rescaled) only when a
+//          tile's max exceeds it by more than 8 (log2 units), so weights
+//          stay <= 256 and most tiles skip the rescale;
+//        * O^T += V^T P^T with the weights rounded to bf16 as the MFMA's
+//          second operand and V^T read with the gfx950 transposing LDS read.
+//      A query with no unmasked key gets O = 0.
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -26,248 +34,455 @@ namespace rmm {
 namespace {
 
 namespace attk {
-constexpr int BQ = 128, BT = 64, NT = 256, D = 128;
-constexpr int RW = D / 2 + 1;              // words per staged Q/K row (odd)
-constexpr int CH = D / 8;                  // 16-byte chunks per row
+constexpr int BQ = 256;                    // queries per workgroup
+constexpr int CNT = 256;                   // threads of the key-compaction kernel
+constexpr int BN = 64;                     // keys per tile
+constexpr int D = 128;                     // head dim (Q, K and V rows)
+constexpr int RW = D / 2 + 1;              // words per staged Q / K row (odd)
+constexpr int CH = D / 8;                  // 16-byte chunks per Q / K / V row
 constexpr int VROW = D * 2;                // bytes per staged V row
-typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+constexpr int VTILE = BN * VROW;           // bytes of V per slot
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kTau = 8.f;                // lazy-rescale threshold, log2 units
+constexpr uint32_t kOut = 0x80000000u;     // buffer offset past any range: reads zeros
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+
+// One ring slot: 64 key rows of 2*KS data chunks + 1 pad chunk (an odd count
+// of 16-byte chunks per row, so 8 or 16 consecutive rows at one chunk fall on
+// distinct banks), then 64 V rows, then 1 KB that absorbs the wave-uniform
+// padding of the key DMA.
+template <int KS> constexpr int ktile_bytes() { return BN * (2 * KS + 1) * 16; }
+template <int KS> constexpr int junk_offset() { return ktile_bytes<KS>() + VTILE; }
+template <int KS> constexpr int slot_bytes() { return junk_offset<KS>() + 1024; }
+constexpr int QSTAGE_BYTES = BQ * RW * 4;
+
+// s_waitcnt vmcnt(N), expcnt and lgkmcnt unconstrained
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_le() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
+// x of lane l combined with x of lane l ^ 32 (both lanes get the result)
+__device__ __forceinline__ float pair_max(float x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+#else
+    return x;
+#endif
+}
+__device__ __forceinline__ float pair_sum(float x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+#else
+    return x;
+#endif
+}
 }  // namespace attk
 
-template <int KSMAX>
-__global__ __launch_bounds__(attk::NT, 2) void attn_bf16_kernel(
-    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Kc,
-    const uint16_t *__restrict__ V, const int32_t *__restrict__ idx, uint16_t *__restrict__ O,
-    int H, int Hkv, int Lq, int Lk, int k, float scale, int causal) {
+// Ki[bh][t][j] = K[b][g][t][I_h[j]] for j < k, 0 for k <= j < 16*KS.
+template <int KS>
+__global__ __launch_bounds__(attk::CNT) void attn_compact_k_kernel(
+    const uint16_t *__restrict__ Kc, const int32_t *__restrict__ idx, uint16_t *__restrict__ Ki,
+    int H, int Hkv, int Lk, int k) {
     using namespace attk;
-    constexpr int KROWS_T = BT * CH / NT;      // 16-byte K (or V) chunks per thread per tile
-    constexpr int QROWS_T = BQ * CH / NT;      // 16-byte Q chunks per thread
-    static_assert(KSMAX * 16 <= D && KROWS_T * NT == BT * CH, "shape");
-
-    __shared__ uint32_t rows_lds[BQ * RW];     // Q (once), then K tiles (first BT rows)
-    __shared__ __attribute__((aligned(16))) char v_lds[BT * VROW];
-    __shared__ __attribute__((aligned(16))) uint16_t col_off[D + 16];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int KP = 16 * KS, CPR = 2 * KS;
+    __shared__ uint32_t rows_lds[BN * RW];
+    __shared__ uint16_t col_off[KP];
+    const int tid = threadIdx.x;
     const int bh = blockIdx.y, b = bh / H, h = bh % H, g = h / (H / Hkv);
-    // causal: the last query tiles carry the most key tiles, so they go first
-    const int qt = causal ? static_cast<int>(gridDim.x) - 1 - static_cast<int>(blockIdx.x) : blockIdx.x;
-    const int q0 = qt * BQ;
-    const int off = Lk - Lq;
+    const int t0 = blockIdx.x * BN;
+    const int rows = min(BN, Lk - t0);
     const int32_t *I = idx + static_cast<int64_t>(bh) * k;
-    const int kp = (k + 15) & ~15;
-    const int KS = kp / 16;
-    // key tiles any of the block's rows keeps
-    int n_tiles = (Lk + BT - 1) / BT;
-    if (causal) {
-        const int limit = min(q0 + BQ, Lq) - 1 + off;
-        n_tiles = limit < 0 ? 0 : min(n_tiles, limit / BT + 1);
-    }
-
-    for (int t = tid; t < D + 16; t += NT) col_off[t] = static_cast<uint16_t>((t < k ? I[t] : D) * 2);
-    for (int r = tid; r < BQ; r += NT) rows_lds[r * RW + D / 2] = 0u;
-
-    const __amdgpu_buffer_rsrc_t qr = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t *>(Q + (static_cast<int64_t>(bh) * Lq + q0) * D), 0,
-        static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
-    const uint16_t *Kh = Kc + (static_cast<int64_t>(b) * Hkv + g) * Lk * D;
-    const uint16_t *Vh = V + (static_cast<int64_t>(b) * Hkv + g) * Lk * D;
-    // a key tile's rows as a buffer: rows past Lk read zeros (and are masked)
-    auto tile_rsrc = [&](const uint16_t *base, int kt) {
-        const int t0 = min(kt * BT, Lk);
-        return __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t *>(base + static_cast<int64_t>(t0) * D), 0,
-            static_cast<uint32_t>(min(BT, Lk - t0) * D * 2), 0x00020000);
-    };
-    auto chunk_off = [&](int v) { return static_cast<uint32_t>(((v / CH) * D + (v % CH) * 8) * 2); };
-    auto stage_rows = [&](const uint4 &x, int v) {      // Q / K row chunk -> odd-stride rows
+    for (int j = tid; j < KP; j += CNT) col_off[j] = static_cast<uint16_t>((j < k ? I[j] : D) * 2);
+    for (int r = tid; r < BN; r += CNT) rows_lds[r * RW + D / 2] = 0u;
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(Kc + ((static_cast<int64_t>(b) * Hkv + g) * Lk + t0) * D), 0,
+        static_cast<uint32_t>(rows * D * 2), 0x00020000);
+#pragma unroll
+    for (int i = 0; i < BN * CH / CNT; ++i) {
+        const int v = tid + CNT * i;
+        const auto x = __builtin_amdgcn_raw_buffer_load_b128(kr, static_cast<uint32_t>(v * 16), 0, 0);
         uint32_t *dst = rows_lds + (v / CH) * RW + (v % CH) * 4;
-        dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
-    };
-    auto stage_v = [&](const uint4 &x, int v) {          // V row chunk -> swizzled chunk
-        const int t = v / CH, c = v % CH;
-        *reinterpret_cast<uint4 *>(v_lds + t * VROW + ((c ^ (4 * (t & 3))) * 16)) = x;
-    };
-    // 8 retained dims (k-step ks, lane half) of staged row `row`
-    auto frag = [&](int row, int ks) -> bf16x8_t {
-        const uint4 co = *reinterpret_cast<const uint4 *>(&col_off[ks * 16 + 8 * (lane >> 5)]);
-        const char *base = reinterpret_cast<const char *>(rows_lds + row * RW);
-        const uint32_t o[4] = {co.x, co.y, co.z, co.w};
+        dst[0] = x[0]; dst[1] = x[1]; dst[2] = x[2]; dst[3] = x[3];
+    }
+    __syncthreads();
+    uint16_t *out = Ki + (static_cast<int64_t>(bh) * Lk + t0) * KP;
+    for (int i = tid; i < rows * CPR; i += CNT) {
+        const int r = i / CPR, cc = i % CPR;
+        const char *base = reinterpret_cast<const char *>(rows_lds + r * RW);
         uint32_t w[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const uint32_t lo = *reinterpret_cast<const uint16_t *>(base + (o[q] & 0xffffu));
-            const uint32_t hi = *reinterpret_cast<const uint16_t *>(base + (o[q] >> 16));
+            const uint32_t lo = *reinterpret_cast<const uint16_t *>(base + col_off[8 * cc + 2 * q]);
+            const uint32_t hi = *reinterpret_cast<const uint16_t *>(base + col_off[8 * cc + 2 * q + 1]);
             w[q] = lo | (hi << 16);
         }
-        return __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+        *reinterpret_cast<uint4 *>(out + r * KP + 8 * cc) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
+template <int KS, int NQB>
+__global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel(
+    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Ki,
+    const uint16_t *__restrict__ V, const int32_t *__restrict__ idx, uint16_t *__restrict__ O,
+    int H, int Hkv, int Lq, int Lk, int k, float c, int neg_q, int causal) {
+    using namespace attk;
+    constexpr int QW = 32 * NQB;                // queries per wave
+    constexpr int NW = BQ / QW, NT = NW * 64;   // waves, threads
+    constexpr int KP = 16 * KS;                 // Ki row width
+    constexpr int KRB = KP * 2;                 // Ki row bytes
+    constexpr int KSL = 2 * KS + 1;             // 16-byte LDS chunks per staged key row
+    constexpr int NJK = KSL;                    // DMA wave-instructions per key tile
+    constexpr int PER_K = (NJK + NW - 1) / NW;  // per wave (the surplus lands in the junk area)
+    constexpr int VPW = VTILE / 1024 / NW;      // V DMA wave-instructions per wave
+    constexpr int PER = PER_K + VPW;            // DMA instructions per wave per tile
+    constexpr int SB = slot_bytes<KS>();
+    static_assert(QSTAGE_BYTES >= SB, "slot 2 lives in the Q staging area");
+    static_assert(VPW * NW * 1024 == VTILE, "V tile split");
+    using IQ0 = std::integral_constant<int, 0>;
+    using IQ1 = std::integral_constant<int, 1>;
+    auto each_qb = [&](auto f) __attribute__((always_inline)) {
+        f(IQ0{});
+        if constexpr (NQB > 1) f(IQ1{});
     };
 
-    const int lr = lane & 31, lh = lane >> 5;
+    __shared__ __attribute__((aligned(1024))) char slot0[SB];
+    __shared__ __attribute__((aligned(1024))) char slot1[SB];
+    __shared__ __attribute__((aligned(1024))) char slot2q[QSTAGE_BYTES];   // Q staging, then slot 2
+    __shared__ __attribute__((aligned(16))) uint16_t col_off[KP];
 
-    // Q: stage the block's rows, gather this wave's 32 queries
-    {
-        uint4 rq[QROWS_T];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lr = lane & 31, lh = lane >> 5;
+    const int nq = (Lq + BQ - 1) / BQ;
+    const int BH = static_cast<int>(gridDim.x) / nq;
+    // Work order: query tiles with the most key tiles first (causal).  When
+    // the head count is a multiple of 8, the XCD that receives workgroup
+    // `lin` (workgroups are dealt to the 8 XCDs in turn) gets a contiguous
+    // range of heads, so heads that share a kv head share its L2.
+    const int lin = blockIdx.x;
+    int bh, rank;
+    if (BH % 8 == 0) {
+        const int hpx = BH / 8, j = lin / 8;
+        bh = (lin % 8) * hpx + j % hpx;
+        rank = j / hpx;
+    } else {
+        bh = lin % BH;
+        rank = lin / BH;
+    }
+    const int b = bh / H, h = bh % H, g = h / (H / Hkv);
+    const int qt = causal ? nq - 1 - rank : rank;
+    const int q0 = qt * BQ;
+    const int off = Lk - Lq;
+    int n_tiles = (Lk + BN - 1) / BN;
+    if (causal) {
+        const int limit = min(q0 + BQ, Lq) - 1 + off;
+        n_tiles = limit < 0 ? 0 : min(n_tiles, limit / BN + 1);
+    }
+    const int lend = min(Lk, n_tiles * BN);     // no row of the block keeps a key at or past this
+
+    const int32_t *I = idx + static_cast<int64_t>(bh) * k;
+    for (int j = tid; j < KP; j += NT) col_off[j] = static_cast<uint16_t>((j < k ? I[j] : D) * 2);
+
+    // ---- DMA addressing (per lane, the same for every tile)
+    uint32_t ksrc[PER_K], vsrc[VPW];
 #pragma unroll
-        for (int i = 0; i < QROWS_T; ++i) {
-            const auto x = __builtin_amdgcn_raw_buffer_load_b128(qr, chunk_off(tid + NT * i), 0, 0);
+    for (int u = 0; u < PER_K; ++u) {
+        const int j = wave + NW * u, i = 64 * j + lane;
+        const int r = i / KSL, cc = i % KSL;
+        ksrc[u] = (j < NJK && cc < 2 * KS) ? static_cast<uint32_t>(r * KRB + 16 * cc) : kOut;
+    }
+#pragma unroll
+    for (int u = 0; u < VPW; ++u) {
+        // V row chunk p of row r goes to LDS chunk p ^ 4*(r % 4) (r % 4 == lane / 16)
+        const int j = wave + NW * u, r = 4 * j + (lane >> 4), p = lane & 15;
+        vsrc[u] = static_cast<uint32_t>(r * VROW + 16 * (p ^ (4 * (lane >> 4))));
+    }
+    const uint16_t *Kih = Ki + static_cast<int64_t>(bh) * Lk * KP;
+    const uint16_t *Vh = V + (static_cast<int64_t>(b) * Hkv + g) * Lk * D;
+    auto dma = [&](char *slot, int kt) __attribute__((always_inline)) {
+        const int t0 = __builtin_amdgcn_readfirstlane(min(kt * BN, Lk));
+        const int rows = __builtin_amdgcn_readfirstlane(max(0, min(BN, lend - t0)));
+        const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(Kih + static_cast<int64_t>(t0) * KP), 0,
+            static_cast<uint32_t>(rows * KRB), 0x00020000);
+        const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(Vh + static_cast<int64_t>(t0) * D), 0,
+            static_cast<uint32_t>(rows * VROW), 0x00020000);
+#pragma unroll
+        for (int u = 0; u < PER_K; ++u) {
+            const int j = wave + NW * u;
+            lds_load16(kr, slot + (j < NJK ? 1024 * j : junk_offset<KS>()), ksrc[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < VPW; ++u)
+            lds_load16(vr, slot + ktile_bytes<KS>() + 1024 * (wave + NW * u), vsrc[u]);
+    };
+
+    // ---- Q: read the block's rows, start the first two key tiles, stage Q,
+    //      gather this wave's retained dims
+    uint32_t *qrows = reinterpret_cast<uint32_t *>(slot2q);
+    {
+        constexpr int QPT = BQ * CH / NT;
+        const __amdgpu_buffer_rsrc_t qr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(Q + (static_cast<int64_t>(bh) * Lq + q0) * D), 0,
+            static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
+        uint4 rq[QPT];
+#pragma unroll
+        for (int i = 0; i < QPT; ++i) {
+            const auto x = __builtin_amdgcn_raw_buffer_load_b128(qr, static_cast<uint32_t>((tid + NT * i) * 16), 0, 0);
             rq[i] = make_uint4(x[0], x[1], x[2], x[3]);
         }
-        __syncthreads();                       // col_off and the pad words are written
+        dma(slot0, 0);
+        dma(slot1, 1);
+        for (int r = tid; r < BQ; r += NT) qrows[r * RW + D / 2] = 0u;
 #pragma unroll
-        for (int i = 0; i < QROWS_T; ++i) stage_rows(rq[i], tid + NT * i);
-        __syncthreads();
+        for (int i = 0; i < QPT; ++i) {
+            const int v = tid + NT * i;
+            uint32_t *dst = qrows + (v / CH) * RW + (v % CH) * 4;
+            dst[0] = rq[i].x; dst[1] = rq[i].y; dst[2] = rq[i].z; dst[3] = rq[i].w;
+        }
     }
-    bf16x8_t qf[KSMAX];
+    lds_barrier();
+    bf16x8_t qf[NQB][KS];
+    {
+        const uint32_t flip = neg_q ? 0x80008000u : 0u;   // exact negation, for scale < 0
 #pragma unroll
-    for (int ks = 0; ks < KSMAX; ++ks)
-        if (ks < KS) qf[ks] = frag(wave * 32 + lr, ks);
+        for (int qb = 0; qb < NQB; ++qb) {
+            const char *base = reinterpret_cast<const char *>(qrows + (wave * QW + 32 * qb + lr) * RW);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const uint4 co = *reinterpret_cast<const uint4 *>(&col_off[ks * 16 + 8 * lh]);
+                const uint32_t o[4] = {co.x, co.y, co.z, co.w};
+                uint32_t w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t lo = *reinterpret_cast<const uint16_t *>(base + (o[q] & 0xffffu));
+                    const uint32_t hi = *reinterpret_cast<const uint16_t *>(base + (o[q] >> 16));
+                    w[q] = (lo | (hi << 16)) ^ flip;
+                }
+                qf[qb][ks] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+            }
+        }
+    }
 
-    // V^T fragment addressing (transposing read): 16-lane group gr reads rows
-    // row0 + (s16 / 4) of dims 16*(gr % 2) + 4*(s16 % 4) .. +3 of a 32-dim block
+    // ---- per-lane fragment addressing
+    // K fragment (A of S^T): key row 32*tb + lane%32, chunk 2*ks + lane/32
+    const int kaddr = (lr * KSL + lh) * 16;
+    // V^T fragment (A of O^T): 16-lane group gr reads keys 16*st + 4*(gr/2) + s16/4
+    // (and +8) of dims 32*db + 16*(gr%2) + 4*(s16%4) .. +3 (transposing read)
     const int gr = lane >> 4, s16 = lane & 15, vv = s16 >> 2, qq = s16 & 3;
     int voff[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
-        voff[db] = (4 * (gr >> 1) + vv) * VROW + ((4 * (db ^ vv) + 2 * (gr & 1) + (qq >> 1)) * 16) +
-                   8 * (qq & 1);
-    auto vfrag = [&](int db, int s) -> bf16x8_t {
-        const char *p = v_lds + voff[db] + 16 * s * VROW;
-        const s16x4_t lo = lds_read_tr16(p);
-        const s16x4_t hi = lds_read_tr16(p + 8 * VROW);
-        typedef short s16x8_t __attribute__((ext_vector_type(8)));
-        return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    };
+        voff[db] = ktile_bytes<KS>() + (4 * (gr >> 1) + vv) * VROW +
+                   ((4 * (db ^ vv) + 2 * (gr & 1) + (qq >> 1)) * 16) + 8 * (qq & 1);
 
-    f32x16_t o_acc[D / 32];
+    f32x16_t o_acc[NQB][D / 32];
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o_acc[db][v] = 0.f;
-    float m_run = -__builtin_inff(), l_run = 0.f;   // this lane's query (q = lane % 32)
-    const int qg = q0 + wave * 32 + lr;
-    const float sl2 = scale * kLog2e;
-
-    uint4 rk[KROWS_T], rv[KROWS_T];
-    auto load_tile = [&](int kt) {
-        const __amdgpu_buffer_rsrc_t kr = tile_rsrc(Kh, kt), vr = tile_rsrc(Vh, kt);
-#pragma unroll
-        for (int i = 0; i < KROWS_T; ++i) {
-            const auto x = __builtin_amdgcn_raw_buffer_load_b128(kr, chunk_off(tid + NT * i), 0, 0);
-            rk[i] = make_uint4(x[0], x[1], x[2], x[3]);
-            const auto y = __builtin_amdgcn_raw_buffer_load_b128(vr, chunk_off(tid + NT * i), 0, 0);
-            rv[i] = make_uint4(y[0], y[1], y[2], y[3]);
-        }
-    };
-    auto store_tile = [&]() {
-#pragma unroll
-        for (int i = 0; i < KROWS_T; ++i) {
-            stage_rows(rk[i], tid + NT * i);
-            stage_v(rv[i], tid + NT * i);
-        }
-    };
-    if (n_tiles > 0) {
-        load_tile(0);
-        __syncthreads();                       // every wave has gathered its Q fragments
-        store_tile();
-        lds_barrier();
-    }
-    for (int kt = 0; kt < n_tiles; ++kt) {
-        if (kt + 1 < n_tiles) load_tile(kt + 1);
-        // S^T for the tile: s[tb][4*gq + r] = key kt*BT + 32*tb + 8*gq + 4*lh + r
-        f32x16_t s[BT / 32];
-#pragma unroll
-        for (int tb = 0; tb < BT / 32; ++tb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) s[tb][v] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KSMAX; ++ks) {
-            if (ks < KS) {
-#pragma unroll
-                for (int tb = 0; tb < BT / 32; ++tb)
-                    s[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag(32 * tb + lr, ks), qf[ks], s[tb], 0, 0, 0);
-            }
-        }
-        // scale to log2 units and mask: key t past Lk, or (causal) past qg + off
-        const int lim = causal ? min(qg + off, Lk - 1) : Lk - 1;
-        float mx = -__builtin_inff();
-#pragma unroll
-        for (int tb = 0; tb < BT / 32; ++tb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int t = kt * BT + 32 * tb + 8 * (v >> 2) + 4 * lh + (v & 3);
-                const float x = t <= lim ? s[tb][v] * sl2 : -__builtin_inff();
-                s[tb][v] = x;
-                mx = fmaxf(mx, x);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;   // nothing kept yet
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        float lsum = 0.f;
-#pragma unroll
-        for (int tb = 0; tb < BT / 32; ++tb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const float p = __builtin_amdgcn_exp2f(s[tb][v] - m_use);
-                s[tb][v] = p;
-                lsum += p;
-            }
-        lsum += __shfl_xor(lsum, 32);
-        l_run = l_run * alpha + lsum;
-        m_run = m_new;
+    for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) o_acc[db][v] *= alpha;
-        // O^T += V^T P^T over the tile's keys, 16 keys per MFMA: the lane's
-        // probabilities for keys 16*st + 4*lh + {0..3} and 16*st + 8 + 4*lh + {0..3}
+            for (int v = 0; v < 16; ++v) o_acc[qb][db][v] = 0.f;
+    float m_run[NQB], l_run[NQB];
+    int lim[NQB];
+    const int qw0 = q0 + wave * QW;
 #pragma unroll
-        for (int st = 0; st < BT / 16; ++st) {
-            const int tb = st >> 1, g0 = 2 * (st & 1);
-            bf16x8_t pf;
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                pf[e] = static_cast<__bf16>(s[tb][4 * (g0 + (e >> 2)) + (e & 3)]);
-#pragma unroll
-            for (int db = 0; db < D / 32; ++db)
-                o_acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(db, st), pf, o_acc[db], 0, 0, 0);
-        }
-        lds_barrier();                         // every wave is done with this tile's K and V
-        if (kt + 1 < n_tiles) store_tile();
-        lds_barrier();
+    for (int qb = 0; qb < NQB; ++qb) {
+        m_run[qb] = -__builtin_inff();
+        l_run[qb] = 0.f;
+        lim[qb] = causal ? min(qw0 + 32 * qb + lr + off, Lk - 1) : Lk - 1;
     }
+    const int lim_lo = causal ? min(qw0 + off, Lk - 1) : Lk - 1;          // every row keeps the keys <= this
+    const int lim_hi = causal ? min(qw0 + QW - 1 + off, Lk - 1) : Lk - 1;   // no row keeps a key above this
 
-    // O[q][d]: the lane holds d = 32*db + 8*gq + 4*lh + {0..3} of query qg
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    auto compute = [&](const char *slot, int kt) __attribute__((always_inline)) {
+        const int t0 = kt * BN;
+        if (t0 > lim_hi) return;                 // every row of the wave masks the whole tile
+        f32x16_t s[NQB][2];
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb)
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) s[qb][tb][v] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb) {
+                const bf16x8_t kf =
+                    *reinterpret_cast<const bf16x8_t *>(slot + kaddr + (32 * tb * KSL + 2 * ks) * 16);
+#pragma unroll
+                for (int qb = 0; qb < NQB; ++qb)
+                    s[qb][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], s[qb][tb], 0, 0, 0);
+            }
+        }
+        // s[qb][tb][v] is key t0 + 32*tb + 8*(v/4) + 4*lh + v%4 of query qw0 + 32*qb + lr
+        bf16x8_t pf[NQB][BN / 16];
+        const bool open = t0 + BN - 1 <= lim_lo;
+        each_qb([&](auto QB) __attribute__((always_inline)) {
+            constexpr int qb = decltype(QB)::value;
+            float mx = -__builtin_inff();
+            if (!open) {
+                const int rel = lim[qb] - t0 - 4 * lh;   // key t0 + 4*lh + x is kept iff x <= rel
+#pragma unroll
+                for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        if (32 * tb + 8 * (v >> 2) + (v & 3) > rel) s[qb][tb][v] = -__builtin_inff();
+            }
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[qb][tb][v]);
+            mx = pair_max(mx);
+            const float mt = mx == -__builtin_inff() ? -__builtin_inff() : mx * c;
+            const bool need = mt > m_run[qb] + kTau;
+            if (__builtin_amdgcn_ballot_w64(need)) {
+                const float alpha = need ? __builtin_amdgcn_exp2f(m_run[qb] - mt) : 1.f;
+                l_run[qb] *= alpha;
+#pragma unroll
+                for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) o_acc[qb][db][v] *= alpha;
+                m_run[qb] = need ? mt : m_run[qb];
+            }
+            // a row with nothing kept yet has only masked (-inf) scores here
+            const float mu = m_run[qb] == -__builtin_inff() ? 0.f : m_run[qb];
+            float ls = 0.f;
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][tb][v], c, -mu));
+                    s[qb][tb][v] = p;
+                    ls += p;
+                }
+            l_run[qb] += ls;
+            // weights of keys 16*st + 8*(e/4) + 4*lh + e%4: the k-slot order of the V^T fragments
+#pragma unroll
+            for (int st = 0; st < BN / 16; ++st) {
+                const int tb = st >> 1, g0 = 2 * (st & 1);
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    pf[qb][st][e] = static_cast<__bf16>(s[qb][tb][4 * (g0 + (e >> 2)) + (e & 3)]);
+            }
+        });
+#pragma unroll
+        for (int st = 0; st < BN / 16; ++st)
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) {
+                const char *p = slot + voff[db] + 16 * st * VROW;
+                const s16x4_t lo = lds_read_tr16(p);
+                const s16x4_t hi = lds_read_tr16(p + 8 * VROW);
+                const bf16x8_t vf =
+                    __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int qb = 0; qb < NQB; ++qb)
+                    o_acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][st], o_acc[qb][db], 0, 0, 0);
+            }
+    };
+
+    // ---- the ring: tile kt lives in slot kt % 3; loads run two tiles ahead.
+    // Every step issues one tile of loads (tiles past the block's last one
+    // read nothing and stage zeros), so the wait before each barrier is a
+    // fixed vmcnt: the tile after the next may stay in flight.  The tile
+    // count is rounded up to a multiple of 3; the extra steps compute nothing.
+    wait_vmcnt_le<PER>();
+    lds_barrier();                               // tile 0 landed; Q gathered by every wave
+    auto slot_ptr = [&](auto S) -> char * {
+        constexpr int s = decltype(S)::value;
+        if constexpr (s == 0) return slot0;
+        else if constexpr (s == 1) return slot1;
+        else return slot2q;
+    };
+    auto step = [&](auto S, int kt) __attribute__((always_inline)) {
+        constexpr int s = decltype(S)::value;
+        dma(slot_ptr(std::integral_constant<int, (s + 2) % 3>{}), kt + 2);
+        if (kt < n_tiles) compute(slot_ptr(S), kt);
+        wait_vmcnt_le<PER>();
+        lds_barrier();
+    };
+    for (int kt = 0; kt < n_tiles; kt += 3) {
+        step(std::integral_constant<int, 0>{}, kt);
+        step(std::integral_constant<int, 1>{}, kt + 1);
+        step(std::integral_constant<int, 2>{}, kt + 2);
+    }
+    wait_vmcnt_le<0>();                          // the trailing out-of-range loads
+
+    // ---- O[q][d]: the lane holds d = 32*db + 8*gq + 4*lh + {0..3} of query qw0 + 32*qb + lr
     const __amdgpu_buffer_rsrc_t orr = __builtin_amdgcn_make_buffer_rsrc(
         O + (static_cast<int64_t>(bh) * Lq + q0) * D, 0,
         static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
-    const int ql = wave * 32 + lr;             // rows past Lq fall outside the buffer
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+    for (int qb = 0; qb < NQB; ++qb) {
+        const float l = pair_sum(l_run[qb]);
+        const float inv = l > 0.f ? 1.f / l : 0.f;
+        const int ql = wave * QW + 32 * qb + lr;   // rows past Lq fall outside the buffer
 #pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-            const uint32_t w0 = pack_bf16x2(o_acc[db][4 * gq] * inv, o_acc[db][4 * gq + 1] * inv);
-            const uint32_t w1 = pack_bf16x2(o_acc[db][4 * gq + 2] * inv, o_acc[db][4 * gq + 3] * inv);
-            __builtin_amdgcn_raw_buffer_store_b64(
-                u32x2_t{w0, w1}, orr,
-                static_cast<uint32_t>((ql * D + 32 * db + 8 * gq + 4 * lh) * 2), 0, 0);
-        }
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                const uint32_t w0 = pack_bf16x2(o_acc[qb][db][4 * gq] * inv, o_acc[qb][db][4 * gq + 1] * inv);
+                const uint32_t w1 = pack_bf16x2(o_acc[qb][db][4 * gq + 2] * inv, o_acc[qb][db][4 * gq + 3] * inv);
+                __builtin_amdgcn_raw_buffer_store_b64(
+                    u32x2_t{w0, w1}, orr,
+                    static_cast<uint32_t>((ql * D + 32 * db + 8 * gq + 4 * lh) * 2), 0, 0);
+            }
+    }
+}
+
+constexpr int kQueryBlocksPerWave = 1;
+
+template <int KS>
+hipError_t launch_ks(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V, const int32_t *idx,
+                     int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t k,
+                     float scale, bool causal, uint16_t *O, uint16_t *Ki, hipStream_t stream) {
+    using namespace attk;
+    const unsigned BH = static_cast<unsigned>(batch * H);
+    hipLaunchKernelGGL(attn_compact_k_kernel<KS>, dim3(static_cast<unsigned>((Lk + BN - 1) / BN), BH),
+                       dim3(CNT), 0, stream, Kc, idx, Ki, static_cast<int>(H), static_cast<int>(Hkv),
+                       static_cast<int>(Lk), static_cast<int>(k));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned nq = static_cast<unsigned>((Lq + BQ - 1) / BQ);
+    // |scale| in log2 units; a zero scale is applied as the smallest normal
+    // float, which leaves every finite score's weight exactly 1 (as zero
+    // would) while masked -inf scores still give weight 0
+    float c = (scale < 0.f ? -scale : scale) * kLog2e;
+    if (c < 1.17549435e-38f) c = 1.17549435e-38f;
+    constexpr int NQB = kQueryBlocksPerWave;
+    hipLaunchKernelGGL((attn_fwd_kernel<KS, NQB>), dim3(nq * BH), dim3(BQ / (32 * NQB) * 64), 0, stream,
+                       Q, Ki, V, idx, O, static_cast<int>(H), static_cast<int>(Hkv),
+                       static_cast<int>(Lq), static_cast<int>(Lk), static_cast<int>(k), c,
+                       scale < 0.f ? 1 : 0, causal ? 1 : 0);
+    return hipGetLastError();
 }
 
 }  // namespace
 
+int attn_k_steps(int64_t k) { return k <= 32 ? 2 : k <= 64 ? 4 : k <= 96 ? 6 : 8; }
+
+size_t attn_workspace_bytes(int64_t batch_heads, int64_t Lk, int64_t k) {
+    return static_cast<size_t>(batch_heads) * static_cast<size_t>(Lk) *
+           static_cast<size_t>(16 * attn_k_steps(k)) * 2;
+}
+
 hipError_t launch_attn_bf16(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V,
                             const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv,
                             int64_t Lq, int64_t Lk, int64_t k, float scale, bool causal,
-                            uint16_t *O, hipStream_t stream) {
-    dim3 grid(static_cast<unsigned>((Lq + attk::BQ - 1) / attk::BQ), static_cast<unsigned>(batch * H));
-    auto kern = k <= 64 ? attn_bf16_kernel<4> : attn_bf16_kernel<8>;
-    hipLaunchKernelGGL(kern, grid, dim3(attk::NT), 0, stream, Q, Kc, V, idx, O,
-                       static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
-                       static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
-    return hipGetLastError();
+                            uint16_t *O, void *workspace, hipStream_t stream) {
+    uint16_t *Ki = static_cast<uint16_t *>(workspace);
+    switch (attn_k_steps(k)) {
+    case 2: return launch_ks<2>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
+    case 4: return launch_ks<4>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
+    case 6: return launch_ks<6>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
+    default: return launch_ks<8>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
+    }
 }
 
 }  // namespace rmm

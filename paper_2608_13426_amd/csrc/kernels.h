@@ -46,11 +46,14 @@ hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx,
                            hipStream_t stream);
 
 // --------------------------------------------------------- reduced QK^T
-// reduced attention block, bf16, D == 128, 16-byte aligned (checked by the caller)
+// reduced attention block, bf16, D == 128, 16-byte aligned (checked by the
+// caller); the workspace holds the per-head compacted key rows
+int attn_k_steps(int64_t k);
+size_t attn_workspace_bytes(int64_t batch_heads, int64_t Lk, int64_t k);
 hipError_t launch_attn_bf16(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V,
                             const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv,
                             int64_t Lq, int64_t Lk, int64_t k, float scale, bool causal,
-                            uint16_t *O, hipStream_t stream);
+                            uint16_t *O, void *workspace, hipStream_t stream);
 hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *idx,
                           int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
                           int64_t Lk, int64_t D, int64_t k, float scale, bool causal,

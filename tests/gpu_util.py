@@ -110,3 +110,35 @@ def isclose_inf_pattern(S_gpu: np.ndarray, S_ref: np.ndarray):
     assert np.array_equal(np.isneginf(S_gpu), np.isneginf(S_ref))
     assert np.all(np.isfinite(S_gpu[~np.isneginf(S_ref)]))
 
+
+
+def attention_bound(Q: np.ndarray, K: np.ndarray, V: np.ndarray, idx: np.ndarray, causal: bool,
+                    scale: float, rows=None) -> np.ndarray:
+    """Per-row bound on |O - O_ref| for the reduced attention block.
+
+    Each weight carries its bf16 rounding (2^-9 relative) and the fp32 error
+    of its score, (k + 4) u32 |scale| sum|q||k| (accumulation, the scale and
+    the exponent argument), which moves it by a factor exp(+-2 err); the
+    output is then within 2 d max|V| of the reference, d the largest of those
+    relative moves.  Q [H x Lq x D], K, V [Hkv x Lk x D], idx [H x k] in
+    float64; ``rows`` selects query rows (default all).  Rows with every key
+    masked get 0 (their output must be exactly 0).
+    """
+    H, Lq, _ = Q.shape
+    Hkv, Lk, _ = K.shape
+    k = idx.shape[1]
+    rows = np.arange(Lq) if rows is None else np.asarray(rows)
+    out = np.empty((H, rows.shape[0]))
+    for h in range(H):
+        g = h // (H // Hkv)
+        I = idx[h]
+        mag = np.abs(Q[h][rows][:, I]) @ np.abs(K[g][:, I]).T          # [rows, Lk]
+        err_s = (k + 4) * U32 * abs(scale) * mag
+        for n, i in enumerate(rows):
+            keep = np.arange(Lk) <= (i + Lk - Lq) if causal else np.ones(Lk, bool)
+            if not keep.any():
+                out[h, n] = 0.0
+                continue
+            d = np.expm1(2.0 ** -9 + 2.0 * err_s[n][keep].max())
+            out[h, n] = 2.0 * d * np.abs(V[g][keep]).max()
+    return out

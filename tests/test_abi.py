@@ -176,7 +176,8 @@ def test_qk_validation():
 def test_attention_validation():
     f = rmm.lib.rmm_reduced_attention
     A = ctypes.c_void_p(0x100000)
-    base = [A, A, A, P, 1, 1, 8, 2, 64, 64, 128, 64, ctypes.c_float(0.088), 1, A, NULL]
+    need = rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, 8, 64, 128, 64)
+    base = [A, A, A, P, 1, 1, 8, 2, 64, 64, 128, 64, ctypes.c_float(0.088), 1, A, A, need, NULL]
 
     def call(i, v):
         a = list(base)
@@ -193,6 +194,18 @@ def test_attention_validation():
     assert call(4, 0) == UNSUPPORTED        # fp32
     assert call(10, 64) == UNSUPPORTED      # D != 128
     assert call(2, ctypes.c_void_p(0x100008)) == UNSUPPORTED   # V not 16-byte aligned
+    assert call(15, NULL) == WS_SMALL       # no workspace
+    assert call(16, need - 1) == WS_SMALL
+    assert call(15, ctypes.c_void_p(0x100008)) == INVALID      # workspace not 16-byte aligned
+
+
+def test_attention_workspace_size():
+    # each query head's retained key dims as rows of kp = 32, 64, 96 or 128 bf16
+    for k, kp in ((1, 32), (32, 32), (33, 64), (64, 64), (65, 96), (96, 96), (97, 128), (128, 128)):
+        assert rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, 32, 8192, 128, k) == 32 * 8192 * kp * 2
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, 3, 70, 128, 5) == 3 * 70 * 32 * 2 // 256 * 256 + 256
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, 1, 64, 128, 0) == 0
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, 1, 64, 128, 129) == 0
 
 
 def test_linear_validation():

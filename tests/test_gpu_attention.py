@@ -8,7 +8,7 @@ import torch
 import paper_2608_13426_amd as rmm
 import workloads as wl
 from oracle import rmm_oracle as ro
-from tests.gpu_util import NORM_TOL, from_device, require_gpu, to_device
+from tests.gpu_util import NORM_TOL, attention_bound, from_device, require_gpu, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -22,37 +22,10 @@ def _case(seed, batch, H, Hkv, Lq, Lk, D):
     return Qs, Ks, Vs
 
 
-def _bound(Q, K, V, idx, causal, D):
-    """Per-row bound on |O - O_ref|: the weights are rounded to bf16 (2^-9) and
-    shifted by the fp32 score error; the output is rounded to bf16."""
-    H, Lq, _ = Q.shape
-    Hkv, Lk, _ = K.shape
-    k = idx.shape[1]
-    out = np.empty((H, Lq))
-    for h in range(H):
-        g = ro.gqa_kv_head(h, H, Hkv)
-        I = idx[h]
-        mag = np.abs(Q[h][:, I]) @ np.abs(K[g][:, I]).T          # [Lq, Lk]
-        err_s = (k + 4) * U32 * mag / math.sqrt(D)
-        for i in range(Lq):
-            keep = np.arange(Lk) <= (i + Lk - Lq) if causal else np.ones(Lk, bool)
-            if not keep.any():
-                out[h, i] = 0.0
-                continue
-            d = 2.0 ** -9 + 2.0 * err_s[i][keep].max()
-            out[h, i] = 2.0 * d * np.abs(V[g][keep]).max()
-    return out
-
-
-@pytest.mark.parametrize("batch,H,Hkv,Lq,Lk,r,causal,seed", [
-    (1, 4, 2, 200, 200, 0.5, True, 0),
-    (2, 2, 1, 130, 70, 0.25, True, 1),        # Lq > Lk: leading rows fully masked -> 0
-    (1, 4, 4, 64, 300, 1.0, False, 2),       # key tail past a 64-key tile
-    (1, 2, 1, 257, 320, 0.75, True, 3),      # k = 96: two register k-groups
-    (1, 8, 2, 128, 128, 0.001, True, 4),     # k = 1
-    (1, 2, 2, 40, 40, 0.5, False, 5),
-])
-def test_reduced_attention(batch, H, Hkv, Lq, Lk, r, causal, seed):
+def _run(seed, batch, H, Hkv, Lq, Lk, r, causal, scale=None):
+    """GPU block against the oracle, element by element.  The oracle applies
+    1/sqrt(D); another scale s is handed to it as Q * s * sqrt(D) (float64,
+    an exact rewrite of the same scores)."""
     dev = require_gpu()
     D = 128
     Qs, Ks, Vs = _case(seed, batch, H, Hkv, Lq, Lk, D)
@@ -66,17 +39,42 @@ def test_reduced_attention(batch, H, Hkv, Lq, Lk, r, causal, seed):
     rmm.rmm_reduced_attention(to_device(Qs, "bf16", dev).reshape(batch, H, Lq, D),
                               to_device(Ks, "bf16", dev).reshape(batch, Hkv, Lk, D),
                               to_device(Vs, "bf16", dev).reshape(batch, Hkv, Lk, D),
-                              torch.from_numpy(idx).to(dev), Od, causal=causal)
+                              torch.from_numpy(idx).to(dev), Od, causal=causal, scale=scale)
     O = from_device(Od)
+    s = D ** -0.5 if scale is None else float(np.float32(scale))
     for b in range(batch):
-        ref = ro.reduced_attention(Q[b], K[b], V[b], idx[b], causal)
-        bound = _bound(Q[b], K[b], V[b], idx[b], causal, D)
+        Qr = Q[b] * (s * math.sqrt(D))
+        ref = ro.reduced_attention(Qr, K[b], V[b], idx[b], causal)
+        bound = attention_bound(Q[b], K[b], V[b], idx[b], causal, s)
         err = np.abs(O[b] - ref)
         assert np.all(err <= bound[:, :, None] + 2.0 ** -8 * np.abs(ref)), float(err.max())
         denom = max(np.abs(ref).max(), 1e-30)
         assert err.max() / denom <= NORM_TOL["bf16"]
         if causal and Lq > Lk:
             assert np.all(O[b][:, :Lq - Lk] == 0.0)
+
+
+@pytest.mark.parametrize("batch,H,Hkv,Lq,Lk,r,causal,seed", [
+    (1, 4, 2, 200, 200, 0.5, True, 0),
+    (2, 2, 1, 130, 70, 0.25, True, 1),        # Lq > Lk: leading rows fully masked -> 0
+    (1, 4, 4, 64, 300, 1.0, False, 2),       # key tail past a 64-key tile
+    (1, 2, 1, 257, 320, 0.75, True, 3),      # k = 96; two query tiles, the second of one row
+    (1, 8, 2, 128, 128, 0.001, True, 4),     # k = 1
+    (1, 2, 2, 40, 40, 0.5, False, 5),
+    (1, 8, 2, 700, 700, 0.5, True, 6),       # 8 heads: heads grouped per XCD; three query tiles
+    (2, 8, 4, 300, 520, 0.25, True, 7),      # Lk > Lq (bottom-right causal), 16 heads
+    (1, 16, 2, 520, 520, 0.375, False, 8),   # k = 48, 16 heads, key tail
+])
+def test_reduced_attention(batch, H, Hkv, Lq, Lk, r, causal, seed):
+    _run(seed, batch, H, Hkv, Lq, Lk, r, causal)
+
+
+@pytest.mark.parametrize("scale", [-0.07, 0.0, 1.0, 3.0])
+def test_reduced_attention_scales(scale):
+    """Negative (Q negated), zero (uniform weights over the kept keys) and
+    large scales (scores spanning many powers of two, so the running max is
+    raised and O rescaled several times along a row)."""
+    _run(12, 1, 4, 2, 300, 300, 0.5, True, scale=scale)
 
 
 def test_reduced_attention_matches_qk_softmax():

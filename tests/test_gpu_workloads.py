@@ -13,8 +13,8 @@ import torch
 import paper_2608_13426_amd as rmm
 import workloads as wl
 from oracle import rmm_oracle as ro
-from tests.gpu_util import (gpu, require_gpu, from_device, check_energies, check_index_sets,
-                            check_product, isclose_inf_pattern)
+from tests.gpu_util import (NORM_TOL, attention_bound, gpu, require_gpu, from_device,
+                            check_energies, check_index_sets, check_product, isclose_inf_pattern)
 
 pytestmark = gpu
 
@@ -125,6 +125,40 @@ def _attention_case(name, ratios, heads=None, n_rows=13):
     torch.cuda.empty_cache()
 
 
+def _fused_attention_case(name, ratios, n_rows=11):
+    """The reduced attention block at full size: every row's output on
+    sampled query rows (first and last included) against the oracle, with
+    the index sets from the library's own selection (checked above)."""
+    dev = require_gpu()
+    wk = wl.WORKLOADS[name]
+    a = wk.attention
+    q, kk = wl.workload_qk(wk)
+    qb, kb = wl.f32_to_bf16_bits(q), wl.f32_to_bf16_bits(kk)
+    vb = wl.f32_to_bf16_bits(wl.workload_v(wk))
+    Q, Kc, V = wl.decode(qb, "bf16"), wl.decode(kb, "bf16"), wl.decode(vb, "bf16")
+    del q, kk
+    Qd = _dev_bf16(qb, dev).reshape(1, a.H, a.L, a.D)
+    Kd = _dev_bf16(kb, dev).reshape(1, a.Hkv, a.L, a.D)
+    Vd = _dev_bf16(vb, dev).reshape(1, a.Hkv, a.L, a.D)
+    e_ref = np.stack([ro.column_energies(Q[h]) for h in range(a.H)])
+    O = torch.empty((1, a.H, a.L, a.D), dtype=torch.bfloat16, device=dev)
+    rows = _rows(a.L, n_rows, a.H + 1)
+    Q64, K64, V64 = (x.astype(np.float64) for x in (Q, Kc, V))
+    for r in ratios:
+        k = rmm.rmm_retained_count(r, a.D)
+        idx_ref = np.stack([ro.topk_indices(e_ref[h], k) for h in range(a.H)]).astype(np.int32)
+        rmm.rmm_reduced_attention(Qd, Kd, Vd, torch.from_numpy(idx_ref).to(dev).view(1, a.H, k), O,
+                                  causal=a.causal)
+        Os = from_device(O[0][:, torch.from_numpy(rows).to(dev)])
+        ref = ro.reduced_attention(Q64, K64, V64, idx_ref, a.causal, rows=rows)
+        bound = attention_bound(Q64, K64, V64, idx_ref, a.causal, a.D ** -0.5, rows=rows)
+        err = np.abs(Os - ref)
+        assert np.all(err <= bound[:, :, None] + 2.0 ** -8 * np.abs(ref)), float(err.max())
+        assert err.max() / max(np.abs(ref).max(), 1e-30) <= NORM_TOL["bf16"]
+    del Qd, Kd, Vd, O
+    torch.cuda.empty_cache()
+
+
 RATIOS = (0.25, 0.5, 0.75, 1.0)
 
 
@@ -144,6 +178,14 @@ def test_layer_8b_projection(proj):
 
 def test_layer_8b_attention():
     _attention_case("layer_8b", RATIOS)
+
+
+def test_layer_8b_fused_attention():
+    _fused_attention_case("layer_8b", RATIOS)
+
+
+def test_attn_4k_fused_attention():
+    _fused_attention_case("attn_4k", (0.5,))
 
 
 @pytest.mark.parametrize("proj", ["gate", "down"])

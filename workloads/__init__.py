@@ -253,7 +253,7 @@ WORKLOADS = {
 }
 
 
-# tensor ids: inputs 0..99, weights 100..199, attention Q/K 200/201
+# tensor ids: inputs 0..99, weights 100..199, attention Q/K/V 200/201/202
 _INPUT_IDS = {"x": 0, "attn_in": 1, "o_in": 2, "mlp_in": 3, "down_in": 4}
 _WEIGHT_IDS = {"linear": 100, "q": 101, "k": 102, "v": 103, "o": 104,
                "gate": 105, "up": 106, "down": 107}
@@ -283,6 +283,13 @@ def workload_qk(wl: Workload, L: int | None = None):
                 heavy_tailed_heads(kk, a.Hkv, L, a.D))
     return (outlier_heads(kq, a.H, L, a.D, 0.01, 20.0),
             outlier_heads(kk, a.Hkv, L, a.D, 0.01, 20.0))
+
+
+def workload_v(wl: Workload, L: int | None = None) -> np.ndarray:
+    """fp32 samples of the value rows V [Hkv x L x D], N(0, 1)."""
+    a = wl.attention
+    L = a.L if L is None else L
+    return normal_blocks((wl.seed, 202), (a.Hkv, L, a.D))
 
 
 def random_case(seed: int, shape, dtype: str, n_outlier: int = 0,
