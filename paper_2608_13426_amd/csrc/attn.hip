@@ -34,7 +34,8 @@ namespace rmm {
 namespace {
 
 namespace attk {
-constexpr int BQ = 256;                    // queries per workgroup
+constexpr int NW = 8, NT = NW * 64;        // waves (32 queries each), threads
+constexpr int BQ = NW * 32;                // queries per workgroup
 constexpr int CNT = 256;                   // threads of the key-compaction kernel
 constexpr int BN = 64;                     // keys per tile
 constexpr int D = 128;                     // head dim (Q, K and V rows)
@@ -54,7 +55,11 @@ typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 template <int KS> constexpr int ktile_bytes() { return BN * (2 * KS + 1) * 16; }
 template <int KS> constexpr int junk_offset() { return ktile_bytes<KS>() + VTILE; }
 template <int KS> constexpr int slot_bytes() { return junk_offset<KS>() + 1024; }
-constexpr int QSTAGE_BYTES = BQ * RW * 4;
+// a slot also holds half of the block's Q rows (odd row stride) before the ring starts
+constexpr int QHALF_BYTES = BQ / 2 * RW * 4;
+template <int KS> constexpr int ring_slot_bytes() {
+    return ((slot_bytes<KS>() > QHALF_BYTES ? slot_bytes<KS>() : QHALF_BYTES) + 1023) / 1024 * 1024;
+}
 
 // s_waitcnt vmcnt(N), expcnt and lgkmcnt unconstrained
 template <int N>
@@ -124,14 +129,12 @@ __global__ __launch_bounds__(attk::CNT) void attn_compact_k_kernel(
     }
 }
 
-template <int KS, int NQB>
-__global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel(
+template <int KS>
+__global__ __launch_bounds__(attk::NT, 1) void attn_fwd_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Ki,
     const uint16_t *__restrict__ V, const int32_t *__restrict__ idx, uint16_t *__restrict__ O,
     int H, int Hkv, int Lq, int Lk, int k, float c, int neg_q, int causal) {
     using namespace attk;
-    constexpr int QW = 32 * NQB;                // queries per wave
-    constexpr int NW = BQ / QW, NT = NW * 64;   // waves, threads
     constexpr int KP = 16 * KS;                 // Ki row width
     constexpr int KRB = KP * 2;                 // Ki row bytes
     constexpr int KSL = 2 * KS + 1;             // 16-byte LDS chunks per staged key row
@@ -139,19 +142,13 @@ __global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel
     constexpr int PER_K = (NJK + NW - 1) / NW;  // per wave (the surplus lands in the junk area)
     constexpr int VPW = VTILE / 1024 / NW;      // V DMA wave-instructions per wave
     constexpr int PER = PER_K + VPW;            // DMA instructions per wave per tile
-    constexpr int SB = slot_bytes<KS>();
-    static_assert(QSTAGE_BYTES >= SB, "slot 2 lives in the Q staging area");
+    constexpr int SB = ring_slot_bytes<KS>();
     static_assert(VPW * NW * 1024 == VTILE, "V tile split");
-    using IQ0 = std::integral_constant<int, 0>;
-    using IQ1 = std::integral_constant<int, 1>;
-    auto each_qb = [&](auto f) __attribute__((always_inline)) {
-        f(IQ0{});
-        if constexpr (NQB > 1) f(IQ1{});
-    };
 
     __shared__ __attribute__((aligned(1024))) char slot0[SB];
     __shared__ __attribute__((aligned(1024))) char slot1[SB];
-    __shared__ __attribute__((aligned(1024))) char slot2q[QSTAGE_BYTES];   // Q staging, then slot 2
+    __shared__ __attribute__((aligned(1024))) char slot2[SB];   // Q rows 0..127 before the ring
+    __shared__ __attribute__((aligned(1024))) char slot3[SB];   // Q rows 128..255 before the ring
     __shared__ __attribute__((aligned(16))) uint16_t col_off[KP];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -222,11 +219,11 @@ __global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel
             lds_load16(vr, slot + ktile_bytes<KS>() + 1024 * (wave + NW * u), vsrc[u]);
     };
 
-    // ---- Q: read the block's rows, start the first two key tiles, stage Q,
-    //      gather this wave's retained dims
-    uint32_t *qrows = reinterpret_cast<uint32_t *>(slot2q);
+    // ---- Q: read the block's rows, start the first two key tiles, stage Q
+    //      (rows 0..127 in slot 2, 128..255 in slot 3), gather this wave's
+    //      retained dims
     {
-        constexpr int QPT = BQ * CH / NT;
+        constexpr int QPT = BQ * CH / NT;       // 16-byte chunks per thread; chunk i is row tid/16 + 32 i
         const __amdgpu_buffer_rsrc_t qr = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<uint16_t *>(Q + (static_cast<int64_t>(bh) * Lq + q0) * D), 0,
             static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
@@ -238,34 +235,35 @@ __global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel
         }
         dma(slot0, 0);
         dma(slot1, 1);
-        for (int r = tid; r < BQ; r += NT) qrows[r * RW + D / 2] = 0u;
+        if (tid < 128) reinterpret_cast<uint32_t *>(slot2)[tid * RW + D / 2] = 0u;
+        else if (tid < 256) reinterpret_cast<uint32_t *>(slot3)[(tid - 128) * RW + D / 2] = 0u;
 #pragma unroll
         for (int i = 0; i < QPT; ++i) {
-            const int v = tid + NT * i;
-            uint32_t *dst = qrows + (v / CH) * RW + (v % CH) * 4;
+            const int v = tid + NT * i, r = v / CH;
+            uint32_t *dst = reinterpret_cast<uint32_t *>(i < QPT / 2 ? slot2 : slot3) +
+                            (r % 128) * RW + (v % CH) * 4;
             dst[0] = rq[i].x; dst[1] = rq[i].y; dst[2] = rq[i].z; dst[3] = rq[i].w;
         }
     }
     lds_barrier();
-    bf16x8_t qf[NQB][KS];
+    bf16x8_t qf[KS];
     {
         const uint32_t flip = neg_q ? 0x80008000u : 0u;   // exact negation, for scale < 0
+        const int row = wave * 32 + lr;
+        const char *base = reinterpret_cast<const char *>(
+            reinterpret_cast<const uint32_t *>(wave < NW / 2 ? slot2 : slot3) + (row % 128) * RW);
 #pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) {
-            const char *base = reinterpret_cast<const char *>(qrows + (wave * QW + 32 * qb + lr) * RW);
+        for (int ks = 0; ks < KS; ++ks) {
+            const uint4 co = *reinterpret_cast<const uint4 *>(&col_off[ks * 16 + 8 * lh]);
+            const uint32_t o[4] = {co.x, co.y, co.z, co.w};
+            uint32_t w[4];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const uint4 co = *reinterpret_cast<const uint4 *>(&col_off[ks * 16 + 8 * lh]);
-                const uint32_t o[4] = {co.x, co.y, co.z, co.w};
-                uint32_t w[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t lo = *reinterpret_cast<const uint16_t *>(base + (o[q] & 0xffffu));
-                    const uint32_t hi = *reinterpret_cast<const uint16_t *>(base + (o[q] >> 16));
-                    w[q] = (lo | (hi << 16)) ^ flip;
-                }
-                qf[qb][ks] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t lo = *reinterpret_cast<const uint16_t *>(base + (o[q] & 0xffffu));
+                const uint32_t hi = *reinterpret_cast<const uint16_t *>(base + (o[q] >> 16));
+                w[q] = (lo | (hi << 16)) ^ flip;
             }
+            qf[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
         }
     }
 
@@ -281,97 +279,95 @@ __global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel
         voff[db] = ktile_bytes<KS>() + (4 * (gr >> 1) + vv) * VROW +
                    ((4 * (db ^ vv) + 2 * (gr & 1) + (qq >> 1)) * 16) + 8 * (qq & 1);
 
-    f32x16_t o_acc[NQB][D / 32];
+    f32x16_t o_acc[D / 32];
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb)
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) o_acc[qb][db][v] = 0.f;
-    float m_run[NQB], l_run[NQB];
-    int lim[NQB];
-    const int qw0 = q0 + wave * QW;
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-        m_run[qb] = -__builtin_inff();
-        l_run[qb] = 0.f;
-        lim[qb] = causal ? min(qw0 + 32 * qb + lr + off, Lk - 1) : Lk - 1;
-    }
-    const int lim_lo = causal ? min(qw0 + off, Lk - 1) : Lk - 1;          // every row keeps the keys <= this
-    const int lim_hi = causal ? min(qw0 + QW - 1 + off, Lk - 1) : Lk - 1;   // no row keeps a key above this
+        for (int v = 0; v < 16; ++v) o_acc[db][v] = 0.f;
+    float m_run = -__builtin_inff(), l_run = 0.f;
+    const int qw0 = q0 + wave * 32;
+    const int lim = causal ? min(qw0 + lr + off, Lk - 1) : Lk - 1;          // this lane's query keeps keys <= lim
+    const int lim_lo = causal ? min(qw0 + off, Lk - 1) : Lk - 1;           // every row of the wave keeps these
+    const int lim_hi = causal ? min(qw0 + 31 + off, Lk - 1) : Lk - 1;      // no row of the wave keeps a key above
 
-    auto compute = [&](const char *slot, int kt) __attribute__((always_inline)) {
+    // scores of the tile last multiplied, and weights waiting for their PV
+    f32x16_t s[2];
+    bf16x8_t pf[BN / 16];
+    // S^T of tile kt: s[tb][v] is key kt*BN + 32*tb + 8*(v/4) + 4*lh + v%4 of query qw0 + lr
+    auto qk = [&](const char *slot) __attribute__((always_inline)) {
+        // all of the tile's fragments are read first, so the MFMAs wait once
+        bf16x8_t kf[KS][2];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+                kf[ks][tb] = *reinterpret_cast<const bf16x8_t *>(slot + kaddr + (32 * tb * KSL + 2 * ks) * 16);
+        __builtin_amdgcn_sched_barrier(0);       // keep the reads ahead of the MFMAs
+#pragma unroll
+        for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) s[tb][v] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+                s[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][tb], qf[ks], s[tb], 0, 0, 0);
+    };
+    auto softmax = [&](int kt) __attribute__((always_inline)) {
         const int t0 = kt * BN;
-        if (t0 > lim_hi) return;                 // every row of the wave masks the whole tile
-        f32x16_t s[NQB][2];
-#pragma unroll
-        for (int qb = 0; qb < NQB; ++qb)
+        float mx = -__builtin_inff();
+        if (t0 + BN - 1 > lim_lo) {              // the tile crosses some row's limit
+            const int rel = lim - t0 - 4 * lh;   // key t0 + 4*lh + x is kept iff x <= rel
 #pragma unroll
             for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) s[qb][tb][v] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-            for (int tb = 0; tb < 2; ++tb) {
-                const bf16x8_t kf =
-                    *reinterpret_cast<const bf16x8_t *>(slot + kaddr + (32 * tb * KSL + 2 * ks) * 16);
-#pragma unroll
-                for (int qb = 0; qb < NQB; ++qb)
-                    s[qb][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], s[qb][tb], 0, 0, 0);
-            }
+                for (int v = 0; v < 16; ++v)
+                    if (32 * tb + 8 * (v >> 2) + (v & 3) > rel) s[tb][v] = -__builtin_inff();
         }
-        // s[qb][tb][v] is key t0 + 32*tb + 8*(v/4) + 4*lh + v%4 of query qw0 + 32*qb + lr
-        bf16x8_t pf[NQB][BN / 16];
-        const bool open = t0 + BN - 1 <= lim_lo;
-        each_qb([&](auto QB) __attribute__((always_inline)) {
-            constexpr int qb = decltype(QB)::value;
-            float mx = -__builtin_inff();
-            if (!open) {
-                const int rel = lim[qb] - t0 - 4 * lh;   // key t0 + 4*lh + x is kept iff x <= rel
-#pragma unroll
-                for (int tb = 0; tb < 2; ++tb)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v)
-                        if (32 * tb + 8 * (v >> 2) + (v & 3) > rel) s[qb][tb][v] = -__builtin_inff();
-            }
+        {
+            // four independent chains, then combined
+            float m4[4] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
 #pragma unroll
             for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[qb][tb][v]);
-            mx = pair_max(mx);
-            const float mt = mx == -__builtin_inff() ? -__builtin_inff() : mx * c;
-            const bool need = mt > m_run[qb] + kTau;
-            if (__builtin_amdgcn_ballot_w64(need)) {
-                const float alpha = need ? __builtin_amdgcn_exp2f(m_run[qb] - mt) : 1.f;
-                l_run[qb] *= alpha;
+                for (int v = 0; v < 16; ++v) m4[v & 3] = fmaxf(m4[v & 3], s[tb][v]);
+            mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
+        }
+        mx = pair_max(mx);
+        const float mt = mx == -__builtin_inff() ? -__builtin_inff() : mx * c;
+        const bool need = mt > m_run + kTau;
+        if (__builtin_amdgcn_ballot_w64(need)) {
+            const float alpha = need ? __builtin_amdgcn_exp2f(m_run - mt) : 1.f;
+            l_run *= alpha;
 #pragma unroll
-                for (int db = 0; db < D / 32; ++db)
+            for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) o_acc[qb][db][v] *= alpha;
-                m_run[qb] = need ? mt : m_run[qb];
+                for (int v = 0; v < 16; ++v) o_acc[db][v] *= alpha;
+            m_run = need ? mt : m_run;
+        }
+        // a row with nothing kept yet has only masked (-inf) scores here
+        const float mu = m_run == -__builtin_inff() ? 0.f : m_run;
+        float l4[4] = {0.f, 0.f, 0.f, 0.f};      // four independent chains
+#pragma unroll
+        for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[tb][v], c, -mu));
+                s[tb][v] = p;
+                l4[v & 3] += p;
             }
-            // a row with nothing kept yet has only masked (-inf) scores here
-            const float mu = m_run[qb] == -__builtin_inff() ? 0.f : m_run[qb];
-            float ls = 0.f;
+        l_run += (l4[0] + l4[1]) + (l4[2] + l4[3]);
+        // weights of keys 16*st + 8*(e/4) + 4*lh + e%4: the k-slot order of the V^T fragments
 #pragma unroll
-            for (int tb = 0; tb < 2; ++tb)
+        for (int st = 0; st < BN / 16; ++st) {
+            const int tb = st >> 1, g0 = 2 * (st & 1);
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][tb][v], c, -mu));
-                    s[qb][tb][v] = p;
-                    ls += p;
-                }
-            l_run[qb] += ls;
-            // weights of keys 16*st + 8*(e/4) + 4*lh + e%4: the k-slot order of the V^T fragments
-#pragma unroll
-            for (int st = 0; st < BN / 16; ++st) {
-                const int tb = st >> 1, g0 = 2 * (st & 1);
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    pf[qb][st][e] = static_cast<__bf16>(s[qb][tb][4 * (g0 + (e >> 2)) + (e & 3)]);
-            }
-        });
+            for (int e = 0; e < 8; ++e) pf[st][e] = static_cast<__bf16>(s[tb][4 * (g0 + (e >> 2)) + (e & 3)]);
+        }
+    };
+    auto pv = [&](const char *slot) __attribute__((always_inline)) {
+        // all of the tile's V^T fragments are read first, so the MFMAs wait once
+        bf16x8_t vf[BN / 16][D / 32];
 #pragma unroll
         for (int st = 0; st < BN / 16; ++st)
 #pragma unroll
@@ -379,64 +375,73 @@ __global__ __launch_bounds__(attk::BQ / (32 * NQB) * 64, 1) void attn_fwd_kernel
                 const char *p = slot + voff[db] + 16 * st * VROW;
                 const s16x4_t lo = lds_read_tr16(p);
                 const s16x4_t hi = lds_read_tr16(p + 8 * VROW);
-                const bf16x8_t vf =
-                    __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-                for (int qb = 0; qb < NQB; ++qb)
-                    o_acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][st], o_acc[qb][db], 0, 0, 0);
+                vf[st][db] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
+        __builtin_amdgcn_sched_barrier(0);       // keep the reads ahead of the MFMAs
+#pragma unroll
+        for (int st = 0; st < BN / 16; ++st)
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+                o_acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[st][db], pf[st], o_acc[db], 0, 0, 0);
     };
 
-    // ---- the ring: tile kt lives in slot kt % 3; loads run two tiles ahead.
-    // Every step issues one tile of loads (tiles past the block's last one
-    // read nothing and stage zeros), so the wait before each barrier is a
-    // fixed vmcnt: the tile after the next may stay in flight.  The tile
-    // count is rounded up to a multiple of 3; the extra steps compute nothing.
+    // ---- the ring.  Tile kt lives in slot kt % 4 and is loaded two steps
+    // ahead.  Step i multiplies the keys of tile i (QK) and the values of tile
+    // i-1 (PV).  The two halves of the workgroup (one wave of each per SIMD)
+    // run the softmax at opposite ends of the step: the first half does
+    // PV(i-1), QK(i), softmax(i); the second softmax(i-1), PV(i-1), QK(i).
+    // So while one wave of a SIMD is in its exp/max work the other is in its
+    // MFMAs.  Every step issues one tile of loads (tiles past the block's last
+    // one read nothing and stage zeros), so the wait before each barrier is a
+    // fixed vmcnt: the tile after the next may stay in flight.
     wait_vmcnt_le<PER>();
     lds_barrier();                               // tile 0 landed; Q gathered by every wave
     auto slot_ptr = [&](auto S) -> char * {
-        constexpr int s = decltype(S)::value;
-        if constexpr (s == 0) return slot0;
-        else if constexpr (s == 1) return slot1;
-        else return slot2q;
+        constexpr int sl = decltype(S)::value;
+        if constexpr (sl == 0) return slot0;
+        else if constexpr (sl == 1) return slot1;
+        else if constexpr (sl == 2) return slot2;
+        else return slot3;
     };
-    auto step = [&](auto S, int kt) __attribute__((always_inline)) {
-        constexpr int s = decltype(S)::value;
-        dma(slot_ptr(std::integral_constant<int, (s + 2) % 3>{}), kt + 2);
-        if (kt < n_tiles) compute(slot_ptr(S), kt);
+    const bool late = wave >= NW / 2;
+    // a tile with work for this wave: in range and not wholly masked for its rows
+    auto active = [&](int kt) { return kt >= 0 && kt < n_tiles && kt * BN <= lim_hi; };
+    auto step = [&](auto S, int i) __attribute__((always_inline)) {
+        constexpr int sl = decltype(S)::value;
+        dma(slot_ptr(std::integral_constant<int, (sl + 2) % 4>{}), i + 2);
+        const bool prev = active(i - 1), cur = active(i);
+        if (late && prev) softmax(i - 1);
+        if (prev) pv(slot_ptr(std::integral_constant<int, (sl + 3) % 4>{}));
+        if (cur) qk(slot_ptr(S));
+        if (!late && cur) softmax(i);
         wait_vmcnt_le<PER>();
         lds_barrier();
     };
-    for (int kt = 0; kt < n_tiles; kt += 3) {
-        step(std::integral_constant<int, 0>{}, kt);
-        step(std::integral_constant<int, 1>{}, kt + 1);
-        step(std::integral_constant<int, 2>{}, kt + 2);
+    for (int i = 0; i <= n_tiles; i += 4) {
+        step(std::integral_constant<int, 0>{}, i);
+        step(std::integral_constant<int, 1>{}, i + 1);
+        step(std::integral_constant<int, 2>{}, i + 2);
+        step(std::integral_constant<int, 3>{}, i + 3);
     }
     wait_vmcnt_le<0>();                          // the trailing out-of-range loads
 
-    // ---- O[q][d]: the lane holds d = 32*db + 8*gq + 4*lh + {0..3} of query qw0 + 32*qb + lr
+    // ---- O[q][d]: the lane holds d = 32*db + 8*gq + 4*lh + {0..3} of query qw0 + lr
     const __amdgpu_buffer_rsrc_t orr = __builtin_amdgcn_make_buffer_rsrc(
         O + (static_cast<int64_t>(bh) * Lq + q0) * D, 0,
         static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
+    const float l = pair_sum(l_run);
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const int ql = wave * 32 + lr;               // rows past Lq fall outside the buffer
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-        const float l = pair_sum(l_run[qb]);
-        const float inv = l > 0.f ? 1.f / l : 0.f;
-        const int ql = wave * QW + 32 * qb + lr;   // rows past Lq fall outside the buffer
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                const uint32_t w0 = pack_bf16x2(o_acc[qb][db][4 * gq] * inv, o_acc[qb][db][4 * gq + 1] * inv);
-                const uint32_t w1 = pack_bf16x2(o_acc[qb][db][4 * gq + 2] * inv, o_acc[qb][db][4 * gq + 3] * inv);
-                __builtin_amdgcn_raw_buffer_store_b64(
-                    u32x2_t{w0, w1}, orr,
-                    static_cast<uint32_t>((ql * D + 32 * db + 8 * gq + 4 * lh) * 2), 0, 0);
-            }
-    }
+        for (int gq = 0; gq < 4; ++gq) {
+            const uint32_t w0 = pack_bf16x2(o_acc[db][4 * gq] * inv, o_acc[db][4 * gq + 1] * inv);
+            const uint32_t w1 = pack_bf16x2(o_acc[db][4 * gq + 2] * inv, o_acc[db][4 * gq + 3] * inv);
+            __builtin_amdgcn_raw_buffer_store_b64(
+                u32x2_t{w0, w1}, orr, static_cast<uint32_t>((ql * D + 32 * db + 8 * gq + 4 * lh) * 2), 0, 0);
+        }
 }
-
-constexpr int kQueryBlocksPerWave = 1;
 
 template <int KS>
 hipError_t launch_ks(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V, const int32_t *idx,
@@ -455,8 +460,7 @@ hipError_t launch_ks(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V, c
     // would) while masked -inf scores still give weight 0
     float c = (scale < 0.f ? -scale : scale) * kLog2e;
     if (c < 1.17549435e-38f) c = 1.17549435e-38f;
-    constexpr int NQB = kQueryBlocksPerWave;
-    hipLaunchKernelGGL((attn_fwd_kernel<KS, NQB>), dim3(nq * BH), dim3(BQ / (32 * NQB) * 64), 0, stream,
+    hipLaunchKernelGGL(attn_fwd_kernel<KS>, dim3(nq * BH), dim3(NT), 0, stream,
                        Q, Ki, V, idx, O, static_cast<int>(H), static_cast<int>(Hkv),
                        static_cast<int>(Lq), static_cast<int>(Lk), static_cast<int>(k), c,
                        scale < 0.f ? 1 : 0, causal ? 1 : 0);
