@@ -20,6 +20,11 @@ K timed steps bracketed by device synchronisation.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--ratios 0.5,1.0]
 
+The fused attention block (softmax of the reduced scores times V, S never
+written) is timed on its own after the sweep, at the same ratios, and
+reported under "fused_attention" with its speedup over r = 1 and its own
+MFMA roofline; it is not part of the step.
+
 The roofline object covers the dominant kernel, the K-major gathered GEMM:
 achieved = retained FLOPs of all its timed launches (every ratio of the run)
 over their summed durations, taken from HIP events recorded on the stream
@@ -70,6 +75,8 @@ def parse():
     p.add_argument("--cpu-tokens", type=int, default=6144,
                    help="tokens of the bounded CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-fused-attention", action="store_true",
+                   help="skip the separate timing of the fused attention block")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="copy this many MiB device to device once before timing (a "
                         "counter-calibration probe for rocprofv3 runs; not timed)")
@@ -127,6 +134,9 @@ class Layer:
         self.Q = put(q).reshape(1, a.H, a.L, a.D)
         self.Kc = put(k).reshape(1, a.Hkv, a.L, a.D)
         self.S = torch.empty((1, a.H, a.L, a.L), dtype=torch.bfloat16, device=dev)
+        # value rows and output of the fused attention block (timed on its own)
+        self.V = put(wl.workload_v(wk)).reshape(1, a.Hkv, a.L, a.D)
+        self.O = torch.empty((1, a.H, a.L, a.D), dtype=torch.bfloat16, device=dev)
         Kmax = max(v[0] for v in wk.inputs.values())
         import paper_2608_13426_amd as rmm
         ws = max(rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, 1, self.M, Kmax),
@@ -206,6 +216,40 @@ def time_ratio(L, r, steps, warmup):
         "gemm_avg_us": gemm_ms * 1e3 / max(len(events), 1),
         "gemm_avg_gflop": gemm_flop / max(len(events), 1) / 1e9,
     }
+
+
+def time_attention(L, r, steps, warmup):
+    """The fused reduced attention block on the layer's Q, K, V (causal): the
+    per-head selection at ratio r is made once outside the timed region, then
+    `steps` calls are timed one by one with HIP events on the launch stream.
+    Each call runs the key compaction and the attention kernel; its retained
+    FLOPs are 2*H*pairs*(k + D) (reduced scores plus the dense value product)."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    a = L.wk.attention
+    kq = rmm.rmm_retained_count(r, a.D)
+    e = L.energy[:a.H * a.D]
+    rmm.rmm_score(L.Q.reshape(a.H, a.L, a.D), e, L.ws)
+    idx = torch.empty(a.H * kq, dtype=torch.int32, device=L.dev)
+    rmm.rmm_select(e, kq, idx)
+    ws = torch.empty(rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, a.H, a.L, a.D, kq),
+                     dtype=torch.uint8, device=L.dev)
+    args = (L.Q, L.Kc, L.V, idx.view(1, a.H, kq), L.O)
+    for _ in range(warmup):
+        rmm.rmm_reduced_attention(*args, causal=True, workspace=ws)
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rmm.rmm_reduced_attention(*args, causal=True, workspace=ws)
+        e1.record()
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = sum(x.elapsed_time(y) for x, y in evs) / steps
+    flop = 2 * a.H * (a.L * (a.L + 1) // 2) * (kq + a.D)
+    return {"r": r, "k": kq, "avg_call_us": ms * 1e3, "gflop": flop / 1e9,
+            "retained_tflops": flop / (ms * 1e-3) / 1e12, "calls": steps}
 
 
 # ---------------------------------------------------------- CPU baseline
@@ -315,6 +359,27 @@ def main():
                      "avg_launch_gflop": round(g_gflop / g_n, 3),
                      "ratios": sorted(sweep)},
     }
+    if not args.no_fused_attention:
+        att = {r: time_attention(L, r, args.steps, args.warmup) for r in sorted(sweep)}
+        for r, rec in att.items():
+            print(f"# fused attention r={r}: {rec['avg_call_us']:.1f} us/call, "
+                  f"{rec['retained_tflops']:.1f} TFLOP/s", file=sys.stderr, flush=True)
+        a_ms = sum(rec["avg_call_us"] * rec["calls"] for rec in att.values()) * 1e-3
+        a_gf = sum(rec["gflop"] * rec["calls"] for rec in att.values())
+        a_ach = a_gf / a_ms
+        a_h, a_1 = att.get(HEADLINE_R), att.get(1.0)
+        out["fused_attention"] = {
+            "op": "softmax(reduced QK^T + causal mask) V per head, S never written; "
+                  "32 q / 8 kv heads, seq 8192, d=128, V dense",
+            "kernels": ["attn_compact_k_kernel", "attn_fwd_kernel"],
+            "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
+                                   for k, v in rec.items()} for r, rec in att.items()},
+            "speedup_vs_r1": round(a_1["avg_call_us"] / a_h["avg_call_us"], 3) if a_1 else None,
+            "speedup_bound": round(2.0 / (1.0 + HEADLINE_R), 3),
+            "roofline": {"bound": "mfma", "kernel": "attn_fwd_kernel (+ attn_compact_k_kernel)",
+                         "achieved": round(a_ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(a_ach / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        }
     if not args.no_cpu_baseline:
         print(f"# CPU oracle on {args.cpu_tokens} tokens ...", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wk, args.cpu_tokens, HEADLINE_R)
