@@ -18,7 +18,7 @@ computed causal score) at r = 0.5, with the speedup of the same pipeline
 over its own r = 1 run.  Each r is timed separately: W warm-up steps, then
 K timed steps bracketed by device synchronisation.
 
-  python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--ratios 0.5,1.0]
+  python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--ratios 0.25,0.5,0.75,1.0]
 
 The fused attention block (softmax of the reduced scores times V, S never
 written) is timed on its own after the sweep, at the same ratios, and
@@ -55,43 +55,30 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (no sparsity)
 PEAK_HBM_GBS = 8000.0
 GEMM_KERNEL = "gemm_kmajor_tr_kernel"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
-# HBM bytes per launch of GEMM_KERNEL in the default command, averaged over its
-# dispatches, from two rocprofv3 --pmc runs (FETCH_SIZE x2.0, WRITE_SIZE x1.0:
-# the factors a 512 MiB device copy reads).  Valid for the gemm.hip whose
-# SHA-256 is recorded and for the same launch mix (workload, ratios, one
-# launch per input group).
-GEMM_TRAFFIC = {"gemm_hip_sha256": "72dbcdbafdde24c62b0e5bb8237c112b3aecc5b888cb5810092f0f2eba4b086b",
-                "mix": "layer_8b r=0.5,1.0 grouped",
-                "bytes_per_launch": round((480461.50 * 2.0 + 227442.45) * 1024)}
+# HBM bytes per launch from two rocprofv3 --pmc runs of the default ratio mix
+# (FETCH_SIZE x2.0, WRITE_SIZE x1.0: the factors a 512 MiB device copy reads),
+# averaged over the kernel's dispatches.  Each figure is valid only for the
+# source whose SHA-256 is recorded and for the same launch mix.
+GEMM_TRAFFIC = {"source": GEMM_SOURCE,
+                "sha256": "72dbcdbafdde24c62b0e5bb8237c112b3aecc5b888cb5810092f0f2eba4b086b",
+                "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
+                "bytes": round((399783.32 * 2.0 + 227851.38) * 1024)}
+# per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
+# plus attn_compact_k_kernel
+ATTN_TRAFFIC = {"source": os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "attn.hip"),
+                "sha256": "e2348a3c4851579e6ae4e805c8094dbcd7b93007e82a311fb9b1d71d822838a7",
+                "mix": "layer_8b r=0.25,0.5,0.75,1.0",
+                "bytes": round((103617.145 * 2.0 + 65554.17 + 8249.90 * 2.0 + 40960.00) * 1024)}
 
 
-def parse():
-    p = argparse.ArgumentParser()
-    p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--ratios", default="0.5,1.0")
-    p.add_argument("--workload", default="layer_8b")
-    p.add_argument("--cpu-tokens", type=int, default=6144,
-                   help="tokens of the bounded CPU-oracle sample")
-    p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--no-fused-attention", action="store_true",
-                   help="skip the separate timing of the fused attention block")
-    p.add_argument("--copy-probe-mib", type=int, default=0,
-                   help="copy this many MiB device to device once before timing (a "
-                        "counter-calibration probe for rocprofv3 runs; not timed)")
-    return p.parse_args()
-
-
-def gemm_traffic(mix):
-    """Recorded HBM bytes per launch of the GEMM, if its source and launch mix
-    are the ones measured."""
-    if GEMM_TRAFFIC is None or GEMM_TRAFFIC["mix"] != mix:
+def recorded_traffic(rec, mix):
+    """A recorded HBM byte count, if its source and launch mix are the ones measured."""
+    if rec is None or rec["mix"] != mix:
         return None
-    with open(GEMM_SOURCE, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != GEMM_TRAFFIC["gemm_hip_sha256"]:
+    with open(rec["source"], "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != rec["sha256"]:
             return None
-    return GEMM_TRAFFIC["bytes_per_launch"]
+    return rec["bytes"]
 
 
 # ---------------------------------------------------------------- inputs
@@ -352,7 +339,8 @@ def main():
         "roofline": {"bound": "mfma", "kernel": GEMM_KERNEL,
                      "achieved": round(roof_ach, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(roof_ach / PEAK_BF16_TFLOPS, 4),
-                     "traffic": gemm_traffic(f"{wk.name} r={','.join(str(r) for r in sorted(sweep))} grouped"),
+                     "traffic": recorded_traffic(
+                         GEMM_TRAFFIC, f"{wk.name} r={','.join(str(r) for r in sorted(sweep))} grouped"),
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE)",
                      "launches": g_n,
                      "avg_launch_us": round(g_ms * 1e3 / g_n, 2),
@@ -378,7 +366,10 @@ def main():
             "speedup_bound": round(2.0 / (1.0 + HEADLINE_R), 3),
             "roofline": {"bound": "mfma", "kernel": "attn_fwd_kernel (+ attn_compact_k_kernel)",
                          "achieved": round(a_ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(a_ach / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                         "frac": round(a_ach / PEAK_BF16_TFLOPS, 4),
+                         "traffic": recorded_traffic(
+                             ATTN_TRAFFIC, f"{wk.name} r={','.join(str(r) for r in sorted(att))}"),
+                         "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, both kernels)"},
         }
     if not args.no_cpu_baseline:
         print(f"# CPU oracle on {args.cpu_tokens} tokens ...", file=sys.stderr, flush=True)
