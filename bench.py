@@ -25,6 +25,10 @@ written) is timed on its own after the sweep, at the same ratios, and
 reported under "fused_attention" with its speedup over r = 1 and its own
 MFMA roofline; it is not part of the step.
 
+A decode step of the same layer (batch 1, one token: energies, TopK and the
+reduced product over the retained weight rows per projection group) is timed
+the same way and reported under "decode" with its HBM roofline.
+
 The roofline object covers the dominant kernel, the K-major gathered GEMM:
 achieved = retained FLOPs of all its timed launches (every ratio of the run)
 over their summed durations, taken from HIP events recorded on the stream
@@ -79,6 +83,26 @@ def recorded_traffic(rec, mix):
         if hashlib.sha256(f.read()).hexdigest() != rec["sha256"]:
             return None
     return rec["bytes"]
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--ratios", default="0.25,0.5,0.75,1.0")
+    p.add_argument("--workload", default="layer_8b")
+    p.add_argument("--cpu-tokens", type=int, default=6144,
+                   help="tokens of the bounded CPU-oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-fused-attention", action="store_true",
+                   help="skip the separate timing of the fused attention block")
+    p.add_argument("--no-decode", action="store_true",
+                   help="skip the separate timing of the decode step")
+    p.add_argument("--copy-probe-mib", type=int, default=0,
+                   help="copy this many MiB device to device once before timing (a "
+                        "counter-calibration probe for rocprofv3 runs; not timed)")
+    return p.parse_args()
 
 
 # ---------------------------------------------------------------- inputs
@@ -239,6 +263,83 @@ def time_attention(L, r, steps, warmup):
             "retained_tflops": flop / (ms * 1e-3) / 1e12, "calls": steps}
 
 
+def time_decode(L, r, steps, warmup, B=1):
+    """One decode step of the layer's projections for B sequences (one token
+    each: the first B tokens of each input stand in for the current tokens):
+    per input group, the TopK of the token's squared activations
+    (rmm_select_tokens: the same set as energies + TopK for one row) and the
+    reduced product that reads only the retained weight rows
+    (rmm_reduced_gemv).  The whole step is timed with HIP events, and each
+    product call on its own."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    wk = L.wk
+    parts = []
+    for name in L.groups:
+        K = wk.inputs[name][0]
+        k = rmm.rmm_retained_count(r, K)
+        X = L.X[name][:B].reshape(B, 1, K)
+        W = L.Wcat[name]
+        N = W.shape[1]
+        gws = torch.empty(max(rmm.rmm_gemv_workspace_size(B, 1, N, k), 1), dtype=torch.uint8,
+                          device=L.dev)
+        parts.append({"X": X, "W": W, "k": k, "K": K, "N": N, "ws": gws,
+                      "idx": torch.empty(B * k, dtype=torch.int32, device=L.dev),
+                      "Y": torch.empty((B, 1, N), dtype=torch.bfloat16, device=L.dev)})
+
+    def step(evs=None):
+        for p in parts:
+            rmm.rmm_select_tokens(p["X"], p["k"], p["idx"])
+            if evs is not None:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+            rmm.rmm_reduced_gemv(p["X"], p["W"], p["idx"].view(B, p["k"]), p["Y"], workspace=p["ws"])
+            if evs is not None:
+                e1.record()
+                evs.append((e0, e1, B * p["k"] * p["N"] * 2 + B * (p["K"] + p["N"]) * 2 + 4 * B * p["k"]))
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    us_eager = start.elapsed_time(end) * 1e3 / steps
+    # a serving loop replays the step as one HIP graph (every call here is
+    # capturable: no allocation, no memset, no synchronisation)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        graph.replay()
+    end.record()
+    torch.cuda.synchronize()
+    us = start.elapsed_time(end) * 1e3 / steps
+    evs = []
+    for _ in range(steps):
+        step(evs)
+    torch.cuda.synchronize()
+    g_us = sum(a.elapsed_time(b) for a, b, _ in evs) * 1e3
+    g_bytes = sum(n for _, _, n in evs)
+    return {"r": r, "batch": B, "us_per_step": us, "us_per_step_eager": us_eager,
+            "gemv_calls": len(evs),
+            "gemv_us_per_step": g_us / steps, "gemv_bytes_per_step": g_bytes / steps,
+            "gemv_gbs": g_bytes / (g_us * 1e-6) / 1e9}
+
+
 # ---------------------------------------------------------- CPU baseline
 
 def cpu_baseline(wk, tokens, r):
@@ -370,6 +471,30 @@ def main():
                          "traffic": recorded_traffic(
                              ATTN_TRAFFIC, f"{wk.name} r={','.join(str(r) for r in sorted(att))}"),
                          "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, both kernels)"},
+        }
+    if not args.no_decode:
+        dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}
+        for r, rec in dec.items():
+            print(f"# decode step r={r}: {rec['us_per_step']:.1f} us as a graph "
+                  f"({rec['us_per_step_eager']:.1f} us eager), reduced products "
+                  f"{rec['gemv_us_per_step']:.1f} us ({rec['gemv_gbs']:.0f} GB/s)",
+                  file=sys.stderr, flush=True)
+        d_us = sum(rec["gemv_us_per_step"] * args.steps for rec in dec.values())
+        d_b = sum(rec["gemv_bytes_per_step"] * args.steps for rec in dec.values())
+        d_ach = d_b / (d_us * 1e-6) / 1e9
+        d_h, d_1 = dec.get(HEADLINE_R), dec.get(1.0)
+        out["decode"] = {
+            "op": "one decode step, batch 1: per projection group of the layer (q|k|v, o, "
+                  "gate|up, down) TopK of the token's squared activations, reduced product "
+                  "over the retained weight rows; us_per_step replays the step as one HIP "
+                  "graph, us_per_step_eager launches it call by call",
+            "kernels": ["select_kernel (token keys)", "gemv_partial_kernel", "gemv_reduce_kernel"],
+            "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
+                                   for k, v in rec.items()} for r, rec in dec.items()},
+            "speedup_vs_r1": round(d_1["us_per_step"] / d_h["us_per_step"], 3) if d_1 else None,
+            "roofline": {"bound": "hbm", "kernel": "gemv_partial_kernel (+ gemv_reduce_kernel)",
+                         "achieved": round(d_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(d_ach / PEAK_HBM_GBS, 4), "traffic": None},
         }
     if not args.no_cpu_baseline:
         print(f"# CPU oracle on {args.cpu_tokens} tokens ...", file=sys.stderr, flush=True)

@@ -142,6 +142,24 @@ rmm_status_t rmm_select(const double *energy, int64_t B, int64_t K, int64_t k,
                         int32_t *idx, hipStream_t stream);
 
 /*
+ * Selection for units of one token   (Sec. 3.2 TopK of the column norms;
+ * App. A: in a decode step the set follows the current token).
+ *
+ * For B units of a single row each (one token per sequence), idx[b] is the
+ * list rmm_score + rmm_select give for M = 1: the k indices with the largest
+ * x_j^2 = X[b][j]^2, ties to the lower index, NaN above +inf above every
+ * finite value, -0 == +0, ascending.  x_j^2 is exact in float64 and orders
+ * like |x_j|, so the keys are taken from the activations directly: one
+ * launch, no energies written.
+ *
+ * X   : [B][ldx] bf16 or fp32 (ldx >= K).    idx : int32 [B*k].
+ * Errors: INVALID_ARGUMENT for null pointers, an unknown dtype, B < 1,
+ *         K < 1, k outside [1, K], ldx < K, K > INT32_MAX.
+ */
+rmm_status_t rmm_select_tokens(const void *X, rmm_dtype_t dtype, int64_t B, int64_t K,
+                               int64_t ldx, int64_t k, int32_t *idx, hipStream_t stream);
+
+/*
  * Gathered reduced product   (Sec. 3.2: RMM = A[:, I] B[I, :]; Sec. 3.3
  * projections Y~ = X[:, I] W[I, :]).
  *
@@ -164,6 +182,30 @@ rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx,
                               rmm_dtype_t dtype, int64_t B, int64_t M, int64_t N,
                               int64_t K, int64_t k, int64_t ldx, int64_t ldw,
                               void *Y, int64_t ldy, hipStream_t stream);
+
+/*
+ * Reduced product for a decode step   (Sec. 3.2 definition of RMM; App. A:
+ * during decoding the retained set follows the current decoding state).
+ *
+ * The same Y as rmm_reduced_gemm, for M <= 8 rows per unit (one token per
+ * sequence in a decode step, or a few): reading the k retained rows of W is
+ * the whole cost, and each is one contiguous row of W, so only those rows
+ * are streamed from memory (k*N*2 bytes per unit).
+ *
+ * X, W, idx, Y, sizes : as rmm_reduced_gemm (bf16 only, M in [1, 8]).
+ * workspace : rmm_gemv_workspace_size(B, M, N, k) bytes (0 is possible),
+ *             16-byte aligned, or NULL when that size is 0; receives fp32
+ *             partial sums when the retained list is split across
+ *             workgroups, which a second kernel adds in a fixed order.
+ * Errors    : as rmm_reduced_gemm; UNSUPPORTED for fp32, M > 8 or
+ *             K*ldw*2 >= 2^31; WORKSPACE_TOO_SMALL.
+ */
+size_t rmm_gemv_workspace_size(int64_t B, int64_t M, int64_t N, int64_t k);
+rmm_status_t rmm_reduced_gemv(const void *X, const void *W, const int32_t *idx,
+                              rmm_dtype_t dtype, int64_t B, int64_t M, int64_t N,
+                              int64_t K, int64_t k, int64_t ldx, int64_t ldw,
+                              void *Y, int64_t ldy, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Gathered reduced product from K-major activations   (Sec. 3.2 definition

@@ -19,7 +19,8 @@ __all__ = [
     "RMM_OP_SELECT", "RMM_OP_LINEAR", "RMM_OP_ATTENTION", "rmm_retained_count", "rmm_workspace_size",
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
-    "rmm_reduced_attention", "EXPORTED_SYMBOLS",
+    "rmm_reduced_attention", "rmm_reduced_gemv", "rmm_gemv_workspace_size", "rmm_select_tokens",
+    "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -37,6 +38,10 @@ _SIGS = {
     "rmm_select": (ctypes.c_int, [_p, _i64, _i64, _i64, _p, _p]),
     "rmm_reduced_gemm": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64,
                                         _i64, _i64, _i64, _p, _i64, _p]),
+    "rmm_gemv_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64]),
+    "rmm_select_tokens": (ctypes.c_int, [_p, ctypes.c_int, _i64, _i64, _i64, _i64, _p, _p]),
+    "rmm_reduced_gemv": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64,
+                                        _i64, _i64, _i64, _p, _i64, _p, ctypes.c_size_t, _p]),
     "rmm_reduced_qk": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64, _i64,
                                       _i64, _i64, ctypes.c_float, ctypes.c_int, _p, _p]),
     "rmm_linear": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
@@ -211,6 +216,56 @@ def rmm_reduced_gemm(X: torch.Tensor, W: torch.Tensor, idx: torch.Tensor, Y: tor
     _check("rmm_reduced_gemm", lib.rmm_reduced_gemm(
         X.data_ptr(), W.data_ptr(), idx.data_ptr(), _dtype_code(X), B, M, N, K, k, ldx, ldw,
         Y.data_ptr(), ldy, _stream(d, stream)))
+    return Y
+
+
+def rmm_select_tokens(X: torch.Tensor, k: int, idx: torch.Tensor, stream=None) -> torch.Tensor:
+    """TopK of X[b][j]^2 per row of X [B, K] (or [B, 1, K]: one token per unit),
+    ascending, into idx (int32, B*k)."""
+    if X.dim() == 3:
+        if X.shape[1] != 1:
+            raise ValueError("X must hold one token per unit")
+        X = X[:, 0, :]
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be [B, K] with contiguous rows")
+    B, K = X.shape
+    d = _dev(X, idx)
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.numel() != B * k:
+        raise ValueError("idx must be contiguous int32 with B*k elements")
+    _check("rmm_select_tokens", lib.rmm_select_tokens(
+        X.data_ptr(), _dtype_code(X), B, K, X.stride(0), int(k), idx.data_ptr(), _stream(d, stream)))
+    return idx
+
+
+def rmm_gemv_workspace_size(B: int, M: int, N: int, k: int) -> int:
+    return int(lib.rmm_gemv_workspace_size(int(B), int(M), int(N), int(k)))
+
+
+def rmm_reduced_gemv(X: torch.Tensor, W: torch.Tensor, idx: torch.Tensor, Y: torch.Tensor,
+                     workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Decode-step form of rmm_reduced_gemm (M <= 8 rows per unit, bf16):
+    Y[b] = X[b][:, I_b] @ W[I_b, :]; `workspace` (uint8,
+    rmm_gemv_workspace_size(B, M, N, k) bytes) is allocated here when not given."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, W, idx, Y)
+    if W.dim() != 2 or W.shape[0] != K or W.stride(1) != 1:
+        raise ValueError("W must be [K, N] with contiguous rows")
+    N, ldw = W.shape[1], W.stride(0)
+    By, My, Ny, ldy = _rows(Y, "Y")
+    if (By, My, Ny) != (B, M, N):
+        raise ValueError("Y must be [B, M, N]")
+    if not (X.dtype == W.dtype == Y.dtype):
+        raise TypeError("X, W and Y must share one dtype")
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.numel() % B:
+        raise ValueError("idx must be contiguous int32 [B, k]")
+    k = idx.numel() // B
+    if workspace is None:
+        need = rmm_gemv_workspace_size(B, M, N, k)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_reduced_gemv", lib.rmm_reduced_gemv(
+        X.data_ptr(), W.data_ptr(), idx.data_ptr(), _dtype_code(X), B, M, N, K, k, ldx, ldw,
+        Y.data_ptr(), ldy, workspace.data_ptr(), ws_bytes, _stream(d, stream)))
     return Y
 
 

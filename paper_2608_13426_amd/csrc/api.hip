@@ -152,6 +152,42 @@ rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx, 
                                          ldw, static_cast<float *>(Y), ldy, stream));
 }
 
+rmm_status_t rmm_select_tokens(const void *X, rmm_dtype_t dtype, int64_t B, int64_t K,
+                               int64_t ldx, int64_t k, int32_t *idx, hipStream_t stream) {
+    if (!X || !idx) return RMM_ERR_INVALID_ARGUMENT;
+    if (!valid_dtype(dtype)) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || K < 1 || k < 1 || k > K || ldx < K) return RMM_ERR_INVALID_ARGUMENT;
+    if (K > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (B > kInt32Max) return RMM_ERR_UNSUPPORTED;
+    return from_hip(rmm::launch_select_tokens(X, dtype == RMM_BF16, B, K, ldx, k, idx, stream));
+}
+
+size_t rmm_gemv_workspace_size(int64_t B, int64_t M, int64_t N, int64_t k) {
+    if (B < 1 || M < 1 || M > 8 || N < 1 || k < 1) return 0;
+    const size_t b = rmm::gemv_workspace_bytes(B, M, N, k);
+    return b == 0 ? 0 : align256(b);
+}
+
+rmm_status_t rmm_reduced_gemv(const void *X, const void *W, const int32_t *idx, rmm_dtype_t dtype,
+                              int64_t B, int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx,
+                              int64_t ldw, void *Y, int64_t ldy, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+    if (!idx) return RMM_ERR_INVALID_ARGUMENT;
+    rmm_status_t st = check_gemm_shapes(X, W, dtype, B, M, N, K, k, ldx, ldw, Y, ldy);
+    if (st != RMM_OK) return st;
+    if (dtype != RMM_BF16 || M > 8) return RMM_ERR_UNSUPPORTED;
+    // 32-bit byte offsets into W (the kernel reads it through one descriptor)
+    if (K * ldw * 2 >= (int64_t(1) << 31)) return RMM_ERR_UNSUPPORTED;
+    const size_t need = rmm::gemv_workspace_bytes(B, M, N, k);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+        if (reinterpret_cast<uintptr_t>(workspace) % 16) return RMM_ERR_INVALID_ARGUMENT;
+    }
+    return from_hip(rmm::launch_gemv_bf16(static_cast<const uint16_t *>(X),
+                                          static_cast<const uint16_t *>(W), idx, B, M, N, K, k, ldx,
+                                          ldw, static_cast<uint16_t *>(Y), ldy, workspace, stream));
+}
+
 rmm_status_t rmm_reduced_gemm_kmajor(const void *Xt, const void *W, const int32_t *idx, int64_t B,
                                      int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldxt,
                                      int64_t ldw, void *Y, int64_t ldy, hipStream_t stream) {

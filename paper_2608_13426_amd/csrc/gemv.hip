@@ -1,0 +1,230 @@
+// Reduced product with few rows per unit (a decode step: one token, or a
+// handful, per sequence)   (Sec. 3.2 definition of RMM; App. A: during
+// decoding the retained set follows the current decoding state).
+//
+//   Y[b][m][:] = sum_{t < k} X[b][m][I_b[t]] * W[I_b[t]][:],   m < M <= 8
+//
+// With so few rows the product is bound by reading the retained rows of W
+// (k*N*2 bytes per unit): each retained index is one contiguous weight row,
+// so the kernel streams exactly those rows.  Work is split over
+// (512-column chunk, slice of the retained list, unit): a workgroup stages
+// its slice's row offsets and activations in LDS, its four waves take every
+// fourth row, each lane holding 8 columns (one 16-byte load per row, 8 rows
+// in flight), and the waves' sums are added in a fixed order in LDS.  Slices write fp32 partials that a second kernel adds in slice
+// order (or, with one slice, the workgroup writes Y directly), so results
+// are bit-reproducible.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace rmm {
+
+namespace {
+
+namespace gv {
+constexpr int NW = 4, NT = NW * 64;
+constexpr int CW = 512;            // columns per workgroup (64 lanes x 8)
+constexpr int RB = 256;            // retained rows staged per pass
+constexpr int TARGET_BLOCKS = 512;
+constexpr int MIN_SLICE = 64;      // retained rows per slice at least
+}  // namespace gv
+
+template <int MR, bool VEC, bool DIRECT>
+__global__ __launch_bounds__(gv::NT) void gemv_partial_kernel(
+    const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, const int32_t *__restrict__ idx,
+    float *__restrict__ P, uint16_t *__restrict__ Y, int M, int N, int K, int k, int64_t ldx,
+    int64_t ldw, int64_t ldy, int SR, int S) {
+    using namespace gv;
+    __shared__ uint32_t roff[RB];              // byte offset of each staged row in W
+    __shared__ float xs[RB][MR];               // its activation value per row m
+    __shared__ float red[NW - 1][MR][CW];      // sums of waves 1..3
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int chunk = blockIdx.x, s = blockIdx.y, b = blockIdx.z;
+    const int n0 = chunk * CW;
+    const int t0 = s * SR, t1 = min(k, t0 + SR);
+    const int32_t *I = idx + static_cast<int64_t>(b) * k;
+    const uint16_t *Xb = X + static_cast<int64_t>(b) * M * ldx;
+    // the whole of W from this chunk's first column on: a row's columns past
+    // N read padding or the next row, and past the matrix's end read zeros
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(W + n0), 0,
+        static_cast<uint32_t>((static_cast<int64_t>(K) * ldw - n0) * 2), 0x00020000);
+
+    float acc[MR][8];
+#pragma unroll
+    for (int m = 0; m < MR; ++m)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
+
+    for (int base = t0; base < t1; base += RB) {
+        const int nr = min(RB, t1 - base);
+        for (int r = tid; r < nr; r += NT) {
+            const int j = I[base + r];
+            roff[r] = static_cast<uint32_t>(j * ldw * 2);
+#pragma unroll
+            for (int m = 0; m < MR; ++m)
+                xs[r][m] = m < M ? bf16_to_f32(Xb[m * ldx + j]) : 0.f;
+        }
+        __syncthreads();
+        // rows wave, wave + 4, ... of this pass; 8 loads in flight per lane
+        for (int r0 = wave; r0 < nr; r0 += 8 * NW) {
+            uint32_t w[8][4];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int r = r0 + NW * u;
+                if (VEC) {
+                    const uint32_t o = r < nr ? roff[r] + 16u * lane : 0x80000000u;
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(wr, o, 0, 0);
+                    w[u][0] = v[0]; w[u][1] = v[1]; w[u][2] = v[2]; w[u][3] = v[3];
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t o = r < nr ? roff[r] + 16u * lane + 4u * q : 0x80000000u;
+                        const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(wr, o, 0, 0);
+                        const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(wr, o + 2u, 0, 0);
+                        w[u][q] = lo | (hi << 16);
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int r = r0 + NW * u;
+                if (r < nr) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float wl = __uint_as_float(w[u][q] << 16);
+                        const float wh = __uint_as_float(w[u][q] & 0xffff0000u);
+#pragma unroll
+                        for (int m = 0; m < MR; ++m) {
+                            acc[m][2 * q] = __builtin_fmaf(xs[r][m], wl, acc[m][2 * q]);
+                            acc[m][2 * q + 1] = __builtin_fmaf(xs[r][m], wh, acc[m][2 * q + 1]);
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();                       // staged rows are reused by the next pass
+    }
+
+    // waves 1..3 hand their sums to wave 0, which adds them in wave order
+    if (wave > 0) {
+#pragma unroll
+        for (int m = 0; m < MR; ++m)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) red[wave - 1][m][8 * lane + e] = acc[m][e];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int w = 0; w < NW - 1; ++w)
+#pragma unroll
+        for (int m = 0; m < MR; ++m)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[m][e] += red[w][m][8 * lane + e];
+    const int nb = n0 + 8 * lane;
+#pragma unroll
+    for (int m = 0; m < MR; ++m) {
+        if (m >= M) break;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int n = nb + e;
+            if (n < N) {
+                if (DIRECT)
+                    Y[(static_cast<int64_t>(b) * M + m) * ldy + n] = f32_to_bf16(acc[m][e]);
+                else
+                    P[((static_cast<int64_t>(b) * S + s) * M + m) * N + n] = acc[m][e];
+            }
+        }
+    }
+}
+
+// Y[b][m][n] = sum over slices s, in order, of P[b][s][m][n]
+__global__ __launch_bounds__(256) void gemv_reduce_kernel(const float *__restrict__ P,
+                                                          uint16_t *__restrict__ Y, int M, int N,
+                                                          int S, int64_t ldy) {
+    const int n = blockIdx.x * 256 + threadIdx.x;
+    const int m = blockIdx.y, b = blockIdx.z;
+    if (n >= N) return;
+    const float *p = P + (static_cast<int64_t>(b) * S * M + m) * N + n;
+    const int64_t st = static_cast<int64_t>(M) * N;
+    float sum = 0.f;
+    int s = 0;
+    for (; s + 8 <= S; s += 8) {               // eight loads in flight, added in slice order
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = p[(s + u) * st];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += v[u];
+    }
+    for (; s < S; ++s) sum += p[s * st];
+    Y[(static_cast<int64_t>(b) * M + m) * ldy + n] = f32_to_bf16(sum);
+}
+
+template <int MR, bool VEC>
+hipError_t launch_mr(const uint16_t *X, const uint16_t *W, const int32_t *idx, int64_t B, int64_t M,
+                     int64_t N, int64_t K, int64_t k, int64_t ldx, int64_t ldw, uint16_t *Y,
+                     int64_t ldy, float *P, int SR, int S, hipStream_t stream) {
+    using namespace gv;
+    dim3 grid(static_cast<unsigned>((N + CW - 1) / CW), static_cast<unsigned>(S), static_cast<unsigned>(B));
+    if (S == 1) {
+        hipLaunchKernelGGL((gemv_partial_kernel<MR, VEC, true>), grid, dim3(NT), 0, stream, X, W, idx,
+                           P, Y, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
+                           static_cast<int>(k), ldx, ldw, ldy, SR, S);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((gemv_partial_kernel<MR, VEC, false>), grid, dim3(NT), 0, stream, X, W, idx,
+                       P, Y, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
+                       static_cast<int>(k), ldx, ldw, ldy, SR, S);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 rgrid(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(M), static_cast<unsigned>(B));
+    hipLaunchKernelGGL(gemv_reduce_kernel, rgrid, dim3(256), 0, stream, P, Y, static_cast<int>(M),
+                       static_cast<int>(N), S, ldy);
+    return hipGetLastError();
+}
+
+template <bool VEC>
+hipError_t launch_vec(const uint16_t *X, const uint16_t *W, const int32_t *idx, int64_t B, int64_t M,
+                      int64_t N, int64_t K, int64_t k, int64_t ldx, int64_t ldw, uint16_t *Y,
+                      int64_t ldy, float *P, int SR, int S, hipStream_t stream) {
+    if (M == 1) return launch_mr<1, VEC>(X, W, idx, B, M, N, K, k, ldx, ldw, Y, ldy, P, SR, S, stream);
+    if (M == 2) return launch_mr<2, VEC>(X, W, idx, B, M, N, K, k, ldx, ldw, Y, ldy, P, SR, S, stream);
+    if (M <= 4) return launch_mr<4, VEC>(X, W, idx, B, M, N, K, k, ldx, ldw, Y, ldy, P, SR, S, stream);
+    return launch_mr<8, VEC>(X, W, idx, B, M, N, K, k, ldx, ldw, Y, ldy, P, SR, S, stream);
+}
+
+}  // namespace
+
+// Rows per slice (a multiple of 4) and slice count: enough workgroups to
+// keep every CU streaming, at least MIN_SLICE rows per slice.
+void gemv_slices(int64_t B, int64_t N, int64_t k, int *SR, int *S) {
+    const int64_t chunks = (N + gv::CW - 1) / gv::CW;
+    int64_t s = (gv::TARGET_BLOCKS + B * chunks - 1) / (B * chunks);
+    const int64_t smax = (k + gv::MIN_SLICE - 1) / gv::MIN_SLICE;
+    if (s > smax) s = smax;
+    if (s < 1) s = 1;
+    int64_t sr = (k + s - 1) / s;
+    sr = (sr + 3) / 4 * 4;
+    *SR = static_cast<int>(sr);
+    *S = static_cast<int>((k + sr - 1) / sr);
+}
+
+size_t gemv_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t k) {
+    int SR, S;
+    gemv_slices(B, N, k, &SR, &S);
+    return S == 1 ? 0 : static_cast<size_t>(B) * S * M * N * sizeof(float);
+}
+
+hipError_t launch_gemv_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx, int64_t B,
+                            int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx, int64_t ldw,
+                            uint16_t *Y, int64_t ldy, void *workspace, hipStream_t stream) {
+    int SR, S;
+    gemv_slices(B, N, k, &SR, &S);
+    const bool vec = ldw % 8 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+    float *P = static_cast<float *>(workspace);
+    return vec ? launch_vec<true>(X, W, idx, B, M, N, K, k, ldx, ldw, Y, ldy, P, SR, S, stream)
+               : launch_vec<false>(X, W, idx, B, M, N, K, k, ldx, ldw, Y, ldy, P, SR, S, stream);
+}
+
+}  // namespace rmm

@@ -26,6 +26,9 @@ hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t 
                         int64_t ldxt, hipStream_t stream);
 
 // -------------------------------------------------------------- selection
+// TopK of x_j^2 for units of one token (row b of X at b * ldx)
+hipError_t launch_select_tokens(const void *X, bool bf16, int64_t B, int64_t K, int64_t ldx,
+                                int64_t k, int32_t *idx, hipStream_t stream);
 hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
                          int32_t *idx, hipStream_t stream);
 
@@ -44,6 +47,14 @@ hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx,
                            int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                            int64_t ldx, int64_t ldw, float *Y, int64_t ldy,
                            hipStream_t stream);
+
+// reduced product with M <= 8 rows per unit (decode); workspace holds the
+// per-slice fp32 partials when the retained list is split
+void gemv_slices(int64_t B, int64_t N, int64_t k, int *SR, int *S);
+size_t gemv_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t k);
+hipError_t launch_gemv_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx, int64_t B,
+                            int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx, int64_t ldw,
+                            uint16_t *Y, int64_t ldy, void *workspace, hipStream_t stream);
 
 // --------------------------------------------------------- reduced QK^T
 // reduced attention block, bf16, D == 128, 16-byte aligned (checked by the

@@ -10,7 +10,9 @@
 // holding the k-th key is taken whole.  Keys tied with
 // the k-th key are taken lowest index first, and the kept indices are
 // compacted in ascending order with two workgroup prefix scans.  Each thread
-// owns a contiguous chunk of keys, kept in registers when it fits.
+// owns a contiguous chunk of keys, kept in registers when it fits.  For a
+// unit of one token (a decode step) the keys come straight from the token's
+// activations: 16 (bf16) or 31 (fp32) key bits, so at most two passes.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -53,10 +55,32 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *b
     return r;
 }
 
+// Where the keys come from: a unit's float64 energies, or (a unit of one
+// token) the token's bf16 or fp32 activations.  For one token the energy of
+// index j is x_j^2, which is exact in float64 and orders like |x_j|, whose
+// IEEE bits (sign cleared) are already an unsigned order key: equal |x| tie
+// exactly as equal squares do, +inf ranks above every finite value and every
+// NaN is mapped to one key above +inf -- the order of the energy keys.
+enum KeySrc { kEnergy = 0, kTokenBf16 = 1, kTokenF32 = 2 };
+
+template <int SRC>
+__device__ __forceinline__ uint64_t load_key(const void *row, int64_t j) {
+    if constexpr (SRC == kEnergy) {
+        return order_key(static_cast<const double *>(row)[j]);
+    } else if constexpr (SRC == kTokenBf16) {
+        uint32_t a = static_cast<const uint16_t *>(row)[j] & 0x7fffu;
+        return a > 0x7f80u ? 0x7fc0u : a;
+    } else {
+        uint32_t a = static_cast<const uint32_t *>(row)[j] & 0x7fffffffu;
+        return a > 0x7f800000u ? 0x7fc00000u : a;
+    }
+}
+
 // NT threads; C keys per thread held in registers (REG) or re-read from
-// memory (REG == false, chunk size `cpt` at run time).
-template <int NT, int C, bool REG>
-__global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ energy,
+// memory (REG == false, chunk size `cpt` at run time).  Unit u's keys start
+// at element u * ld of `src`.
+template <int NT, int C, bool REG, int SRC>
+__global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src, int64_t ld,
                                                     int64_t K, int64_t k, int cpt,
                                                     int32_t *__restrict__ idx) {
     __shared__ uint32_t hist[256];
@@ -64,7 +88,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ e
     __shared__ uint32_t s_digit, s_above, s_count;
 
     const int tid = threadIdx.x;
-    const double *e = energy + static_cast<int64_t>(blockIdx.x) * K;
+    constexpr int esize = SRC == kEnergy ? 8 : SRC == kTokenBf16 ? 2 : 4;
+    const void *e = static_cast<const char *>(src) + static_cast<int64_t>(blockIdx.x) * ld * esize;
     int32_t *out = idx + static_cast<int64_t>(blockIdx.x) * k;
     const int chunk = REG ? C : cpt;
     const int64_t c0 = static_cast<int64_t>(tid) * chunk;
@@ -79,12 +104,12 @@ __global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ e
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int64_t j = c0 + c;
-            keys[c] = j < K ? order_key(e[j]) : 0ull;
+            keys[c] = j < K ? load_key<SRC>(e, j) : 0ull;
         }
     }
     auto key_at = [&](int c) -> uint64_t {
         if constexpr (REG) return keys[c];
-        else return order_key(e[c0 + c]);
+        else return load_key<SRC>(e, c0 + c);
     };
     const int n_own = static_cast<int>(max<int64_t>(0, min<int64_t>(chunk, K - c0)));
 
@@ -192,28 +217,40 @@ __global__ __launch_bounds__(NT) void select_kernel(const double *__restrict__ e
     }
 }
 
-template <int NT, int C, bool REG>
-hipError_t launch(const double *energy, int64_t B, int64_t K, int64_t k, int cpt,
+template <int NT, int C, bool REG, int SRC>
+hipError_t launch(const void *src, int64_t ld, int64_t B, int64_t K, int64_t k, int cpt,
                   int32_t *idx, hipStream_t stream) {
-    hipLaunchKernelGGL((select_kernel<NT, C, REG>), dim3(static_cast<unsigned>(B)), dim3(NT), 0,
-                       stream, energy, K, k, cpt, idx);
+    hipLaunchKernelGGL((select_kernel<NT, C, REG, SRC>), dim3(static_cast<unsigned>(B)), dim3(NT), 0,
+                       stream, src, ld, K, k, cpt, idx);
     return hipGetLastError();
+}
+
+template <int SRC>
+hipError_t launch_src(const void *src, int64_t ld, int64_t B, int64_t K, int64_t k, int32_t *idx,
+                      hipStream_t stream) {
+    if (K <= 256) return launch<256, 1, true, SRC>(src, ld, B, K, k, 1, idx, stream);
+    if (K <= 512) return launch<256, 2, true, SRC>(src, ld, B, K, k, 2, idx, stream);
+    if (K <= 1024) return launch<256, 4, true, SRC>(src, ld, B, K, k, 4, idx, stream);
+    if (K <= 2048) return launch<256, 8, true, SRC>(src, ld, B, K, k, 8, idx, stream);
+    if (K <= 4096) return launch<1024, 4, true, SRC>(src, ld, B, K, k, 4, idx, stream);
+    if (K <= 8192) return launch<1024, 8, true, SRC>(src, ld, B, K, k, 8, idx, stream);
+    if (K <= 16384) return launch<1024, 16, true, SRC>(src, ld, B, K, k, 16, idx, stream);
+    if (K <= 32768) return launch<1024, 32, true, SRC>(src, ld, B, K, k, 32, idx, stream);
+    const int cpt = static_cast<int>((K + 1023) / 1024);
+    return launch<1024, 1, false, SRC>(src, ld, B, K, k, cpt, idx, stream);
 }
 
 }  // namespace
 
 hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
                          int32_t *idx, hipStream_t stream) {
-    if (K <= 256) return launch<256, 1, true>(energy, B, K, k, 1, idx, stream);
-    if (K <= 512) return launch<256, 2, true>(energy, B, K, k, 2, idx, stream);
-    if (K <= 1024) return launch<256, 4, true>(energy, B, K, k, 4, idx, stream);
-    if (K <= 2048) return launch<256, 8, true>(energy, B, K, k, 8, idx, stream);
-    if (K <= 4096) return launch<1024, 4, true>(energy, B, K, k, 4, idx, stream);
-    if (K <= 8192) return launch<1024, 8, true>(energy, B, K, k, 8, idx, stream);
-    if (K <= 16384) return launch<1024, 16, true>(energy, B, K, k, 16, idx, stream);
-    if (K <= 32768) return launch<1024, 32, true>(energy, B, K, k, 32, idx, stream);
-    const int cpt = static_cast<int>((K + 1023) / 1024);
-    return launch<1024, 1, false>(energy, B, K, k, cpt, idx, stream);
+    return launch_src<kEnergy>(energy, K, B, K, k, idx, stream);
+}
+
+hipError_t launch_select_tokens(const void *X, bool bf16, int64_t B, int64_t K, int64_t ldx,
+                                int64_t k, int32_t *idx, hipStream_t stream) {
+    return bf16 ? launch_src<kTokenBf16>(X, ldx, B, K, k, idx, stream)
+                : launch_src<kTokenF32>(X, ldx, B, K, k, idx, stream);
 }
 
 }  // namespace rmm

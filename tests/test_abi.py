@@ -233,3 +233,60 @@ def test_binding_rejects_host_tensors():
     e = torch.zeros(8, dtype=torch.float64)
     with pytest.raises(ValueError):
         rmm.rmm_score(x, e)
+
+
+def test_gemv_validation():
+    f = rmm.lib.rmm_reduced_gemv
+    need = rmm.rmm_gemv_workspace_size(1, 1, 4096, 2048)
+    assert need > 0                          # one token: the list is split over slices
+    base = [P, P, P, 1, 1, 1, 4096, 4096, 2048, 4096, 4096, P, 4096, P, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 11):
+        assert call(i, NULL) == INVALID
+    assert call(3, 7) == INVALID            # dtype
+    assert call(3, 0) == UNSUPPORTED        # fp32
+    assert call(5, 9) == UNSUPPORTED        # more than 8 rows per unit
+    assert call(8, 0) == INVALID            # k
+    assert call(10, 4000) == INVALID        # ldw < N
+    assert call(13, NULL) == WS_SMALL
+    assert call(14, need - 1) == WS_SMALL
+    assert call(13, ctypes.c_void_p(0x100008)) == INVALID     # workspace not 16-byte aligned
+    big = list(base)
+    big[7], big[9], big[10] = 65536, 65536, 65536     # K * ldw * 2 reaches 2^33
+    big[6], big[12] = 65536, 65536
+    assert f(*big) == UNSUPPORTED
+
+
+def test_gemv_workspace_size():
+    # many units and wide rows: one slice per workgroup column, no partials
+    assert rmm.rmm_gemv_workspace_size(16, 1, 28672, 64) == 0
+    # one unit: fp32 partials of every slice, 256-byte aligned
+    n = rmm.rmm_gemv_workspace_size(1, 1, 4096, 2048)
+    assert n > 0 and n % 256 == 0 and n % (4096 * 4) == 0
+    assert rmm.rmm_gemv_workspace_size(1, 2, 4096, 2048) == 2 * n
+    for bad in ((0, 1, 8, 8), (1, 0, 8, 8), (1, 9, 8, 8), (1, 1, 0, 8), (1, 1, 8, 0)):
+        assert rmm.rmm_gemv_workspace_size(*bad) == 0
+
+
+def test_select_tokens_validation():
+    f = rmm.lib.rmm_select_tokens
+    base = [P, 1, 2, 4096, 4096, 100, P, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    assert call(0, NULL) == INVALID
+    assert call(6, NULL) == INVALID
+    assert call(1, 5) == INVALID            # dtype
+    assert call(2, 0) == INVALID            # B
+    assert call(3, 0) == INVALID            # K
+    assert call(5, 0) == INVALID            # k
+    assert call(5, 4097) == INVALID         # k > K
+    assert call(4, 4095) == INVALID         # ldx < K
