@@ -720,6 +720,51 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     const int rows = min(BT, M - m0);
     const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
         Yu + static_cast<int64_t>(m0) * ldy, 0, static_cast<uint32_t>(rows * ldy * 2), 0x00020000);
+    if (vec_y == 2 && n0 + BT <= N) {
+        // Whole-width tile with 16-byte aligned rows: the tile goes out in two
+        // passes through the (now idle) ring, so that every store writes 16
+        // bytes of a 512-byte row run.  Pass p holds fragments i = 2p, 2p+1 of
+        // every wave: 128 rows, 32 per ring object; within a row the 16-byte
+        // chunk c sits at position c ^ (row % 32).
+        static_assert(FM == 4 && BT == 256, "staged epilogue layout");
+        auto obj = [&](int q) -> char * {
+            return q == 0 ? sA0 : q == 1 ? sA1 : q == 2 ? sB0 : sB1;
+        };
+        __syncthreads();                      // ring reads done, tail loads landed
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii) {
+                const int i = 2 * p + ii;
+                char *o = obj(2 * wm + ii);
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        const int c = (wn * TWN) / 8 + 4 * j + gq;
+                        typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+                        const u32x2_t v = {pack_bf16x2(acc[j][i][4 * gq], acc[j][i][4 * gq + 1]),
+                                           pack_bf16x2(acc[j][i][4 * gq + 2], acc[j][i][4 * gq + 3])};
+                        *reinterpret_cast<u32x2_t *>(o + lr * ROWB + 16 * (c ^ lr) + 8 * lh) = v;
+                    }
+            }
+            __syncthreads();
+            // wave w stores half-tile rows 16w .. 16w+15, two rows per instruction
+            const char *o = obj(wave / 2);
+            const int c = lane & 31;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int rl = 16 * (wave & 1) + 2 * q + lh;          // row within the object
+                const int R = 16 * wave + 2 * q + lh;                 // row within the half tile
+                const int ml = (R / 64) * 128 + 64 * p + (R % 64);
+                typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+                const u32x4_t v = *reinterpret_cast<const u32x4_t *>(o + rl * ROWB + 16 * (c ^ rl));
+                __builtin_amdgcn_raw_buffer_store_b128(v, yr, static_cast<uint32_t>((ml * ldy + n0 + 8 * c) * 2), 0, 0);
+            }
+            if (p == 0) __syncthreads();      // pass 1 overwrites the staged rows
+        }
+        return;
+    }
     const bool full_n = vec_y && n0 + BT <= N;
 #pragma unroll
     for (int j = 0; j < FN; ++j)
@@ -854,7 +899,8 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
     // Y rows of one 256-row tile are addressed with 32-bit byte offsets
     if (t256 * B >= 128 && ldy < (int64_t(1) << 23)) {
         const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
-        const int vec_y = reinterpret_cast<uintptr_t>(Y) % 8 == 0 && ldy % 4 == 0;
+        const int vec_y = (reinterpret_cast<uintptr_t>(Y) % 16 == 0 && ldy % 8 == 0) ? 2
+                          : (reinterpret_cast<uintptr_t>(Y) % 8 == 0 && ldy % 4 == 0) ? 1 : 0;
         hipLaunchKernelGGL((gemm_kmajor_tr_kernel<kTrWaves, kTrRows, kTrStages>),
                            dim3(tm * tn, static_cast<unsigned>(B)), dim3(kTrWaves * 64), 0, stream,
                            Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),

@@ -283,10 +283,13 @@ def test_reduced_gemm_kmajor(B, M, N, K, k, seed):
         check_product(Yn[b], ref, np.abs(X[b][:, idx[b]]) @ np.abs(W[idx[b], :]), k, "bf16")
 
 
-@pytest.mark.parametrize("pad", [3, 8])
+@pytest.mark.parametrize("pad", [3, 6, 10])
 def test_reduced_gemm_kmajor_strided_y(pad):
-    """256-wide tiles with Y rows longer than N: an odd row stride takes the
-    element-wise store path; nothing is written past column N."""
+    """256-wide tiles with Y rows longer than N, one per store path: an odd
+    row stride (pad 3) stores element by element, a stride of 4 mod 8 (pad 6)
+    in 8-byte pieces, a stride of 0 mod 8 (pad 10) stages whole-width tiles
+    through LDS and stores 16-byte row pieces.  Nothing is written past
+    column N."""
     dev = require_gpu()
     B, M, N, K, k = 3, 2050, 1030, 300, 150
     Xs = wl.random_case(60 + pad, (B, M, K), "bf16", n_outlier=8)
