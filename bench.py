@@ -64,9 +64,9 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
 # averaged over the kernel's dispatches.  Each figure is valid only for the
 # source whose SHA-256 is recorded and for the same launch mix.
 GEMM_TRAFFIC = {"source": GEMM_SOURCE,
-                "sha256": "72dbcdbafdde24c62b0e5bb8237c112b3aecc5b888cb5810092f0f2eba4b086b",
+                "sha256": "11e911b1d8786feb4504a3e740ba2f9821fec13ed3ab6f6eb89d24b28300329d",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
-                "bytes": round((399783.32 * 2.0 + 227851.38) * 1024)}
+                "bytes": round((399647.63 * 2.0 + 172032.00) * 1024)}
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"source": os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "attn.hip"),
