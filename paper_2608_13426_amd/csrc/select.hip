@@ -217,6 +217,122 @@ __global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src
     }
 }
 
+// One bf16 token per workgroup (a decode step), K <= 16 * 1024: the keys are
+// the 15 magnitude bits, so the k-th largest key is found in at most two
+// histogram passes (bits 14..7, then 6..0), each of the NT threads owning C
+// consecutive keys loaded as 16-byte vectors.  The kept set is then
+// written in ascending order after one scan of a packed pair per thread
+// (keys above the threshold | ties with it << 16): a kept key's slot is the
+// number of kept keys before it, i.e. keys above before it plus
+// min(ties before it, ties kept).
+template <int NT, int C>
+__global__ __launch_bounds__(NT) void select_token16_kernel(const uint16_t *__restrict__ X,
+                                                            int64_t ldx, int K, int k,
+                                                            int32_t *__restrict__ idx) {
+    static_assert(C % 8 == 0 && C <= 16 && NT >= 256 && NT <= 1024, "chunk");
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t scan_buf[NT / kWave];
+    __shared__ int s_thr, s_need;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const uint16_t *x = X + static_cast<int64_t>(blockIdx.x) * ldx;
+    int32_t *out = idx + static_cast<int64_t>(blockIdx.x) * k;
+    if (k == K) {                       // everything is kept
+        for (int j = tid; j < K; j += NT) out[j] = j;
+        return;
+    }
+    const int c0 = tid * C;
+    // keys past K are marked with bit 15 and never counted
+    uint32_t key[C];
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(x), 0, static_cast<uint32_t>(K) * 2u, 0x00020000);
+#pragma unroll
+    for (int q = 0; q < C / 8; ++q) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, static_cast<uint32_t>(c0 + 8 * q) * 2u, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const uint32_t h = (v[e / 2] >> (16 * (e % 2))) & 0x7fffu;
+            key[8 * q + e] = c0 + 8 * q + e < K ? (h > 0x7f80u ? 0x7fc0u : h) : 0x8000u;
+        }
+    }
+    // pass 1 over bits 14..7, pass 2 over bits 6..0 of the keys in the chosen bucket
+    int need = k, thr = -1, take_ties = 0;
+    int prefix = -1;                    // pass-1 digit, once chosen
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        if (tid < 256) hist[tid] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const uint32_t u = key[c];
+            if (u & 0x8000u) continue;
+            if (pass == 0) atomicAdd(&hist[u >> 7], 1u);
+            else if (static_cast<int>(u >> 7) == prefix) atomicAdd(&hist[u & 0x7fu], 1u);
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            // lane L holds digits 255-4L .. 252-4L (descending value order)
+            uint32_t h[4], sum = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) { h[q] = hist[255 - 4 * lane - q]; sum += h[q]; }
+            const uint32_t incl = wave_inclusive_scan(sum, lane);
+            uint32_t run = incl - sum;
+            const uint32_t nd = static_cast<uint32_t>(need);
+            if (run < nd && nd <= incl) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (run + h[q] >= nd) {
+                        s_thr = 255 - 4 * lane - q;
+                        s_need = static_cast<int>(nd - run);   // keys of this bucket to keep
+                        hist[0] = h[q];                        // its size (read after the barrier)
+                        break;
+                    }
+                    run += h[q];
+                }
+            }
+        }
+        __syncthreads();
+        const int d = s_thr, nb = s_need, size = static_cast<int>(hist[0]);
+        __syncthreads();                // hist is cleared by the next pass
+        if (pass == 0) {
+            if (size == nb) { thr = (d << 7) - 1; take_ties = 0; break; }   // the whole bucket
+            prefix = d;
+            need = nb;
+        } else {
+            thr = (prefix << 7) | d;    // the k-th largest key; keep nb of its ties
+            take_ties = nb;
+        }
+    }
+    // compaction: keys above thr, then the first take_ties keys equal to thr
+    uint32_t above = 0, ties = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int u = static_cast<int>(key[c]);
+        above += u < 0x8000 && u > thr;
+        ties += u == thr;
+    }
+    const uint32_t pre = block_exclusive_scan<NT>(above | (ties << 16), scan_buf);
+    int sa = static_cast<int>(pre & 0xffffu), st = static_cast<int>(pre >> 16);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int u = static_cast<int>(key[c]);
+        if (u < 0x8000 && u > thr) {
+            out[sa + min(st, take_ties)] = c0 + c;
+            ++sa;
+        } else if (u == thr) {
+            if (st < take_ties) out[sa + st] = c0 + c;
+            ++st;
+        }
+    }
+}
+
+template <int NT, int C>
+hipError_t launch_token16(const void *X, int64_t ldx, int64_t B, int64_t K, int64_t k, int32_t *idx,
+                          hipStream_t stream) {
+    hipLaunchKernelGGL((select_token16_kernel<NT, C>), dim3(static_cast<unsigned>(B)), dim3(NT), 0, stream,
+                       static_cast<const uint16_t *>(X), ldx, static_cast<int>(K), static_cast<int>(k), idx);
+    return hipGetLastError();
+}
+
 template <int NT, int C, bool REG, int SRC>
 hipError_t launch(const void *src, int64_t ld, int64_t B, int64_t K, int64_t k, int cpt,
                   int32_t *idx, hipStream_t stream) {
@@ -249,6 +365,12 @@ hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
 
 hipError_t launch_select_tokens(const void *X, bool bf16, int64_t B, int64_t K, int64_t ldx,
                                 int64_t k, int32_t *idx, hipStream_t stream) {
+    if (bf16 && K <= 16 * 1024 && reinterpret_cast<uintptr_t>(X) % 16 == 0 && ldx % 8 == 0) {
+        if (K <= 8 * 256) return launch_token16<256, 8>(X, ldx, B, K, k, idx, stream);
+        if (K <= 16 * 256) return launch_token16<256, 16>(X, ldx, B, K, k, idx, stream);
+        if (K <= 16 * 512) return launch_token16<512, 16>(X, ldx, B, K, k, idx, stream);
+        return launch_token16<1024, 16>(X, ldx, B, K, k, idx, stream);
+    }
     return bf16 ? launch_src<kTokenBf16>(X, ldx, B, K, k, idx, stream)
                 : launch_src<kTokenF32>(X, ldx, B, K, k, idx, stream);
 }
