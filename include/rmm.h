@@ -58,7 +58,8 @@ typedef enum rmm_op {
     RMM_OP_SCORE = 0,   /* rmm_score   */
     RMM_OP_SELECT = 1,  /* rmm_select  */
     RMM_OP_LINEAR = 2,  /* rmm_linear  */
-    RMM_OP_ATTENTION = 3 /* rmm_reduced_attention */
+    RMM_OP_ATTENTION = 3, /* rmm_reduced_attention */
+    RMM_OP_PV = 4         /* rmm_reduced_pv */
 } rmm_op_t;
 
 /*
@@ -80,6 +81,7 @@ int64_t rmm_retained_count(double r, int64_t K);
  *   RMM_OP_ATTENTION: B = batch*H, M = Lk, K = D, k  (each query head's
  *                  retained key dims as rows: B*Lk*kp bf16, kp = k rounded
  *                  up to 32, 64, 96 or 128)
+ *   RMM_OP_PV    : B = batch*H, M = Lq, K = Lk, k = kt (as RMM_OP_LINEAR)
  * Returns 0 for non-positive sizes.  Host-only.
  */
 size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t k);
@@ -300,6 +302,38 @@ rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtyp
                         int64_t B, int64_t M, int64_t N, int64_t K, int64_t ldx,
                         int64_t ldw, void *Y, int64_t ldy, int32_t *idx_out,
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Token-axis reduced value product   (Sec. 3.3, attention: token scores are
+ * the column norms of the attention weights P, the value product keeps the
+ * top ceil(rho_t * Lk) tokens; App. D: its MACs scale with rho_t).
+ *
+ *   a[u][t]    = sum_q P[u][q][t]^2             float64 (orders like the norm)
+ *   T_u        = TopK(a[u], kt)                  ties -> lower index, ascending
+ *   O[u][q][d] = sum_{t in T_u} P[u][q][t] * V[v(u)][t][d]
+ *
+ * with u = b*H + h over the batch*H query heads and v(u) = b*Hkv + h/(H/Hkv)
+ * their shared value head.  Run as rmm_score over each head's Lq rows, one
+ * rmm_select per head, then one gathered product per (sequence, kv head)
+ * with that head's H/Hkv query heads as units (K-major path as rmm_linear).
+ *
+ * P   : [batch][H][Lq][ldp] (e.g. softmax probabilities), ldp >= Lk.
+ * V   : [batch][Hkv][Lk][D], rows contiguous.  Same dtype as P.
+ * O   : [batch][H][Lq][D], written.
+ * kt  : tokens kept per head, 1 <= kt <= Lk (rmm_retained_count(rho_t, Lk)).
+ * idx_out   : int32 [batch*H*kt] receiving the token sets, or NULL (kept in
+ *             the workspace).
+ * workspace : rmm_workspace_size(RMM_OP_PV, batch*H, Lq, Lk, kt) bytes,
+ *             256-byte aligned.
+ * Errors    : INVALID_ARGUMENT for null P/V/O, sizes < 1, H % Hkv != 0, kt
+ *             outside [1, Lk], ldp < Lk, or a misaligned workspace;
+ *             UNSUPPORTED when batch*H exceeds the grid limit;
+ *             WORKSPACE_TOO_SMALL.
+ */
+rmm_status_t rmm_reduced_pv(const void *P, const void *V, rmm_dtype_t dtype, int64_t batch,
+                            int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                            int64_t ldp, int64_t kt, void *O, int32_t *idx_out,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);

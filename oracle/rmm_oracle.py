@@ -22,7 +22,9 @@ Paper passages followed (arXiv 2608.13426, "Reduced Matrix Multiplication"):
   scores are (1 / sqrt(d_h)) Q[:, I] K[:, I]^T with the full d_h in the
   scale; the optional causal mask M is added before the softmax; with
   grouped-query attention the selection is made per query head and applied
-  to the shared K.
+  to the shared K.  Optionally the value product PV is reduced over the
+  token axis: token scores a_t = ||P[:, t]||_2, T = TopK(a, ceil(rho_t L_k)),
+  O = P[:, T] V[T, :].
 * Sec. 3.5 and Appendix E: the rank-one decomposition, the error bound
   (Proposition "RMM Approximation Error Bound"), the factorised bound
   (Corollary) and the normalised bound with the discarded-energy ratios;
@@ -59,6 +61,7 @@ import numpy as np
 __all__ = [
     "retained_count", "column_energies", "topk_indices", "reduced_matmul",
     "rmm", "rmm_batched", "gqa_kv_head", "reduced_qk", "rmm_qk", "reduced_attention",
+    "reduced_pv",
     "residual_energy", "retained_energy_fraction", "discarded_energy_ratio",
     "rank_one_bound", "factorized_bound", "normalized_bound",
     "selection_margin",
@@ -241,6 +244,24 @@ def reduced_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, idx: np.ndarr
             w[keep] = np.exp(s[keep] - s[keep].max())
             O[h, i] = (w / w.sum()) @ V[g]
     return O
+
+
+def reduced_pv(P: np.ndarray, V: np.ndarray, kt: int):
+    """Token-axis reduced value product (Sec. 3.3, attention).
+
+    P [H x Lq x Lk] holds the attention weights of H query heads, V
+    [Hkv x Lk x Dv] the value rows of their kv heads.  For each head h: the
+    token scores are the column norms of P[h], ranked by their squares
+    a_t^2 = column_energies(P[h]); T_h = TopK(a, kt); the output is
+    P[h][:, T_h] @ V[g(h)][T_h, :].  Returns (O [H x Lq x Dv] float64,
+    idx [H x kt]).
+    """
+    P = np.asarray(P, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    H, Hkv = P.shape[0], V.shape[0]
+    idx = np.stack([topk_indices(column_energies(P[h]), kt) for h in range(H)])
+    O = np.stack([reduced_matmul(P[h], V[gqa_kv_head(h, H, Hkv)], idx[h]) for h in range(H)])
+    return O, idx
 
 
 # ---------------------------------------------------------------------------

@@ -16,7 +16,8 @@ import torch
 
 __all__ = [
     "RmmError", "LIB_PATH", "lib", "RMM_F32", "RMM_BF16", "RMM_OP_SCORE",
-    "RMM_OP_SELECT", "RMM_OP_LINEAR", "RMM_OP_ATTENTION", "rmm_retained_count", "rmm_workspace_size",
+    "RMM_OP_SELECT", "RMM_OP_LINEAR", "RMM_OP_ATTENTION", "RMM_OP_PV", "rmm_retained_count",
+    "rmm_workspace_size", "rmm_reduced_pv",
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
     "rmm_reduced_attention", "rmm_reduced_gemv", "rmm_gemv_workspace_size", "rmm_select_tokens",
@@ -26,7 +27,7 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
 
 RMM_F32, RMM_BF16 = 0, 1
-RMM_OP_SCORE, RMM_OP_SELECT, RMM_OP_LINEAR, RMM_OP_ATTENTION = 0, 1, 2, 3
+RMM_OP_SCORE, RMM_OP_SELECT, RMM_OP_LINEAR, RMM_OP_ATTENTION, RMM_OP_PV = 0, 1, 2, 3, 4
 
 _p = ctypes.c_void_p
 _i64 = ctypes.c_int64
@@ -54,6 +55,8 @@ _SIGS = {
     "rmm_reduced_attention": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int, _i64, _i64, _i64, _i64,
                                              _i64, _i64, _i64, ctypes.c_float, ctypes.c_int, _p,
                                              _p, ctypes.c_size_t, _p]),
+    "rmm_reduced_pv": (ctypes.c_int, [_p, _p, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64,
+                                      _i64, _i64, _p, _p, _p, ctypes.c_size_t, _p]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -355,6 +358,41 @@ def rmm_reduced_attention(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor, id
         Q.data_ptr(), Kc.data_ptr(), V.data_ptr(), idx.data_ptr(), _dtype_code(Q), batch, H, Hkv,
         Lq, Lk, D, k, float(scale), 1 if causal else 0, O.data_ptr(), workspace.data_ptr(),
         ws_bytes, _stream(d, stream)))
+    return O
+
+
+def rmm_reduced_pv(P: torch.Tensor, V: torch.Tensor, kt: int, O: torch.Tensor,
+                   idx_out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                   stream=None) -> torch.Tensor:
+    """Token-axis reduced value product (Sec. 3.3): per query head u, the kt
+    tokens with the largest column norms of P[u] and O[u] = P[u][:, T] @
+    V[kv(u)][T, :].  P: [batch, H, Lq, Lk] (rows contiguous, any row stride),
+    V: [batch, Hkv, Lk, D] contiguous, O: [batch, H, Lq, D] contiguous;
+    `idx_out` (int32 [batch*H*kt]) receives the token sets when given."""
+    if P.dim() != 4 or V.dim() != 4 or O.dim() != 4:
+        raise ValueError("P, V and O must be 4-D")
+    batch, H, Lq, Lk = P.shape
+    if P.stride(3) != 1 or P.stride(1) != Lq * P.stride(2) or P.stride(0) != H * P.stride(1):
+        raise ValueError("P must be [batch, H, Lq, Lk] with contiguous rows and packed rows")
+    ldp = P.stride(2)
+    if V.shape[0] != batch or V.shape[2] != Lk or not V.is_contiguous():
+        raise ValueError("V must be contiguous [batch, Hkv, Lk, D]")
+    Hkv, D = V.shape[1], V.shape[3]
+    if tuple(O.shape) != (batch, H, Lq, D) or not O.is_contiguous():
+        raise ValueError("O must be contiguous [batch, H, Lq, D]")
+    d = _dev(P, V, O)
+    if not (P.dtype == V.dtype == O.dtype):
+        raise TypeError("P, V and O must share one dtype")
+    if idx_out is not None and (idx_out.dtype != torch.int32 or idx_out.numel() != batch * H * kt
+                                or not idx_out.is_contiguous()):
+        raise ValueError("idx_out must be contiguous int32 [batch*H*kt]")
+    if workspace is None:
+        workspace = torch.empty(max(rmm_workspace_size(RMM_OP_PV, batch * H, Lq, Lk, kt), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_reduced_pv", lib.rmm_reduced_pv(
+        P.data_ptr(), V.data_ptr(), _dtype_code(P), batch, H, Hkv, Lq, Lk, D, ldp, int(kt),
+        O.data_ptr(), _ptr(idx_out), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
     return O
 
 

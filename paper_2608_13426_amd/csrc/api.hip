@@ -88,6 +88,7 @@ size_t rmm_workspace_size(rmm_op_t op, int64_t B, int64_t M, int64_t K, int64_t 
     case RMM_OP_SELECT:
         return 0;
     case RMM_OP_LINEAR:
+    case RMM_OP_PV:
         if (M < 1 || k < 1 || k > K) return 0;
         return align256(rmm::score_workspace_bytes(B, M, K)) +
                align256(static_cast<size_t>(B * K) * sizeof(double)) +
@@ -286,6 +287,64 @@ rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtyp
     else
         e = rmm::launch_gemm_f32(static_cast<const float *>(X), static_cast<const float *>(W), idx,
                                  B, M, N, K, k, ldx, ldw, static_cast<float *>(Y), ldy, stream);
+    return from_hip(e);
+}
+
+rmm_status_t rmm_reduced_pv(const void *P, const void *V, rmm_dtype_t dtype, int64_t batch,
+                            int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D, int64_t ldp,
+                            int64_t kt, void *O, int32_t *idx_out, void *workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+    if (!P || !V || !O) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (H % Hkv != 0) return RMM_ERR_INVALID_ARGUMENT;
+    const int64_t U = batch * H, grp = H / Hkv;
+    // one product per (sequence, kv head): its query heads' units against V
+    rmm_status_t st = check_gemm_shapes(P, V, dtype, grp, Lq, D, Lk, kt, ldp, D, O, D);
+    if (st != RMM_OK) return st;
+    if (U > kGridYZMax) return RMM_ERR_UNSUPPORTED;
+    const size_t need = rmm_workspace_size(RMM_OP_PV, U, Lq, Lk, kt);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
+
+    char *ws = static_cast<char *>(workspace);
+    double *partials = reinterpret_cast<double *>(ws);
+    ws += align256(rmm::score_workspace_bytes(U, Lq, Lk));
+    double *energy = reinterpret_cast<double *>(ws);
+    ws += align256(static_cast<size_t>(U * Lk) * sizeof(double));
+    int32_t *idx = idx_out ? idx_out : reinterpret_cast<int32_t *>(ws);
+    ws += align256(static_cast<size_t>(U * kt) * sizeof(int32_t));
+    uint16_t *Pt = reinterpret_cast<uint16_t *>(ws);
+
+    // token energies of every head (column sums of P^2 over its queries),
+    // with the K-major copy of P for bf16, then every head's TopK
+    const bool bf16 = dtype == RMM_BF16;
+    const bool kmajor = bf16 && aligned16(P) && ldp % 8 == 0 && aligned16(Pt) &&
+                        kmajor_ok(Pt, V, grp, Lq, Lk, xt_ld(Lq), D);
+    hipError_t e = rmm::launch_score(P, bf16, U, Lq, Lk, ldp, energy, partials,
+                                     kmajor ? Pt : nullptr, xt_ld(Lq), stream);
+    if (e != hipSuccess) return RMM_ERR_HIP;
+    e = rmm::launch_select(energy, U, Lk, kt, idx, stream);
+    if (e != hipSuccess) return RMM_ERR_HIP;
+    const size_t esz = bf16 ? 2 : 4;
+    for (int64_t b = 0; b < batch && e == hipSuccess; ++b)
+        for (int64_t g = 0; g < Hkv && e == hipSuccess; ++g) {
+            const int64_t u0 = b * H + g * grp;
+            const char *Vg = static_cast<const char *>(V) + (b * Hkv + g) * Lk * D * esz;
+            char *Og = static_cast<char *>(O) + u0 * Lq * D * esz;
+            const int32_t *ig = idx + u0 * kt;
+            if (kmajor)
+                e = rmm::launch_gemm_kmajor_bf16(Pt + u0 * Lk * xt_ld(Lq), reinterpret_cast<const uint16_t *>(Vg),
+                                                 ig, grp, Lq, D, Lk, kt, xt_ld(Lq), D,
+                                                 reinterpret_cast<uint16_t *>(Og), D, stream);
+            else if (bf16)
+                e = rmm::launch_gemm_bf16(static_cast<const uint16_t *>(P) + u0 * Lq * ldp,
+                                          reinterpret_cast<const uint16_t *>(Vg), ig, grp, Lq, D, Lk, kt,
+                                          ldp, D, reinterpret_cast<uint16_t *>(Og), D, stream);
+            else
+                e = rmm::launch_gemm_f32(static_cast<const float *>(P) + u0 * Lq * ldp,
+                                         reinterpret_cast<const float *>(Vg), ig, grp, Lq, D, Lk, kt,
+                                         ldp, D, reinterpret_cast<float *>(Og), D, stream);
+        }
     return from_hip(e);
 }
 

@@ -408,6 +408,42 @@ def check_attention(o):
     assert np.array_equal(Or[:, 0], Of[:, 4]) and np.array_equal(Or[:, 1], Of[:, 1])
 
 
+def check_pv(o):
+    """Token-axis reduced value product (Sec. 3.3): token scores are the
+    column norms of each head's weights, the kt strongest tokens are kept."""
+    # hand-worked: column energies 0.29, 0.34, 0.25 -> tokens {0, 1}
+    P = np.array([[[0.5, 0.5, 0.0], [0.2, 0.3, 0.5]]])
+    V = np.array([[[1.0, 2.0], [-1.0, 4.0], [8.0, 8.0]]])
+    O, idx = o.reduced_pv(P, V, 2)
+    assert idx.tolist() == [[0, 1]]
+    assert np.allclose(O[0], [[0.0, 3.0], [-0.1, 1.6]], rtol=0, atol=1e-15)
+    # all tokens kept: the dense product (exact dot products, independent of the oracle)
+    P, V = _bf16(90, (3, 5, 9)), _bf16(91, (1, 9, 4))
+    O, idx = o.reduced_pv(P, V, 9)
+    for h in range(3):
+        assert np.allclose(O[h], exact_matmul(P[h], V[0]), rtol=1e-14, atol=1e-15)
+        assert idx[h].tolist() == list(range(9))
+    # brute force: the kept tokens carry the most energy (ties -> lower index),
+    # and the dropped part is the sum of the discarded rank-one terms
+    for seed in range(4):
+        P, V = _ints(92 + seed, (2, 4, 7), -3, 4), _bf16(96 + seed, (2, 7, 3))
+        kt = 3
+        O, idx = o.reduced_pv(P, V, kt)
+        for h in range(2):
+            e = [sum(Fraction(int(P[h, q, t])) ** 2 for q in range(4)) for t in range(7)]
+            assert idx[h].tolist() == brute_force_topk(e, kt)
+            dense = exact_matmul(P[h], V[h])
+            rest = sum(np.outer(P[h][:, t], V[h][t]) for t in range(7) if t not in set(idx[h]))
+            assert np.allclose(dense - O[h], rest, rtol=1e-12, atol=1e-12)
+    # GQA: query head h reads the value rows of kv head h // (H / Hkv)
+    P = np.abs(_bf16(100, (4, 3, 6))) + 0.5
+    V = np.stack([np.full((6, 2), g + 1.0) for g in range(2)])
+    O, idx = o.reduced_pv(P, V, 4)
+    for h in range(4):
+        rows = P[h][:, idx[h]].sum(axis=1)
+        assert np.allclose(O[h], (h // 2 + 1.0) * rows[:, None], rtol=1e-14, atol=0)
+
+
 def check_margin(o):
     assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
     assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
@@ -416,4 +452,5 @@ def check_margin(o):
 
 
 ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
-              check_bounds, check_worked_example, check_qk, check_attention, check_margin)
+              check_bounds, check_worked_example, check_qk, check_attention, check_pv,
+              check_margin)

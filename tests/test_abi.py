@@ -262,6 +262,31 @@ def test_gemv_validation():
     assert f(*big) == UNSUPPORTED
 
 
+def test_pv_validation():
+    f = rmm.lib.rmm_reduced_pv
+    # P [1][4][64][96], V [1][2][96][128], kt = 48
+    need = rmm.rmm_workspace_size(rmm.RMM_OP_PV, 4, 64, 96, 48)
+    assert need == rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 4, 64, 96, 48) > 0
+    base = [P, P, 1, 1, 4, 2, 64, 96, 128, 96, 48, P, NULL, P, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 11):
+        assert call(i, NULL) == INVALID
+    assert call(2, 7) == INVALID            # dtype
+    assert call(5, 3) == INVALID            # H % Hkv != 0
+    assert call(4, 0) == INVALID            # H
+    assert call(10, 0) == INVALID           # kt < 1
+    assert call(10, 97) == INVALID          # kt > Lk
+    assert call(9, 95) == INVALID           # ldp < Lk
+    assert call(13, NULL) == WS_SMALL
+    assert call(14, need - 1) == WS_SMALL
+    assert call(13, ctypes.c_void_p(0x100004)) == INVALID     # workspace not 8-byte aligned
+
+
 def test_gemv_workspace_size():
     # many units and wide rows: one slice per workgroup column, no partials
     assert rmm.rmm_gemv_workspace_size(16, 1, 28672, 64) == 0

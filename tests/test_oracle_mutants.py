@@ -193,7 +193,26 @@ _attn_mask_as_zero = _attn_patch(_w_mask_as_zero, _gqa)
 _attn_gqa_modulo = _attn_patch(_w_softmax, lambda h, H, Hkv: h % Hkv)
 
 
+def _pv_patch(energies, value_head):
+    """reduced_pv with the token scores or the value head replaced."""
+    def f(P, V, kt):
+        P, V = np.asarray(P, dtype=np.float64), np.asarray(V, dtype=np.float64)
+        H, Hkv = P.shape[0], V.shape[0]
+        idx = np.stack([ro.topk_indices(energies(P[h]), kt) for h in range(H)])
+        O = np.stack([ro.reduced_matmul(P[h], V[value_head(h, H, Hkv)], idx[h]) for h in range(H)])
+        return O, idx
+    return f
+
+
+_pv_scores_rows = _pv_patch(lambda A: ro.column_energies(A.T), _gqa)
+_pv_scores_l1 = _pv_patch(lambda A: np.abs(A).sum(axis=0), _gqa)
+_pv_gqa_modulo = _pv_patch(ro.column_energies, lambda h, H, Hkv: h % Hkv)
+
+
 MUTANTS = {
+    "pv_scores_over_rows": ("reduced_pv", _pv_scores_rows),
+    "pv_scores_l1": ("reduced_pv", _pv_scores_l1),
+    "pv_gqa_modulo": ("reduced_pv", _pv_gqa_modulo),
     "attn_softmax_over_queries": ("reduced_attention", _attn_over_queries),
     "attn_unnormalised": ("reduced_attention", _attn_unnormalised),
     "attn_mask_as_zero_score": ("reduced_attention", _attn_mask_as_zero),
