@@ -99,6 +99,8 @@ def parse():
                    help="skip the separate timing of the fused attention block")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the separate timing of the decode step")
+    p.add_argument("--no-pv", action="store_true",
+                   help="skip the separate timing of the token-axis reduced value product")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="copy this many MiB device to device once before timing (a "
                         "counter-calibration probe for rocprofv3 runs; not timed)")
@@ -261,6 +263,72 @@ def time_attention(L, r, steps, warmup):
     flop = 2 * a.H * (a.L * (a.L + 1) // 2) * (kq + a.D)
     return {"r": r, "k": kq, "avg_call_us": ms * 1e3, "gflop": flop / 1e9,
             "retained_tflops": flop / (ms * 1e-3) / 1e12, "calls": steps}
+
+
+def attention_weights(L):
+    """P = softmax(S) per head, in place in L.S (bf16).  S holds the causal
+    scores of the sweep's last ratio (r = 1 in the default run: the full
+    QK^T/sqrt(D)), so P is the layer's attention weights (masked entries
+    -inf -> weight 0)."""
+    import torch
+    a = L.wk.attention
+    for h in range(a.H):
+        L.S[0, h] = torch.softmax(L.S[0, h].float(), dim=-1).to(torch.bfloat16)
+    torch.cuda.synchronize()
+
+
+def time_pv(L, r, steps, warmup, ws):
+    """The token-axis reduced value product on the layer's attention weights
+    P (L.S after attention_weights) and values V: per query head the TopK of
+    the column norms of P, then P[:, T] V[T, :] (rmm_reduced_pv: scoring with
+    the K-major copy of P, TopK, one gathered product per kv head), timed call
+    by call with HIP events; and torch's dense bf16 product P @ V (V repeated
+    over each kv head's query heads) for reference."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    a = L.wk.attention
+    kt = rmm.rmm_retained_count(r, a.L)
+    idx = torch.empty(a.H * kt, dtype=torch.int32, device=L.dev)
+
+    def call():
+        rmm.rmm_reduced_pv(L.S, L.V, kt, L.O, idx_out=idx, workspace=ws)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        call()
+        e1.record()
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = sum(x.elapsed_time(y) for x, y in evs) / steps
+    flop = 2 * a.H * a.L * kt * a.D
+    # one read of P (the least any evaluation of the token scores moves), the
+    # kept value rows, and O
+    nbytes = a.H * a.L * a.L * 2 + a.Hkv * kt * a.D * 2 + a.H * a.L * a.D * 2
+    return {"r": r, "kt": kt, "avg_call_us": ms * 1e3, "gflop": flop / 1e9,
+            "retained_tflops": flop / (ms * 1e-3) / 1e12, "bytes": nbytes,
+            "gbs": nbytes / (ms * 1e-3) / 1e9, "calls": steps}
+
+
+def time_dense_pv(L, steps, warmup):
+    import torch
+    a = L.wk.attention
+    Vr = L.V.repeat_interleave(a.H // a.Hkv, dim=1).contiguous()
+    out = torch.empty_like(L.O)
+    for _ in range(warmup):
+        torch.matmul(L.S, Vr, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        torch.matmul(L.S, Vr, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps
 
 
 def time_decode(L, r, steps, warmup, B=1):
@@ -500,13 +568,47 @@ def main():
                   "gate|up, down) TopK of the token's squared activations, reduced product "
                   "over the retained weight rows; us_per_step replays the step as one HIP "
                   "graph, us_per_step_eager launches it call by call",
-            "kernels": ["select_kernel (token keys)", "gemv_partial_kernel", "gemv_reduce_kernel"],
+            "kernels": ["select_token16_kernel", "gemv_partial_kernel", "gemv_reduce_kernel"],
             "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
                                    for k, v in rec.items()} for r, rec in dec.items()},
             "speedup_vs_r1": round(d_1["us_per_step"] / d_h["us_per_step"], 3) if d_1 else None,
             "roofline": {"bound": "hbm", "kernel": "gemv_partial_kernel (+ gemv_reduce_kernel)",
                          "achieved": round(d_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(d_ach / PEAK_HBM_GBS, 4), "traffic": None},
+        }
+    if not args.no_pv:
+        import torch
+        import paper_2608_13426_amd as rmm
+        a = wk.attention
+        attention_weights(L)
+        ws = torch.empty(rmm.rmm_workspace_size(rmm.RMM_OP_PV, a.H, a.L, a.L, a.L),
+                         dtype=torch.uint8, device=L.dev)
+        pv = {r: time_pv(L, r, args.steps, args.warmup, ws) for r in sorted(sweep)}
+        del ws
+        dense_us = time_dense_pv(L, args.steps, args.warmup)
+        for r, rec in pv.items():
+            print(f"# token-axis PV r={r}: {rec['avg_call_us']:.1f} us/call "
+                  f"({rec['gbs']:.0f} GB/s of one P read); dense P@V {dense_us:.1f} us",
+                  file=sys.stderr, flush=True)
+        p_us = sum(rec["avg_call_us"] * rec["calls"] for rec in pv.values())
+        p_b = sum(rec["bytes"] * rec["calls"] for rec in pv.values())
+        p_ach = p_b / (p_us * 1e-6) / 1e9
+        p_h, p_1 = pv.get(HEADLINE_R), pv.get(1.0)
+        out["pv_token"] = {
+            "op": "token-axis reduced value product per query head: TopK of the column norms "
+                  "of the attention weights P (softmax of the layer's causal scores), then "
+                  "P[:, T] V[T, :]; 32 q / 8 kv heads, seq 8192, d=128",
+            "kernels": ["score_tile_kernel", "score_finalize_kernel", "select_kernel",
+                        "gemm_kmajor_tr_kernel"],
+            "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
+                                   for k, v in rec.items()} for r, rec in pv.items()},
+            "speedup_vs_r1": round(p_1["avg_call_us"] / p_h["avg_call_us"], 3) if p_1 else None,
+            "dense_torch_us": round(dense_us, 1),
+            "speedup_vs_dense_torch": round(dense_us / p_h["avg_call_us"], 3) if p_h else None,
+            "roofline": {"bound": "hbm", "kernel": "rmm_reduced_pv (all kernels of a call)",
+                         "achieved": round(p_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(p_ach / PEAK_HBM_GBS, 4), "traffic": None,
+                         "bytes_basis": "one read of P + kept V rows + O per call"},
         }
     if not args.no_cpu_baseline:
         print(f"# CPU oracle on {args.cpu_tokens} tokens ...", file=sys.stderr, flush=True)
