@@ -61,12 +61,13 @@ GEMM_KERNEL = "gemm_kmajor_tr_kernel"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
 # HBM bytes per launch from two rocprofv3 --pmc runs of the default ratio mix
 # (FETCH_SIZE x2.0, WRITE_SIZE x1.0: the factors a 512 MiB device copy reads),
-# averaged over the kernel's dispatches.  Each figure is valid only for the
+# averaged over the kernel's dispatches of the layer step (the value product's
+# per-kv-head launches, smaller grids, excluded).  Each figure is valid only for the
 # source whose SHA-256 is recorded and for the same launch mix.
 GEMM_TRAFFIC = {"source": GEMM_SOURCE,
-                "sha256": "11e911b1d8786feb4504a3e740ba2f9821fec13ed3ab6f6eb89d24b28300329d",
+                "sha256": "383f6ce3e5976e9a42786d740c7006cc2d8c619fb1cb354b93eb8020730394a7",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
-                "bytes": round((399647.63 * 2.0 + 172032.00) * 1024)}
+                "bytes": round((399437.54 * 2.0 + 172170.95) * 1024)}
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"source": os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "attn.hip"),
