@@ -20,6 +20,11 @@ K timed steps bracketed by device synchronisation.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--ratios 0.25,0.5,0.75,1.0]
 
+The same step is also timed under per-component retention ratios
+("component_ratios": attention-side products, and optionally the MLP down
+projection, at 0.7 with the sensitive gate/up group dense), the policies the
+paper's component analysis points to, with the speedup over the r = 1 run.
+
 The fused attention block (softmax of the reduced scores times V, S never
 written) is timed on its own after the sweep, at the same ratios, and
 reported under "fused_attention" with its speedup over r = 1 and its own
@@ -100,6 +105,8 @@ def parse():
                    help="skip the separate timing of the fused attention block")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the separate timing of the decode step")
+    p.add_argument("--no-policies", action="store_true",
+                   help="skip the steps with per-component retention ratios")
     p.add_argument("--no-pv", action="store_true",
                    help="skip the separate timing of the token-axis reduced value product")
     p.add_argument("--copy-probe-mib", type=int, default=0,
@@ -161,24 +168,42 @@ class Layer:
         self.qidx = None
 
 
+# Component policies (per-component retention ratios; App. C, compute-normalized
+# component analysis): at RR = 0.7 the attention-side products and the MLP down
+# projection lose the least accuracy, the up and gate projections the most, so
+# the sensitive group stays dense (r = 1: the same pipeline with k = K).
+# Components are the input groups of the step plus "qk" for the per-head QK^T.
+POLICIES = {
+    "attention_side_0.7": {"attn_in": 0.7, "o_in": 0.7, "qk": 0.7, "mlp_in": 1.0, "down_in": 1.0},
+    "attention_side_and_down_0.7": {"attn_in": 0.7, "o_in": 0.7, "qk": 0.7, "mlp_in": 1.0,
+                                    "down_in": 0.7},
+}
+
+
+def ratio_of(r, component):
+    """The ratio a component runs at: r itself, or its entry in a policy."""
+    return r[component] if isinstance(r, dict) else r
+
+
 def flops(wk, r):
-    """Retained FLOPs of one step at ratio r."""
+    """Retained FLOPs of one step at ratio r (a float, or a policy dict)."""
     import paper_2608_13426_amd as rmm
-    proj = sum(2 * wk.M * p.N * rmm.rmm_retained_count(r, p.K) for p in wk.projections)
+    proj = sum(2 * wk.M * p.N * rmm.rmm_retained_count(ratio_of(r, p.input_name), p.K)
+               for p in wk.projections)
     a = wk.attention
     pairs = a.L * (a.L + 1) // 2
-    qk = 2 * a.H * pairs * rmm.rmm_retained_count(r, a.D)
+    qk = 2 * a.H * pairs * rmm.rmm_retained_count(ratio_of(r, "qk"), a.D)
     return proj, qk
 
 
 def run_step(L, r, gemm_events=None):
-    """Enqueue one full step on the current stream."""
+    """Enqueue one full step on the current stream (r: a ratio or a policy)."""
     import torch
     import paper_2608_13426_amd as rmm
     wk = L.wk
     for name, projs in L.groups.items():
         K = wk.inputs[name][0]
-        k = rmm.rmm_retained_count(r, K)
+        k = rmm.rmm_retained_count(ratio_of(r, name), K)
         X = L.X[name]
         e = L.energy[:K]
         rmm.rmm_score_kmajor(X, e, L.Xt[name], L.ws)
@@ -193,7 +218,7 @@ def run_step(L, r, gemm_events=None):
             ev1.record()
             gemm_events.append((ev0, ev1, 2 * wk.M * L.Ycat[name].shape[1] * k))
     a = wk.attention
-    kq = rmm.rmm_retained_count(r, a.D)
+    kq = rmm.rmm_retained_count(ratio_of(r, "qk"), a.D)
     e = L.energy[:a.H * a.D]
     rmm.rmm_score(L.Q.reshape(a.H, a.L, a.D), e, L.ws)
     if L.qidx is None or L.qidx.numel() != a.H * kq:
@@ -348,7 +373,7 @@ def time_decode(L, r, steps, warmup, B=1):
     parts = []
     for name in L.groups:
         K = wk.inputs[name][0]
-        k = rmm.rmm_retained_count(r, K)
+        k = rmm.rmm_retained_count(ratio_of(r, name), K)
         X = L.X[name][:B].reshape(B, 1, K)
         W = L.Wcat[name]
         N = W.shape[1]
@@ -529,6 +554,20 @@ def main():
                      "avg_launch_gflop": round(g_gflop / g_n, 3),
                      "ratios": sorted(sweep)},
     }
+    if not args.no_policies:
+        pol = {}
+        for name, policy in POLICIES.items():
+            rec = time_ratio(L, policy, args.steps, args.warmup)
+            rec["speedup_vs_r1"] = (base["ms_per_step"] / rec["ms_per_step"]) if base else None
+            pol[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in rec.items()}
+            print(f"# policy {name}: {rec['ms_per_step']:.3f} ms/step, {rec['tflops']:.1f} TFLOP/s",
+                  file=sys.stderr, flush=True)
+        out["component_ratios"] = {
+            "op": "the same step with a retention ratio per component (attn_in: q|k|v, o_in: o, "
+                  "mlp_in: gate|up, down_in: down, qk: per-head QK^T); speedup over the "
+                  "same pipeline at r = 1",
+            "policies": pol,
+        }
     if not args.no_fused_attention:
         att = {r: time_attention(L, r, args.steps, args.warmup) for r in sorted(sweep)}
         for r, rec in att.items():
