@@ -28,7 +28,10 @@ paper's component analysis points to, with the speedup over the r = 1 run.
 The fused attention block (softmax of the reduced scores times V, S never
 written) is timed on its own after the sweep, at the same ratios, and
 reported under "fused_attention" with its speedup over r = 1 and its own
-MFMA roofline; it is not part of the step.
+MFMA roofline; it is not part of the step.  "attention_o_chain" times that
+block feeding the reduced output projection, with the block writing the
+projection's K-major input and column energies (no separate scoring pass)
+against the unfused chain.
 
 A decode step of the same layer (batch 1, one token: energies, TopK and the
 reduced product over the retained weight rows per projection group) is timed
@@ -168,7 +171,7 @@ class Layer:
         self.qidx = None
 
 
-# Component policies (per-component retention ratios; App. C, compute-normalized
+# Component policies (per-component retention ratios; App. B.4, compute-normalized
 # component analysis): at RR = 0.7 the attention-side products and the MLP down
 # projection lose the least accuracy, the up and gate projections the most, so
 # the sensitive group stays dense (r = 1: the same pipeline with k = K).
@@ -289,6 +292,74 @@ def time_attention(L, r, steps, warmup):
     flop = 2 * a.H * (a.L * (a.L + 1) // 2) * (kq + a.D)
     return {"r": r, "k": kq, "avg_call_us": ms * 1e3, "gflop": flop / 1e9,
             "retained_tflops": flop / (ms * 1e-3) / 1e12, "calls": steps}
+
+
+def time_attention_chain(L, r, steps, warmup):
+    """The attention block feeding the reduced output projection, both ways,
+    at ratio r for the heads' and the projection's selections (the per-head
+    selection made once outside the timed region):
+      fused   : rmm_reduced_attention_kmajor (writes the projection's K-major
+                input and its column energies) -> TopK -> K-major GEMM;
+      unfused : rmm_reduced_attention (O per head) -> O laid out as the
+                projection's token-major input (a torch copy) ->
+                rmm_score_kmajor -> TopK -> K-major GEMM.
+    Every call is bracketed by HIP events on the launch stream; the layout
+    copy is also timed alone, so the unfused chain can be read without it."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    a, M = L.wk.attention, L.M
+    HD = a.H * a.D
+    kq = rmm.rmm_retained_count(r, a.D)
+    e = L.energy[:HD]
+    rmm.rmm_score(L.Q.reshape(a.H, a.L, a.D), e, L.ws)
+    idx = torch.empty(a.H * kq, dtype=torch.int32, device=L.dev)
+    rmm.rmm_select(e, kq, idx)
+    idx = idx.view(1, a.H, kq)
+    Wo, Yo = L.W["o"], L.Y["o"]
+    ko = rmm.rmm_retained_count(r, HD)
+    sel = torch.empty(ko, dtype=torch.int32, device=L.dev)
+    ws_k = torch.empty(rmm.rmm_attention_kmajor_workspace_size(1, a.H, a.L, a.L, a.D, kq),
+                       dtype=torch.uint8, device=L.dev)
+    ws_a = torch.empty(rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, a.H, a.L, a.D, kq),
+                       dtype=torch.uint8, device=L.dev)
+    Ot = torch.empty((HD, a.L), dtype=torch.bfloat16, device=L.dev)
+    Xo = torch.empty((a.L, HD), dtype=torch.bfloat16, device=L.dev)
+    Xt = L.Xt["o_in"]
+    eo = torch.empty(HD, dtype=torch.float64, device=L.dev)
+
+    def fused():
+        rmm.rmm_reduced_attention_kmajor(L.Q, L.Kc, L.V, idx, Ot, eo, causal=True, workspace=ws_k)
+        rmm.rmm_select(eo, ko, sel)
+        rmm.rmm_reduced_gemm_kmajor(Ot, Wo, sel.view(1, ko), Yo)
+
+    def layout():
+        Xo.view(a.L, a.H, a.D).copy_(L.O[0].permute(1, 0, 2))
+
+    def unfused():
+        rmm.rmm_reduced_attention(L.Q, L.Kc, L.V, idx, L.O, causal=True, workspace=ws_a)
+        layout()
+        rmm.rmm_score_kmajor(Xo, eo, Xt, L.ws)
+        rmm.rmm_select(eo, ko, sel)
+        rmm.rmm_reduced_gemm_kmajor(Xt, Wo, sel.view(1, ko), Yo)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = []
+        for _ in range(steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        return sum(x.elapsed_time(y) for x, y in evs) / steps * 1e3
+
+    us_f, us_u, us_l = timed(fused), timed(unfused), timed(layout)
+    return {"r": r, "k_heads": kq, "k_o": ko, "fused_us": us_f, "unfused_us": us_u,
+            "layout_copy_us": us_l, "unfused_without_copy_us": us_u - us_l,
+            "speedup": us_u / us_f, "speedup_without_copy": (us_u - us_l) / us_f, "calls": steps}
 
 
 def attention_weights(L):
@@ -591,6 +662,22 @@ def main():
                          "traffic": recorded_traffic(
                              ATTN_TRAFFIC, f"{wk.name} r={','.join(str(r) for r in sorted(att))}"),
                          "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, both kernels)"},
+        }
+    if not args.no_fused_attention:
+        ch = {r: time_attention_chain(L, r, args.steps, args.warmup) for r in sorted(sweep)}
+        for r, rec in ch.items():
+            print(f"# attention -> o-projection r={r}: fused {rec['fused_us']:.1f} us, unfused "
+                  f"{rec['unfused_us']:.1f} us ({rec['layout_copy_us']:.1f} us of it the layout "
+                  f"copy)", file=sys.stderr, flush=True)
+        out["attention_o_chain"] = {
+            "op": "reduced attention block feeding the reduced output projection (o, 4096 x "
+                  "4096): fused = the block writes the projection's K-major input and its "
+                  "column energies (no scoring pass), unfused = block, token-major layout "
+                  "copy, scoring pass with K-major copy; both then TopK and K-major GEMM",
+            "kernels": ["attn_compact_k_kernel", "attn_fwd_kernel", "score_finalize_kernel",
+                        "select_kernel", "gemm_kmajor_tr_kernel"],
+            "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
+                                   for k, v in rec.items()} for r, rec in ch.items()},
         }
     if not args.no_decode:
         dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}

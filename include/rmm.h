@@ -282,6 +282,42 @@ rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
                                    hipStream_t stream);
 
 /*
+ * Reduced attention block feeding a reduced projection   (Sec. 3.3: the
+ * block's output is the input of the attention output projection, whose
+ * retained set Sec. 3.2 scores from that input's columns; the Limitations
+ * section names the memory movement of separate scoring as a cost to remove).
+ *
+ * The same block as rmm_reduced_attention (same arguments, same output
+ * values bit for bit), written as the output projection's K-major input
+ * instead of O, together with that input's column energies, so that the
+ * projection needs no separate scoring pass:
+ *   Ot[b][h*D + j][t] = O[b][h][t][j]        (heads concatenated along the
+ *                                             projection's contraction axis)
+ *   energy[b][h*D + j] = sum over t < Lq of Ot[b][h*D + j][t]^2
+ * (float64 sums of the exact squares of the bf16 outputs, in a fixed order).
+ * Feed them to rmm_select (B = batch, K = H*D) and rmm_reduced_gemm_kmajor
+ * (Xt = Ot, ldxt = ldot, M = Lq).
+ *
+ * Ot     : bf16 [batch][H*D][ldot], ldot >= Lq, 16-byte aligned; columns
+ *          Lq..ldot-1 are not written.
+ * energy : float64 [batch][H*D], 8-byte aligned.
+ * workspace : rmm_attention_kmajor_workspace_size(batch, H, Lq, Lk, D, k)
+ *          bytes, 256-byte aligned (compacted key rows and per-query-tile
+ *          partial energies; overwritten by every call).
+ * Errors : as rmm_reduced_attention, plus INVALID_ARGUMENT for a null energy
+ *          or ldot < Lq; UNSUPPORTED when Lq or ldot is not a multiple of 8
+ *          or Ot is not 16-byte aligned.
+ */
+size_t rmm_attention_kmajor_workspace_size(int64_t batch, int64_t H, int64_t Lq, int64_t Lk,
+                                            int64_t D, int64_t k);
+rmm_status_t rmm_reduced_attention_kmajor(const void *Q, const void *Kc, const void *V,
+                                          const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
+                                          int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
+                                          int64_t D, int64_t k, float scale, int causal, void *Ot,
+                                          int64_t ldot, double *energy, void *workspace,
+                                          size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Fused RMM projection   (Sec. 3.2 + Sec. 3.3 "MLP and linear projections").
  *
  * k = rmm_retained_count(r, K); then score -> rmm_select -> gathered GEMM

@@ -57,6 +57,11 @@ _SIGS = {
                                              _p, ctypes.c_size_t, _p]),
     "rmm_reduced_pv": (ctypes.c_int, [_p, _p, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64,
                                       _i64, _i64, _p, _p, _p, ctypes.c_size_t, _p]),
+    "rmm_attention_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64, _i64, _i64]),
+    "rmm_reduced_attention_kmajor": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int, _i64, _i64, _i64,
+                                                    _i64, _i64, _i64, _i64, ctypes.c_float,
+                                                    ctypes.c_int, _p, _i64, _p, _p, ctypes.c_size_t,
+                                                    _p]),
 }
 EXPORTED_SYMBOLS = tuple(_SIGS)
 
@@ -359,6 +364,63 @@ def rmm_reduced_attention(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor, id
         Lq, Lk, D, k, float(scale), 1 if causal else 0, O.data_ptr(), workspace.data_ptr(),
         ws_bytes, _stream(d, stream)))
     return O
+
+
+def rmm_attention_kmajor_workspace_size(batch: int, H: int, Lq: int, Lk: int, D: int,
+                                        k: int) -> int:
+    return int(lib.rmm_attention_kmajor_workspace_size(batch, H, Lq, Lk, D, k))
+
+
+def rmm_reduced_attention_kmajor(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor,
+                                 idx: torch.Tensor, Ot: torch.Tensor, energy: torch.Tensor,
+                                 causal: bool = True, scale: float | None = None,
+                                 workspace: torch.Tensor | None = None,
+                                 stream=None) -> torch.Tensor:
+    """The reduced attention block of rmm_reduced_attention, written as the
+    output projection's K-major input Ot [batch, H*D, ldot] (a view whose
+    rows have stride ldot >= Lq) with that input's column energies
+    energy float64 [batch, H*D].  `workspace` (uint8,
+    rmm_attention_kmajor_workspace_size(...) bytes, 256-byte aligned) is
+    allocated here when not given."""
+    if Q.dim() == 3:
+        Q, Kc, V = Q.unsqueeze(0), Kc.unsqueeze(0), V.unsqueeze(0)
+    if Ot.dim() == 2:
+        Ot = Ot.unsqueeze(0)
+    if energy.dim() == 1:
+        energy = energy.unsqueeze(0)
+    batch, H, Lq, D = Q.shape
+    bk, Hkv, Lk, Dk = Kc.shape
+    d = _dev(Q, Kc, V, idx, Ot, energy)
+    if bk != batch or Dk != D:
+        raise ValueError("Kc must be [batch, Hkv, Lk, D]")
+    if tuple(V.shape) != (batch, Hkv, Lk, D):
+        raise ValueError("V must be [batch, Hkv, Lk, D]")
+    if Ot.shape[0] != batch or Ot.shape[1] != H * D or Ot.shape[2] < Lq:
+        raise ValueError("Ot must be [batch, H*D, >= Lq]")
+    if Ot.stride(2) != 1 or Ot.stride(0) != Ot.shape[1] * Ot.stride(1):
+        raise ValueError("Ot rows must be contiguous, with one row stride ldot")
+    if tuple(energy.shape) != (batch, H * D) or not energy.is_contiguous() or \
+            energy.dtype != torch.float64:
+        raise ValueError("energy must be contiguous float64 [batch, H*D]")
+    for t, n in ((Q, "Q"), (Kc, "Kc"), (V, "V"), (idx, "idx")):
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    if not (Q.dtype == Kc.dtype == V.dtype == Ot.dtype):
+        raise TypeError("Q, Kc, V and Ot must share one dtype")
+    if idx.dtype != torch.int32 or idx.numel() % (batch * H):
+        raise ValueError("idx must be int32 [batch, H, k]")
+    k = idx.numel() // (batch * H)
+    if scale is None:
+        scale = D ** -0.5
+    if workspace is None:
+        workspace = torch.empty(max(rmm_attention_kmajor_workspace_size(batch, H, Lq, Lk, D, k), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_reduced_attention_kmajor", lib.rmm_reduced_attention_kmajor(
+        Q.data_ptr(), Kc.data_ptr(), V.data_ptr(), idx.data_ptr(), _dtype_code(Q), batch, H, Hkv,
+        Lq, Lk, D, k, float(scale), 1 if causal else 0, Ot.data_ptr(), Ot.stride(1),
+        energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    return Ot
 
 
 def rmm_reduced_pv(P: torch.Tensor, V: torch.Tensor, kt: int, O: torch.Tensor,

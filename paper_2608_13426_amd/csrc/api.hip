@@ -247,6 +247,41 @@ rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
         static_cast<uint16_t *>(O), workspace, stream));
 }
 
+size_t rmm_attention_kmajor_workspace_size(int64_t batch, int64_t H, int64_t Lq, int64_t Lk,
+                                            int64_t D, int64_t k) {
+    if (batch < 1 || H < 1 || Lq < 1 || Lk < 1 || D < 1 || k < 1 || k > D) return 0;
+    return align256(rmm::attn_workspace_bytes(batch * H, Lk, k)) +
+           align256(static_cast<size_t>(batch * rmm::attn_query_tiles(Lq) * H * D) * sizeof(double));
+}
+
+rmm_status_t rmm_reduced_attention_kmajor(const void *Q, const void *Kc, const void *V,
+                                          const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
+                                          int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
+                                          int64_t D, int64_t k, float scale, int causal, void *Ot,
+                                          int64_t ldot, double *energy, void *workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+    if (!Q || !Kc || !V || !idx || !Ot || !energy) return RMM_ERR_INVALID_ARGUMENT;
+    if (!valid_dtype(dtype)) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (H % Hkv != 0) return RMM_ERR_INVALID_ARGUMENT;
+    if (k < 1 || k > D) return RMM_ERR_INVALID_ARGUMENT;
+    if (Lq > kInt32Max || Lk > kInt32Max || ldot < Lq) return RMM_ERR_INVALID_ARGUMENT;
+    if (dtype != RMM_BF16 || D != 128) return RMM_ERR_UNSUPPORTED;
+    if (!aligned16(Q) || !aligned16(Kc) || !aligned16(V) || !aligned16(Ot)) return RMM_ERR_UNSUPPORTED;
+    if (Lq % 8 || ldot % 8 || reinterpret_cast<uintptr_t>(energy) % 8) return RMM_ERR_UNSUPPORTED;
+    if (batch * H > kGridYZMax || (Lq + 255) / 256 * batch * H > kInt32Max) return RMM_ERR_UNSUPPORTED;
+    const size_t need = rmm_attention_kmajor_workspace_size(batch, H, Lq, Lk, D, k);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
+    char *ws = static_cast<char *>(workspace);
+    uint16_t *Ki = reinterpret_cast<uint16_t *>(ws);
+    double *partials = reinterpret_cast<double *>(ws + align256(rmm::attn_workspace_bytes(batch * H, Lk, k)));
+    return from_hip(rmm::launch_attn_kmajor_bf16(
+        static_cast<const uint16_t *>(Q), static_cast<const uint16_t *>(Kc),
+        static_cast<const uint16_t *>(V), idx, batch, H, Hkv, Lq, Lk, k, scale, causal != 0,
+        static_cast<uint16_t *>(Ot), ldot, energy, Ki, partials, stream));
+}
+
 rmm_status_t rmm_linear(const void *X, const void *W, double r, rmm_dtype_t dtype, int64_t B,
                         int64_t M, int64_t N, int64_t K, int64_t ldx, int64_t ldw, void *Y,
                         int64_t ldy, int32_t *idx_out, void *workspace, size_t workspace_bytes,

@@ -85,6 +85,21 @@ __device__ __forceinline__ float pair_sum(float x) {
     return x;
 #endif
 }
+// x of the lane whose index within the quad is given by the quad_perm
+// control CTRL (0xB1: lane ^ 1, 0x4E: lane ^ 2), for a float64 value
+template <int CTRL>
+__device__ __forceinline__ double quad_f64(double x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+    const uint32_t lo = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, 0xF, 0xF, false));
+    const uint32_t hi = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, 0xF, 0xF, false));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+#else
+    return x;
+#endif
+}
 }  // namespace attk
 
 // Ki[bh][t][j] = K[b][g][t][I_h[j]] for j < k, 0 for k <= j < 16*KS.
@@ -129,11 +144,18 @@ __global__ __launch_bounds__(attk::CNT) void attn_compact_k_kernel(
     }
 }
 
-template <int KS>
+// KM selects the output form.  false: O[b][h][q][d].  true: the block output
+// as the K-major input of the projection that follows attention (heads
+// concatenated along its contraction axis), Ot[b][h*D + d][q] with row stride
+// ldot, plus part[b][qt][h*D + d] = sum over the block's queries q < Lq of
+// bf16(O[q][d])^2 in float64 (one query tile's share of that input's column
+// energies; a fixed-order sum over the tiles completes them).
+template <int KS, bool KM>
 __global__ __launch_bounds__(attk::NT, 1) void attn_fwd_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Ki,
     const uint16_t *__restrict__ V, const int32_t *__restrict__ idx, uint16_t *__restrict__ O,
-    int H, int Hkv, int Lq, int Lk, int k, float c, int neg_q, int causal) {
+    int H, int Hkv, int Lq, int Lk, int k, float c, int neg_q, int causal, int64_t ldot,
+    double *__restrict__ part) {
     using namespace attk;
     constexpr int KP = 16 * KS;                 // Ki row width
     constexpr int KRB = KP * 2;                 // Ki row bytes
@@ -425,13 +447,72 @@ __global__ __launch_bounds__(attk::NT, 1) void attn_fwd_kernel(
     }
     wait_vmcnt_le<0>();                          // the trailing out-of-range loads
 
+    const float l = pair_sum(l_run);
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const int ql = wave * 32 + lr;               // rows past Lq fall outside the buffer
+    if constexpr (KM) {
+        // ---- O^T of the block through the idle ring: dim d in slot d / 64, row
+        //      d % 64 (OROW bytes: 256 queries + a 16-byte pad, so the two lane
+        //      halves, 4 dims apart, write distinct banks), query column ql
+        constexpr int OROW = BQ * 2 + 16;
+        static_assert(64 * OROW <= SB, "staged O^T rows");
+        __syncthreads();                         // every wave's last reads and loads are done
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+            char *so = (db < 2 ? slot0 : slot1) + (32 * (db & 1) + 4 * lh) * OROW + 2 * ql;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const __bf16 x = static_cast<__bf16>(o_acc[db][v] * inv);
+                *reinterpret_cast<__bf16 *>(so + (8 * (v >> 2) + (v & 3)) * OROW) = x;
+            }
+        }
+        __syncthreads();
+        const int nvq = min(BQ, Lq - q0);           // queries of the block (Lq % 8 == 0)
+        // stores: each half-wave writes one dim row per pass, 32 lanes x 16
+        // bytes = the block's 256 queries
+        {
+            const int cq = lane & 31, rr = tid >> 5;     // rr = 0..15
+            uint16_t *Otb = O + (static_cast<int64_t>(b) * H + h) * D * ldot + q0;
+#pragma unroll
+            for (int i = 0; i < D / 16; ++i) {
+                const int dd = rr + 16 * i;
+                const uint4 w = *reinterpret_cast<const uint4 *>((i < 4 ? slot0 : slot1) + (dd & 63) * OROW + 16 * cq);
+                if (8 * cq < nvq) *reinterpret_cast<uint4 *>(Otb + dd * ldot + 8 * cq) = w;
+            }
+        }
+        // energies: thread t sums dim row t/4 over its quarter of the queries
+        // (64, as eight 16-byte pieces), then the quad adds its four quarters
+        // (lane ^ 1, then lane ^ 2: every lane of the quad ends with the same sum)
+        {
+            const int dd = tid >> 2, qa = tid & 3;
+            const char *row = (dd < 64 ? slot0 : slot1) + (dd & 63) * OROW;
+            double e = 0.0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int ch = 8 * qa + j;
+                if (8 * ch < nvq) {
+                    const uint4 w = *reinterpret_cast<const uint4 *>(row + 16 * ch);
+                    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const double lo = static_cast<double>(__uint_as_float(u[q] << 16));
+                        const double hi = static_cast<double>(__uint_as_float(u[q] & 0xffff0000u));
+                        e = fma(lo, lo, e);
+                        e = fma(hi, hi, e);
+                    }
+                }
+            }
+            e += quad_f64<0xB1>(e);
+            e += quad_f64<0x4E>(e);
+            if (qa == 0)
+                part[(static_cast<int64_t>(b) * nq + qt) * H * D + static_cast<int64_t>(h) * D + dd] = e;
+        }
+        return;
+    }
     // ---- O[q][d]: the lane holds d = 32*db + 8*gq + 4*lh + {0..3} of query qw0 + lr
     const __amdgpu_buffer_rsrc_t orr = __builtin_amdgcn_make_buffer_rsrc(
         O + (static_cast<int64_t>(bh) * Lq + q0) * D, 0,
         static_cast<uint32_t>(min(BQ, Lq - q0) * D * 2), 0x00020000);
-    const float l = pair_sum(l_run);
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    const int ql = wave * 32 + lr;               // rows past Lq fall outside the buffer
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -443,10 +524,11 @@ __global__ __launch_bounds__(attk::NT, 1) void attn_fwd_kernel(
         }
 }
 
-template <int KS>
+template <int KS, bool KM>
 hipError_t launch_ks(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V, const int32_t *idx,
                      int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t k,
-                     float scale, bool causal, uint16_t *O, uint16_t *Ki, hipStream_t stream) {
+                     float scale, bool causal, uint16_t *O, uint16_t *Ki, int64_t ldot,
+                     double *part, hipStream_t stream) {
     using namespace attk;
     const unsigned BH = static_cast<unsigned>(batch * H);
     hipLaunchKernelGGL(attn_compact_k_kernel<KS>, dim3(static_cast<unsigned>((Lk + BN - 1) / BN), BH),
@@ -460,11 +542,24 @@ hipError_t launch_ks(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V, c
     // would) while masked -inf scores still give weight 0
     float c = (scale < 0.f ? -scale : scale) * kLog2e;
     if (c < 1.17549435e-38f) c = 1.17549435e-38f;
-    hipLaunchKernelGGL(attn_fwd_kernel<KS>, dim3(nq * BH), dim3(NT), 0, stream,
+    hipLaunchKernelGGL((attn_fwd_kernel<KS, KM>), dim3(nq * BH), dim3(NT), 0, stream,
                        Q, Ki, V, idx, O, static_cast<int>(H), static_cast<int>(Hkv),
                        static_cast<int>(Lq), static_cast<int>(Lk), static_cast<int>(k), c,
-                       scale < 0.f ? 1 : 0, causal ? 1 : 0);
+                       scale < 0.f ? 1 : 0, causal ? 1 : 0, ldot, part);
     return hipGetLastError();
+}
+
+template <bool KM>
+hipError_t launch_attn(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V,
+                       const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
+                       int64_t Lk, int64_t k, float scale, bool causal, uint16_t *O, uint16_t *Ki,
+                       int64_t ldot, double *part, hipStream_t stream) {
+    switch (attn_k_steps(k)) {
+    case 2: return launch_ks<2, KM>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, ldot, part, stream);
+    case 4: return launch_ks<4, KM>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, ldot, part, stream);
+    case 6: return launch_ks<6, KM>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, ldot, part, stream);
+    default: return launch_ks<8, KM>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, ldot, part, stream);
+    }
 }
 
 }  // namespace
@@ -476,17 +571,26 @@ size_t attn_workspace_bytes(int64_t batch_heads, int64_t Lk, int64_t k) {
            static_cast<size_t>(16 * attn_k_steps(k)) * 2;
 }
 
+int64_t attn_query_tiles(int64_t Lq) { return (Lq + attk::BQ - 1) / attk::BQ; }
+
 hipError_t launch_attn_bf16(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V,
                             const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv,
                             int64_t Lq, int64_t Lk, int64_t k, float scale, bool causal,
                             uint16_t *O, void *workspace, hipStream_t stream) {
-    uint16_t *Ki = static_cast<uint16_t *>(workspace);
-    switch (attn_k_steps(k)) {
-    case 2: return launch_ks<2>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
-    case 4: return launch_ks<4>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
-    case 6: return launch_ks<6>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
-    default: return launch_ks<8>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O, Ki, stream);
-    }
+    return launch_attn<false>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal, O,
+                              static_cast<uint16_t *>(workspace), 0, nullptr, stream);
+}
+
+hipError_t launch_attn_kmajor_bf16(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V,
+                                   const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv,
+                                   int64_t Lq, int64_t Lk, int64_t k, float scale, bool causal,
+                                   uint16_t *Ot, int64_t ldot, double *energy, uint16_t *Ki,
+                                   double *partials, hipStream_t stream) {
+    const hipError_t e = launch_attn<true>(Q, Kc, V, idx, batch, H, Hkv, Lq, Lk, k, scale, causal,
+                                           Ot, Ki, ldot, partials, stream);
+    if (e != hipSuccess) return e;
+    // energies: the query tiles' partial sums, added in tile order
+    return launch_score_finalize(partials, batch, attn_query_tiles(Lq), H * attk::D, energy, stream);
 }
 
 }  // namespace rmm

@@ -16,6 +16,9 @@ constexpr int kScoreMinRows = 64;      // fewest rows per split
 constexpr int kScoreTargetBlocks = 2048;
 
 int64_t score_rows_per_split(int64_t B, int64_t M, int64_t K);
+// energy[b][j] = sum over s = 0..S-1, in order, of partials[b][s][j]
+hipError_t launch_score_finalize(const double *partials, int64_t B, int64_t S, int64_t K,
+                                 double *energy, hipStream_t stream);
 int64_t score_splits(int64_t B, int64_t M, int64_t K);
 size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K);
 
@@ -65,6 +68,16 @@ hipError_t launch_attn_bf16(const uint16_t *Q, const uint16_t *Kc, const uint16_
                             const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv,
                             int64_t Lq, int64_t Lk, int64_t k, float scale, bool causal,
                             uint16_t *O, void *workspace, hipStream_t stream);
+// the same block writing its output as the K-major input of the following
+// projection, Ot[b][h*D + j][ldot] (Lq % 8 == 0, ldot % 8 == 0, Ot 16-byte
+// aligned), and that input's column energies energy[b][h*D + j]; partials
+// holds batch * attn_query_tiles(Lq) * H * D doubles
+int64_t attn_query_tiles(int64_t Lq);
+hipError_t launch_attn_kmajor_bf16(const uint16_t *Q, const uint16_t *Kc, const uint16_t *V,
+                                   const int32_t *idx, int64_t batch, int64_t H, int64_t Hkv,
+                                   int64_t Lq, int64_t Lk, int64_t k, float scale, bool causal,
+                                   uint16_t *Ot, int64_t ldot, double *energy, uint16_t *Ki,
+                                   double *partials, hipStream_t stream);
 hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *idx,
                           int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
                           int64_t Lk, int64_t D, int64_t k, float scale, bool causal,

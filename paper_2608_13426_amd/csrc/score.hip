@@ -312,6 +312,14 @@ size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K) {
     return s > 1 ? static_cast<size_t>(B * s * K) * sizeof(double) : 0;
 }
 
+hipError_t launch_score_finalize(const double *partials, int64_t B, int64_t S, int64_t K,
+                                 double *energy, hipStream_t stream) {
+    const int64_t n = B * K;
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(static_cast<unsigned>((n + 63) / 64)), dim3(64), 0,
+                       stream, partials, B, S, K, energy);
+    return hipGetLastError();
+}
+
 hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t K,
                         int64_t ldx, double *energy, double *partials, uint16_t *Xt,
                         int64_t ldxt, hipStream_t stream) {
@@ -347,10 +355,7 @@ hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t 
                                                         split_stride, nullptr, 0, stream);
     }
     if (err != hipSuccess || S == 1) return err;
-    const int64_t n = B * K;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(static_cast<unsigned>((n + 63) / 64)), dim3(64), 0,
-                       stream, partials, B, S, K, energy);
-    return hipGetLastError();
+    return launch_score_finalize(partials, B, S, K, energy, stream);
 }
 
 }  // namespace rmm

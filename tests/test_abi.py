@@ -208,6 +208,52 @@ def test_attention_workspace_size():
     assert rmm.rmm_workspace_size(rmm.RMM_OP_ATTENTION, 1, 64, 128, 129) == 0
 
 
+def test_attention_kmajor_validation():
+    f = rmm.lib.rmm_reduced_attention_kmajor
+    A = ctypes.c_void_p(0x100000)
+    need = rmm.rmm_attention_kmajor_workspace_size(1, 8, 64, 64, 128, 64)
+    # Q Kc V idx dtype batch H Hkv Lq Lk D k scale causal Ot ldot energy ws ws_bytes stream
+    base = [A, A, A, P, 1, 1, 8, 2, 64, 64, 128, 64, ctypes.c_float(0.088), 1, A, 64, A, A, need,
+            NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 3, 14, 16):
+        assert call(i, NULL) == INVALID
+    assert call(4, 9) == INVALID            # dtype
+    assert call(5, 0) == INVALID            # batch
+    assert call(7, 3) == INVALID            # H % Hkv
+    assert call(11, 0) == INVALID           # k
+    assert call(11, 129) == INVALID         # k > D
+    assert call(15, 56) == INVALID          # ldot < Lq
+    assert call(4, 0) == UNSUPPORTED        # fp32
+    assert call(10, 64) == UNSUPPORTED      # D != 128
+    assert call(14, ctypes.c_void_p(0x100008)) == UNSUPPORTED  # Ot not 16-byte aligned
+    assert call(15, 68) == UNSUPPORTED      # ldot % 8
+    assert call(16, ctypes.c_void_p(0x100004)) == UNSUPPORTED  # energy not 8-byte aligned
+    a = list(base)
+    a[8], a[15] = 60, 64                    # Lq % 8
+    assert f(*a) == UNSUPPORTED
+    assert call(17, NULL) == WS_SMALL       # no workspace
+    assert call(18, need - 1) == WS_SMALL
+    assert call(17, ctypes.c_void_p(0x100010)) == INVALID      # workspace not 256-byte aligned
+
+
+def test_attention_kmajor_workspace_size():
+    # compacted key rows (as rmm_reduced_attention), then one float64 partial
+    # energy per (sequence, 256-query tile, output channel)
+    n = rmm.rmm_attention_kmajor_workspace_size(1, 32, 8192, 8192, 128, 64)
+    assert n == 32 * 8192 * 64 * 2 + 32 * 32 * 128 * 8
+    n = rmm.rmm_attention_kmajor_workspace_size(2, 4, 300, 520, 128, 33)
+    ki = 2 * 4 * 520 * 64 * 2
+    assert n == (ki + 255) // 256 * 256 + (2 * 2 * 4 * 128 * 8 + 255) // 256 * 256
+    assert rmm.rmm_attention_kmajor_workspace_size(1, 4, 64, 64, 128, 0) == 0
+    assert rmm.rmm_attention_kmajor_workspace_size(1, 4, 0, 64, 128, 8) == 0
+
+
 def test_linear_validation():
     f = rmm.lib.rmm_linear
     need = rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 64, 128, 64)
