@@ -7,7 +7,7 @@ copy equal to the transpose bit for bit, every index set bit-exact (float64
 margin rule), and each projection's output columns on sampled rows.
 
 Ratios: 0.5 (the headline) and 0.7, the per-component ratio of the paper's
-component analysis (App. C), whose retained counts are not multiples of the
+component analysis (App. B.4), whose retained counts are not multiples of the
 GEMM's 32-row stages (2868 of 4096, 10036 of 14336; 90 of 128 head dims)."""
 import functools
 import zlib
