@@ -31,7 +31,9 @@ reported under "fused_attention" with its speedup over r = 1 and its own
 MFMA roofline; it is not part of the step.  "attention_o_chain" times that
 block feeding the reduced output projection, with the block writing the
 projection's K-major input and column energies (no separate scoring pass)
-against the unfused chain.
+against the unfused chain; "mlp_chain" likewise for the gate|up GEMM whose
+epilogue applies silu(g) * u and writes the down projection's K-major input
+and column energies.
 
 A decode step of the same layer (batch 1, one token: energies, TopK and the
 reduced product over the retained weight rows per projection group) is timed
@@ -108,6 +110,8 @@ def parse():
                    help="skip the separate timing of the fused attention block")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the separate timing of the decode step")
+    p.add_argument("--no-mlp-chain", action="store_true",
+                   help="skip the timing of the MLP chain (fused and unfused)")
     p.add_argument("--no-policies", action="store_true",
                    help="skip the steps with per-component retention ratios")
     p.add_argument("--no-pv", action="store_true",
@@ -360,6 +364,77 @@ def time_attention_chain(L, r, steps, warmup):
     return {"r": r, "k_heads": kq, "k_o": ko, "fused_us": us_f, "unfused_us": us_u,
             "layout_copy_us": us_l, "unfused_without_copy_us": us_u - us_l,
             "speedup": us_u / us_f, "speedup_without_copy": (us_u - us_l) / us_f, "calls": steps}
+
+
+def time_mlp_chain(L, r, steps, warmup):
+    """The MLP of the layer at ratio r (both selections), both ways:
+      fused   : energies + TopK of the MLP input -> rmm_reduced_gemm_swiglu_kmajor
+                (the gate|up product whose epilogue writes the down
+                projection's K-major input H^T and its column energies) ->
+                TopK -> down K-major GEMM;
+      unfused : energies + TopK -> gate|up GEMM (Y) -> torch silu(g) * u (H,
+                token-major) -> rmm_score_kmajor(H) -> TopK -> down GEMM.
+    Every call is bracketed by HIP events on the launch stream; the torch
+    activation is also timed alone."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    wk, M = L.wk, L.M
+    K = wk.inputs["mlp_in"][0]
+    F = wk.inputs["down_in"][0]
+    k = rmm.rmm_retained_count(r, K)
+    kd = rmm.rmm_retained_count(r, F)
+    idx = torch.empty(k, dtype=torch.int32, device=L.dev)
+    sel = torch.empty(kd, dtype=torch.int32, device=L.dev)
+    Wgu = rmm.swiglu_weight_layout(L.W["gate"], L.W["up"])
+    Ht = torch.empty((F, M), dtype=torch.bfloat16, device=L.dev)
+    H = torch.empty((M, F), dtype=torch.bfloat16, device=L.dev)
+    eh = torch.empty(F, dtype=torch.float64, device=L.dev)
+    ws_s = torch.empty(rmm.rmm_gemm_swiglu_workspace_size(1, M, F), dtype=torch.uint8,
+                       device=L.dev)
+    X, Xt, e = L.X["mlp_in"], L.Xt["mlp_in"], L.energy[:K]
+    Xtd, Wd, Yd, Ygu = L.Xt["down_in"], L.W["down"], L.Y["down"], L.Ycat["mlp_in"]
+
+    def head():
+        rmm.rmm_score_kmajor(X, e, Xt, L.ws)
+        rmm.rmm_select(e, k, idx)
+
+    def fused():
+        head()
+        rmm.rmm_reduced_gemm_swiglu_kmajor(Xt, Wgu, idx.view(1, k), Ht, eh, workspace=ws_s)
+        rmm.rmm_select(eh, kd, sel)
+        rmm.rmm_reduced_gemm_kmajor(Ht, Wd, sel.view(1, kd), Yd)
+
+    def activation():
+        torch.mul(torch.nn.functional.silu(Ygu[:, :F]), Ygu[:, F:], out=H)
+
+    def unfused():
+        head()
+        rmm.rmm_reduced_gemm_kmajor(Xt, L.Wcat["mlp_in"], idx.view(1, k), Ygu)
+        activation()
+        rmm.rmm_score_kmajor(H, eh, Xtd, L.ws)
+        rmm.rmm_select(eh, kd, sel)
+        rmm.rmm_reduced_gemm_kmajor(Xtd, Wd, sel.view(1, kd), Yd)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = []
+        for _ in range(steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        return sum(x.elapsed_time(y) for x, y in evs) / steps * 1e3
+
+    us_f, us_u, us_a = timed(fused), timed(unfused), timed(activation)
+    flop = 2 * M * (2 * F) * k + 2 * M * wk.inputs["mlp_in"][0] * kd
+    return {"r": r, "k_gate_up": k, "k_down": kd, "fused_us": us_f, "unfused_us": us_u,
+            "activation_us": us_a, "unfused_without_activation_us": us_u - us_a,
+            "speedup": us_u / us_f, "speedup_without_activation": (us_u - us_a) / us_f,
+            "retained_tflops_fused": flop / (us_f * 1e-6) / 1e12, "calls": steps}
 
 
 def attention_weights(L):
@@ -678,6 +753,23 @@ def main():
                         "select_kernel", "gemm_kmajor_tr_kernel"],
             "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
                                    for k, v in rec.items()} for r, rec in ch.items()},
+        }
+    if not args.no_mlp_chain:
+        mc = {r: time_mlp_chain(L, r, args.steps, args.warmup) for r in sorted(sweep)}
+        for r, rec in mc.items():
+            print(f"# MLP chain r={r}: fused {rec['fused_us']:.1f} us, unfused "
+                  f"{rec['unfused_us']:.1f} us ({rec['activation_us']:.1f} us of it the torch "
+                  f"activation)", file=sys.stderr, flush=True)
+        out["mlp_chain"] = {
+            "op": "the layer's MLP: gate|up (4096 -> 2 x 14336) then down (14336 -> 4096), "
+                  "each reduced at r; fused = the gate|up GEMM's epilogue applies silu(g)*u "
+                  "and writes the down projection's K-major input and its column energies "
+                  "(no scoring pass over it), unfused = gate|up GEMM, torch activation, "
+                  "scoring pass with K-major copy; both then TopK and the down GEMM",
+            "kernels": ["score_tile_kernel", "select_kernel", "gemm_kmajor_tr_kernel",
+                        "score_finalize_kernel"],
+            "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
+                                   for k, v in rec.items()} for r, rec in mc.items()},
         }
     if not args.no_decode:
         dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}

@@ -282,6 +282,45 @@ rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
                                    hipStream_t stream);
 
 /*
+ * Reduced gate|up projection feeding the reduced down projection   (Sec. 3.3
+ * "MLP and linear projections": gate, up and down are each reduced, the down
+ * projection selecting from its own input; that input is the MLP's
+ * activation of the gate and up outputs, here SwiGLU as in the LLaMA-family
+ * models the paper evaluates; the Limitations section names the memory
+ * movement of separate scoring as a cost to remove).
+ *
+ * The gathered GEMM of rmm_reduced_gemm_kmajor over the gate and up weights,
+ * whose epilogue applies the activation and writes the down projection's
+ * K-major input and its column energies instead of the two outputs:
+ *   g = bf16(X[:, I] Wg[I, :]),  u = bf16(X[:, I] Wu[I, :])   (as Y would be),
+ *   Ht[b][c][m] = bf16(bf16(silu(g[m][c])) * u[m][c]),  silu(x) = x/(1+e^-x)
+ *                 in fp32,
+ *   energy[b][c] = sum over m < M of Ht[b][c][m]^2 (float64 sums of exact
+ *                 squares, in a fixed order).
+ * Feed them to rmm_select (K = F) and rmm_reduced_gemm_kmajor (Xt = Ht).
+ *
+ * Xt  : the MLP input's K-major copy [B][K][ldxt] (from rmm_score_kmajor).
+ * Wgu : bf16 [K][ldw], 2F columns in 128-column blocks: block 2q holds the
+ *       gate weights of channels 128q .. 128q+127, block 2q+1 the up weights
+ *       of the same channels (a column permutation of [Wg | Wu] made once at
+ *       load time).  idx: int32 [B*k] ascending, as for rmm_reduced_gemm.
+ * Ht  : bf16 [B][F][ldht], ldht >= M, 16-byte aligned; columns M..ldht-1
+ *       are not written.  energy: float64 [B][F], 8-byte aligned.
+ * workspace : rmm_gemm_swiglu_workspace_size(B, M, F) bytes, 8-byte aligned
+ *       (per-row-tile partial energies; overwritten by every call).
+ * Errors : INVALID_ARGUMENT for null pointers, sizes < 1, k outside [1, K],
+ *       ldxt < M, ldw < 2F or ldht < M; UNSUPPORTED unless F % 128 == 0,
+ *       M % 8 == 0, ldht % 8 == 0, Ht 16-byte aligned and the conditions of
+ *       rmm_reduced_gemm_kmajor hold; WORKSPACE_TOO_SMALL.
+ */
+size_t rmm_gemm_swiglu_workspace_size(int64_t B, int64_t M, int64_t F);
+rmm_status_t rmm_reduced_gemm_swiglu_kmajor(const void *Xt, const void *Wgu, const int32_t *idx,
+                                            int64_t B, int64_t M, int64_t F, int64_t K, int64_t k,
+                                            int64_t ldxt, int64_t ldw, void *Ht, int64_t ldht,
+                                            double *energy, void *workspace,
+                                            size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Reduced attention block feeding a reduced projection   (Sec. 3.3: the
  * block's output is the input of the attention output projection, whose
  * retained set Sec. 3.2 scores from that input's columns; the Limitations

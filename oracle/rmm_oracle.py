@@ -29,6 +29,9 @@ Paper passages followed (arXiv 2608.13426, "Reduced Matrix Multiplication"):
   (Proposition "RMM Approximation Error Bound"), the factorised bound
   (Corollary) and the normalised bound with the discarded-energy ratios;
   Appendix B.4 defines the retained-energy diagnostic.
+* The MLP activation between the reduced gate/up and down projections of
+  the evaluated LLaMA-family models: silu(gate) * up (used to chain the
+  projections; it is the models' own operation, not part of RMM).
 * Appendix A, "Inference setup": the index set is recomputed per affected
   product from the current sequence's activation block (one selection per
   sequence; one per query head on the attention side).
@@ -262,6 +265,26 @@ def reduced_pv(P: np.ndarray, V: np.ndarray, kt: int):
     idx = np.stack([topk_indices(column_energies(P[h]), kt) for h in range(H)])
     O = np.stack([reduced_matmul(P[h], V[gqa_kv_head(h, H, Hkv)], idx[h]) for h in range(H)])
     return O, idx
+
+
+# ---------------------------------------------------------------------------
+# The MLP between the reduced gate/up and down projections
+# ---------------------------------------------------------------------------
+
+def silu(x: np.ndarray) -> np.ndarray:
+    """SiLU, x * sigmoid(x) = x / (1 + exp(-x)), in float64.
+
+    The MLP of the LLaMA-family models the paper evaluates (Sec. 4 setup;
+    Sec. 3.3 reduces its up, gate and down projections) feeds the down
+    projection with silu(gate output) * up output."""
+    x = np.asarray(x, dtype=np.float64)
+    with np.errstate(over="ignore"):
+        return x / (1.0 + np.exp(-x))
+
+
+def swiglu(g: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """The down projection's input: silu(g) * u, elementwise, float64."""
+    return silu(g) * np.asarray(u, dtype=np.float64)
 
 
 # ---------------------------------------------------------------------------

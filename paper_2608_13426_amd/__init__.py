@@ -58,6 +58,10 @@ _SIGS = {
     "rmm_reduced_pv": (ctypes.c_int, [_p, _p, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64,
                                       _i64, _i64, _p, _p, _p, ctypes.c_size_t, _p]),
     "rmm_attention_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64, _i64, _i64]),
+    "rmm_gemm_swiglu_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64]),
+    "rmm_reduced_gemm_swiglu_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64,
+                                                      _i64, _i64, _p, _i64, _p, _p,
+                                                      ctypes.c_size_t, _p]),
     "rmm_reduced_attention_kmajor": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int, _i64, _i64, _i64,
                                                     _i64, _i64, _i64, _i64, ctypes.c_float,
                                                     ctypes.c_int, _p, _i64, _p, _p, ctypes.c_size_t,
@@ -297,6 +301,59 @@ def rmm_reduced_gemm_kmajor(Xt: torch.Tensor, W: torch.Tensor, idx: torch.Tensor
         Xt.data_ptr(), W.data_ptr(), idx.data_ptr(), B, M, N, K, k, ldxt, ldw, Y.data_ptr(),
         ldy, _stream(d, stream)))
     return Y
+
+
+def swiglu_weight_layout(Wg: torch.Tensor, Wu: torch.Tensor) -> torch.Tensor:
+    """The gate and up weights [K, F] as rmm_reduced_gemm_swiglu_kmajor reads
+    them: [K, 2F] in 128-column blocks, gate then up of the same 128 channels
+    (a column permutation, made once at load time)."""
+    if Wg.shape != Wu.shape or Wg.dim() != 2 or Wg.shape[1] % 128:
+        raise ValueError("Wg and Wu must be [K, F] with F a multiple of 128")
+    K, F = Wg.shape
+    return torch.stack([Wg.reshape(K, F // 128, 128), Wu.reshape(K, F // 128, 128)],
+                       dim=2).reshape(K, 2 * F).contiguous()
+
+
+def rmm_gemm_swiglu_workspace_size(B: int, M: int, F: int) -> int:
+    return int(lib.rmm_gemm_swiglu_workspace_size(B, M, F))
+
+
+def rmm_reduced_gemm_swiglu_kmajor(Xt: torch.Tensor, Wgu: torch.Tensor, idx: torch.Tensor,
+                                   Ht: torch.Tensor, energy: torch.Tensor,
+                                   workspace: torch.Tensor | None = None,
+                                   stream=None) -> torch.Tensor:
+    """The reduced gate|up product from the K-major copy Xt [B, K, M] with the
+    SwiGLU epilogue: writes the down projection's K-major input Ht [B, F, M]
+    (rows of stride ldht >= M) and its column energies energy float64 [B, F].
+    Wgu [K, 2F] in the layout of swiglu_weight_layout; idx [B, k]."""
+    B, K, M, ldxt = _rows(Xt, "Xt")
+    if Ht.dim() == 2:
+        Ht = Ht.unsqueeze(0)
+    if energy.dim() == 1:
+        energy = energy.unsqueeze(0)
+    d = _dev(Xt, Wgu, idx, Ht, energy)
+    if Wgu.dim() != 2 or Wgu.shape[0] != K or Wgu.stride(1) != 1 or Wgu.shape[1] % 2:
+        raise ValueError("Wgu must be [K, 2F] with contiguous rows")
+    F, ldw = Wgu.shape[1] // 2, Wgu.stride(0)
+    if Ht.shape[0] != B or Ht.shape[1] != F or Ht.shape[2] != M:
+        raise ValueError("Ht must be [B, F, M]")
+    if Ht.stride(2) != 1 or (B > 1 and Ht.stride(0) != F * Ht.stride(1)):
+        raise ValueError("Ht rows must be contiguous, with one row stride ldht")
+    if tuple(energy.shape) != (B, F) or not energy.is_contiguous() or energy.dtype != torch.float64:
+        raise ValueError("energy must be contiguous float64 [B, F]")
+    if not (Xt.dtype == Wgu.dtype == Ht.dtype == torch.bfloat16):
+        raise TypeError("Xt, Wgu and Ht must be bfloat16")
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.numel() % B:
+        raise ValueError("idx must be contiguous int32 [B, k]")
+    k = idx.numel() // B
+    if workspace is None:
+        workspace = torch.empty(max(rmm_gemm_swiglu_workspace_size(B, M, F), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_reduced_gemm_swiglu_kmajor", lib.rmm_reduced_gemm_swiglu_kmajor(
+        Xt.data_ptr(), Wgu.data_ptr(), idx.data_ptr(), B, M, F, K, k, ldxt, ldw, Ht.data_ptr(),
+        Ht.stride(1), energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    return Ht
 
 
 def rmm_reduced_qk(Q: torch.Tensor, Kc: torch.Tensor, idx: torch.Tensor, S: torch.Tensor,

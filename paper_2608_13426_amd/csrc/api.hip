@@ -202,6 +202,33 @@ rmm_status_t rmm_reduced_gemm_kmajor(const void *Xt, const void *W, const int32_
                                                  ldxt, ldw, static_cast<uint16_t *>(Y), ldy, stream));
 }
 
+size_t rmm_gemm_swiglu_workspace_size(int64_t B, int64_t M, int64_t F) {
+    if (B < 1 || M < 1 || F < 1) return 0;
+    return align256(static_cast<size_t>(B * ((M + 255) / 256) * F) * sizeof(double));
+}
+
+rmm_status_t rmm_reduced_gemm_swiglu_kmajor(const void *Xt, const void *Wgu, const int32_t *idx,
+                                            int64_t B, int64_t M, int64_t F, int64_t K, int64_t k,
+                                            int64_t ldxt, int64_t ldw, void *Ht, int64_t ldht,
+                                            double *energy, void *workspace,
+                                            size_t workspace_bytes, hipStream_t stream) {
+    if (!Xt || !Wgu || !idx || !Ht || !energy) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || M < 1 || F < 1 || K < 1 || k < 1 || k > K) return RMM_ERR_INVALID_ARGUMENT;
+    if (ldxt < M || ldw < 2 * F || ldht < M) return RMM_ERR_INVALID_ARGUMENT;
+    if (K > kInt32Max || M > kInt32Max || 2 * F > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (!kmajor_ok(Xt, Wgu, B, M, K, ldxt, ldw)) return RMM_ERR_UNSUPPORTED;
+    if (F % 128 || M % 8 || ldht % 8 || !aligned16(Ht) || reinterpret_cast<uintptr_t>(energy) % 8)
+        return RMM_ERR_UNSUPPORTED;
+    if ((M + 255) / 256 * (F / 128) > kInt32Max) return RMM_ERR_UNSUPPORTED;
+    const size_t need = rmm_gemm_swiglu_workspace_size(B, M, F);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
+    return from_hip(rmm::launch_gemm_swiglu_kmajor_bf16(
+        static_cast<const uint16_t *>(Xt), static_cast<const uint16_t *>(Wgu), idx, B, M, F, K, k,
+        ldxt, ldw, static_cast<uint16_t *>(Ht), ldht, energy, static_cast<double *>(workspace),
+        stream));
+}
+
 rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx, rmm_dtype_t dtype,
                             int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
                             int64_t D, int64_t k, float scale, int causal, void *S,

@@ -525,12 +525,47 @@ __device__ __forceinline__ void wait_vmcnt_le() {
 }
 }  // namespace trk
 
-template <int NW, int BKS, int S>
+// x of the lane that the DPP control CTRL names (within a row of 16 lanes),
+// for a float64 value
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+    const uint32_t lo = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, 0xF, 0xF, false));
+    const uint32_t hi = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, 0xF, 0xF, false));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+#else
+    return x;
+#endif
+}
+
+// bf16(bf16(silu(g)) * u) for bf16 g, u (bits in the low half); silu(g) =
+// g / (1 + e^-g) in fp32 with the hardware exp2 and reciprocal (each about
+// one ulp), far below the bf16 rounding that follows
+__device__ __forceinline__ uint32_t swiglu_bf16(uint32_t gb, uint32_t ub) {
+    const float g = __uint_as_float(gb << 16), u = __uint_as_float(ub << 16);
+    const float sg = bf16_to_f32(f32_to_bf16(g * __builtin_amdgcn_rcpf(1.f + __expf(-g))));
+    return f32_to_bf16(sg * u);
+}
+
+// EPI selects the epilogue.  0: Y = the product.  1 (SwiGLU): the weight
+// columns come in 128-column blocks, gate then up of the same 128 channels,
+// so a 256-column tile holds both halves of channels c0 = n0/2 .. c0+127;
+// the tile writes, for the down projection that follows,
+//   Ht[unit][c][m] = bf16(bf16(silu(g[m][c])) * u[m][c])   (K-major, row
+//   stride ldy; g and u the bf16-rounded products, as a plain launch would
+//   store them),
+// and part[(unit * tiles_m + m0/256) * N/2 + c] = sum over its rows m < M of
+// Ht[unit][c][m]^2 in float64 (one row tile's share of that input's column
+// energies).
+template <int NW, int BKS, int S, int EPI = 0>
 __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     const uint16_t *__restrict__ Xt, const uint16_t *__restrict__ W,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int k,
     int64_t ldxt, int64_t ldw, int64_t ldy, int64_t xt_bytes, int64_t w_bytes, int tiles_m,
-    int tiles_n, int vec_y) {
+    int tiles_n, int vec_y, double *__restrict__ part) {
     using namespace trk;
     constexpr int ASZ = BKS * ROWB;      // one operand, one stage
     constexpr int PPW = BKS / 2 / NW;    // staged row pairs per wave per operand
@@ -539,7 +574,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     constexpr int FM = 4, FN = TWN / 32;
     constexpr int D = S - 1;             // stages in flight ahead of the MFMAs
     constexpr int PER_STAGE = 2 * PPW;   // loads per wave per stage
-    static_assert((NW == 4 || NW == 8) && PPW * NW * 2 == BKS && PPW % 2 == 0, "wave layout");
+    static_assert((NW == 4 || NW == 8) && PPW * NW * 2 == BKS && PPW >= 1, "wave layout");
     static_assert(BKS % 16 == 0 && S >= 2 && S <= 4 && 2 * S * ASZ <= 160 * 1024, "stages");
     static_assert((D - 1) * PER_STAGE < 64, "vmcnt range");
     // One LDS object per stage and operand: the compiler then sees that a
@@ -585,7 +620,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
 
     // DMA role: row pair P = wave*PPW + q of a stage holds retained rows
     // 2P + h; this lane fills chunk position p of its row with source chunk
-    // p ^ 4*(row % 4), and row % 4 = (2q + h) % 4.
+    // p ^ 4*(row % 4), and row % 4 = (2P + h) % 4.
     const int h = lane >> 5, p = lane & 31;
     uint32_t acol[2], bcol[2];
 #pragma unroll
@@ -608,9 +643,9 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
         for (int q = 0; q < PPW; ++q) {
             const bool in = base + 2 * q + h < k;
             const uint32_t j = static_cast<uint32_t>(h ? r[2 * q + 1] : r[2 * q]);
-            const uint32_t ao = in ? j * arow + acol[q & 1] : kOut;
-            const uint32_t bo = in ? j * brow + bcol[q & 1] : kOut;
             const int P = wave * PPW + q;
+            const uint32_t ao = in ? j * arow + acol[P & 1] : kOut;
+            const uint32_t bo = in ? j * brow + bcol[P & 1] : kOut;
             lds_load16(ar, la + P * 1024, ao);
             lds_load16(br, lb + P * 1024, bo);
         }
@@ -716,6 +751,114 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     // acc[j][i][4*gq + r]: n = n0 + wn*TWN + 32j + 8gq + 4*(lane/32) + r,
     //                      m = m0 + wm*128 + 32i + lane%32
     const int lr = lane & 31, lh = lane >> 5;
+    if constexpr (EPI == 1) {
+        static_assert(NW == 8 && FM == 4 && FN == 2 && BT == 256 && BKS >= 32, "SwiGLU epilogue layout");
+        typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+        typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+        auto obj = [&](int q) -> char * {
+            return q == 0 ? sA0 : q == 1 ? sA1 : q == 2 ? sB0 : sB1;
+        };
+        const int F = N / 2, c0 = n0 / 2;
+        // thread role: channel pair cp (channels c0 + 2cp, +1), row group g8
+        // (rows 8*g8 .. +7 and 64 + 8*g8 .. +7 of a pass's 128)
+        const int cp = tid >> 3, g8 = tid & 7;
+        double eA = 0.0, eB = 0.0;
+        uint32_t hk[2][2][2][4];                 // [pass][half][channel][8 packed rows]
+        __syncthreads();                         // ring reads done, tail loads landed
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            // pass p: rows m0 + 128p .. +127 (the waves with wm == p), object i
+            // holding rows 32i .. 32i+31 of the pass; within a row the 16-byte
+            // chunk c sits at c ^ (row % 32)
+            if (wm == p) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+#pragma unroll
+                        for (int gq = 0; gq < 4; ++gq) {
+                            const int c = (wn * TWN) / 8 + 4 * j + gq;
+                            const u32x2_t v = {pack_bf16x2(acc[j][i][4 * gq], acc[j][i][4 * gq + 1]),
+                                               pack_bf16x2(acc[j][i][4 * gq + 2], acc[j][i][4 * gq + 3])};
+                            *reinterpret_cast<u32x2_t *>(obj(i) + lr * ROWB + 16 * (c ^ lr) + 8 * lh) = v;
+                        }
+            }
+            __syncthreads();
+            const int mp = m0 + 128 * p;
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int R0 = 64 * half + 8 * g8;          // first of the thread's 8 rows
+                const char *o = obj(R0 / 32);
+                uint32_t *hA = hk[p][half][0], *hB = hk[p][half][1];
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const int rl = (R0 % 32) + r;           // row within the object
+                    const uint32_t gw = *reinterpret_cast<const uint32_t *>(
+                        o + rl * ROWB + 16 * ((cp >> 2) ^ rl) + 4 * (cp & 3));
+                    const uint32_t uw = *reinterpret_cast<const uint32_t *>(
+                        o + rl * ROWB + 16 * ((16 + (cp >> 2)) ^ rl) + 4 * (cp & 3));
+                    const uint32_t a = swiglu_bf16(gw & 0xffffu, uw & 0xffffu);
+                    const uint32_t b = swiglu_bf16(gw >> 16, uw >> 16);
+                    if (r & 1) { hA[r >> 1] |= a << 16; hB[r >> 1] |= b << 16; }
+                    else { hA[r >> 1] = a; hB[r >> 1] = b; }
+                }
+                // M % 8 == 0: the 8 rows are all inside or all past M
+                if (mp + R0 < M) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const double a0 = static_cast<double>(__uint_as_float(hA[q] << 16));
+                        const double a1 = static_cast<double>(__uint_as_float(hA[q] & 0xffff0000u));
+                        const double b0 = static_cast<double>(__uint_as_float(hB[q] << 16));
+                        const double b1 = static_cast<double>(__uint_as_float(hB[q] & 0xffff0000u));
+                        eA = fma(a0, a0, eA); eA = fma(a1, a1, eA);
+                        eB = fma(b0, b0, eB); eB = fma(b1, b1, eB);
+                    }
+                }
+            }
+            __syncthreads();                     // the staged rows are read
+        }
+        // H^T of the tile through the same objects: channel row c (0..127) in
+        // object c / 32, row c % 32; its 16-byte chunk q (8 tokens) at q ^ (c % 32)
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int ch = 0; ch < 2; ++ch) {
+                    const int c = 2 * cp + ch, q = 16 * p + 8 * half + g8;
+                    const uint32_t *h = hk[p][half][ch];
+                    *reinterpret_cast<u32x4_t *>(obj(c >> 5) + (c & 31) * ROWB + 16 * (q ^ (c & 31))) =
+                        u32x4_t{h[0], h[1], h[2], h[3]};
+                }
+        __syncthreads();
+        {
+            // each half-wave writes one channel row per pass: 32 lanes x 16
+            // bytes = the tile's 256 tokens (streaming stores, as Y's)
+            uint16_t *Hu = Y + unit * static_cast<int64_t>(F) * ldy + m0;
+            const int q = lane & 31, hw = tid >> 5;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = hw + 16 * i;
+                const u32x4_t v = *reinterpret_cast<const u32x4_t *>(obj(c >> 5) + (c & 31) * ROWB +
+                                                                     16 * (q ^ (c & 31)));
+                if (m0 + 8 * q < M)
+                    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t *>(
+                        Hu + static_cast<int64_t>(c0 + c) * ldy + 8 * q));
+            }
+        }
+        // the 8 row groups of a channel pair are lanes 8q .. 8q+7: add them
+        // (lane ^ 1, lane ^ 2, then the mirror within 8 lanes; every lane of
+        // the group ends with the same sum)
+        eA += dpp_f64<0xB1>(eA);  eB += dpp_f64<0xB1>(eB);
+        eA += dpp_f64<0x4E>(eA);  eB += dpp_f64<0x4E>(eB);
+        eA += dpp_f64<0x141>(eA); eB += dpp_f64<0x141>(eB);
+        if (g8 == 0) {
+            double *pp = part + (unit * tiles_m + m0 / BT) * static_cast<int64_t>(F) + c0 + 2 * cp;
+            pp[0] = eA;
+            pp[1] = eB;
+        }
+        return;
+    }
     uint16_t *Yu = Y + unit * static_cast<int64_t>(M) * ldy;
     const int rows = min(BT, M - m0);
     const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
@@ -906,7 +1049,8 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
         hipLaunchKernelGGL((gemm_kmajor_tr_kernel<kTrWaves, kTrRows, kTrStages>),
                            dim3(tm * tn, static_cast<unsigned>(B)), dim3(kTrWaves * 64), 0, stream,
                            Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
-                           static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, tn, vec_y);
+                           static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, tn, vec_y,
+                           nullptr);
     } else if (t256 * B >= 128) {
         const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
         hipLaunchKernelGGL((gemm_kmajor_bf16_kernel<256, kKmajorWaves>),
@@ -921,6 +1065,23 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                            ldw, ldy, xt_bytes, w_bytes, tm, tn);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_gemm_swiglu_kmajor_bf16(const uint16_t *Xt, const uint16_t *W,
+                                         const int32_t *idx, int64_t B, int64_t M, int64_t F,
+                                         int64_t K, int64_t k, int64_t ldxt, int64_t ldw,
+                                         uint16_t *Ht, int64_t ldht, double *energy,
+                                         double *partials, hipStream_t stream) {
+    const int64_t xt_bytes = K * ldxt * 2, w_bytes = K * ldw * 2;
+    const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>(F / 128);
+    hipLaunchKernelGGL((gemm_kmajor_tr_kernel<kTrWaves, kTrRows, kTrStages, 1>),
+                       dim3(tm * tn, static_cast<unsigned>(B)), dim3(kTrWaves * 64), 0, stream,
+                       Xt, W, idx, Ht, static_cast<int>(M), static_cast<int>(2 * F),
+                       static_cast<int>(k), ldxt, ldw, ldht, xt_bytes, w_bytes, tm, tn, 2, partials);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // energies: the row tiles' partial sums, added in tile order
+    return launch_score_finalize(partials, B, tm, F, energy, stream);
 }
 
 hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx, int64_t B,

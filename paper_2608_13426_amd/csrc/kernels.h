@@ -46,6 +46,16 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                                   int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                                   int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
                                   hipStream_t stream);
+// the gate|up product with the SwiGLU epilogue: W [K][ldw] holds 2F columns
+// in 128-column blocks (gate, then up, of the same 128 channels); writes the
+// down projection's K-major input Ht [B][F][ldht] and its column energies
+// energy [B][F]; partials holds B * ceil(M/256) * F doubles.  F % 128 == 0,
+// M % 8 == 0, ldht % 8 == 0, Ht 16-byte aligned (checked by the caller).
+hipError_t launch_gemm_swiglu_kmajor_bf16(const uint16_t *Xt, const uint16_t *W,
+                                         const int32_t *idx, int64_t B, int64_t M, int64_t F,
+                                         int64_t K, int64_t k, int64_t ldxt, int64_t ldw,
+                                         uint16_t *Ht, int64_t ldht, double *energy,
+                                         double *partials, hipStream_t stream);
 hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx,
                            int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                            int64_t ldx, int64_t ldw, float *Y, int64_t ldy,

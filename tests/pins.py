@@ -444,6 +444,25 @@ def check_pv(o):
         assert np.allclose(O[h], (h // 2 + 1.0) * rows[:, None], rtol=1e-14, atol=0)
 
 
+def check_swiglu(o):
+    # silu(0) = 0; silu(x) - silu(-x) = x (sigmoid(x) + sigmoid(-x) = 1);
+    # silu(1) = 1 / (1 + 1/e), silu(-1) = -1 / (1 + e) (closed forms)
+    assert o.silu(np.array([0.0]))[0] == 0.0
+    xs = np.linspace(-9.0, 9.0, 37)
+    assert np.allclose(o.silu(xs) - o.silu(-xs), xs, rtol=0, atol=1e-14)
+    assert abs(o.silu(np.array([1.0]))[0] - 1.0 / (1.0 + math.exp(-1.0))) < 1e-16
+    assert abs(o.silu(np.array([-1.0]))[0] + 1.0 / (1.0 + math.e)) < 1e-16
+    # tails: x for large x, 0 from below for very negative x
+    assert o.silu(np.array([40.0]))[0] == 40.0
+    v = o.silu(np.array([-40.0]))[0]
+    assert -1e-15 < v < 0.0
+    # the activation gates with g and scales by u (not the other way round)
+    g, u = np.array([1.0, -2.0, 3.0]), np.array([2.0, 0.5, -1.0])
+    want = np.array([2.0 / (1.0 + math.exp(-1.0)), 0.5 * -2.0 / (1.0 + math.exp(2.0)),
+                     -3.0 / (1.0 + math.exp(-3.0))])
+    assert np.allclose(o.swiglu(g, u), want, rtol=1e-15, atol=0)
+
+
 def check_margin(o):
     assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
     assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
@@ -453,4 +472,4 @@ def check_margin(o):
 
 ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
               check_bounds, check_worked_example, check_qk, check_attention, check_pv,
-              check_margin)
+              check_swiglu, check_margin)

@@ -254,6 +254,48 @@ def test_attention_kmajor_workspace_size():
     assert rmm.rmm_attention_kmajor_workspace_size(1, 4, 0, 64, 128, 8) == 0
 
 
+def test_gemm_swiglu_validation():
+    f = rmm.lib.rmm_reduced_gemm_swiglu_kmajor
+    A = ctypes.c_void_p(0x100000)
+    need = rmm.rmm_gemm_swiglu_workspace_size(1, 512, 256)
+    # Xt Wgu idx B M F K k ldxt ldw Ht ldht energy ws ws_bytes stream
+    base = [A, A, P, 1, 512, 256, 300, 150, 512, 512, A, 512, A, A, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 10, 12):
+        assert call(i, NULL) == INVALID
+    assert call(3, 0) == INVALID            # B
+    assert call(5, 0) == INVALID            # F
+    assert call(7, 0) == INVALID            # k
+    assert call(7, 301) == INVALID          # k > K
+    assert call(8, 504) == INVALID          # ldxt < M
+    assert call(9, 504) == INVALID          # ldw < 2F
+    assert call(11, 504) == INVALID         # ldht < M
+    assert call(5, 192) == UNSUPPORTED      # F % 128 (ldw 512 still >= 2F)
+    a = list(base)
+    a[4], a[8], a[11] = 500, 504, 504       # M % 8
+    assert f(*a) == UNSUPPORTED
+    assert call(11, 516) == UNSUPPORTED     # ldht % 8
+    assert call(10, ctypes.c_void_p(0x100008)) == UNSUPPORTED  # Ht not 16-byte aligned
+    assert call(1, ctypes.c_void_p(0x100008)) == UNSUPPORTED   # Wgu not 16-byte aligned
+    assert call(12, ctypes.c_void_p(0x100004)) == UNSUPPORTED  # energy not 8-byte aligned
+    assert call(13, NULL) == WS_SMALL
+    assert call(14, need - 1) == WS_SMALL
+    assert call(13, ctypes.c_void_p(0x100004)) == INVALID      # workspace not 8-byte aligned
+
+
+def test_gemm_swiglu_workspace_size():
+    # one float64 partial energy per (unit, 256-row tile, channel)
+    assert rmm.rmm_gemm_swiglu_workspace_size(1, 8192, 14336) == 32 * 14336 * 8
+    assert rmm.rmm_gemm_swiglu_workspace_size(2, 264, 128) == 2 * 2 * 128 * 8
+    assert rmm.rmm_gemm_swiglu_workspace_size(1, 8, 128) == 1024
+    assert rmm.rmm_gemm_swiglu_workspace_size(0, 8, 128) == 0
+
+
 def test_linear_validation():
     f = rmm.lib.rmm_linear
     need = rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 64, 128, 64)

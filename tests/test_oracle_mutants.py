@@ -209,7 +209,24 @@ _pv_scores_l1 = _pv_patch(lambda A: np.abs(A).sum(axis=0), _gqa)
 _pv_gqa_modulo = _pv_patch(ro.column_energies, lambda h, H, Hkv: h % Hkv)
 
 
+def _silu_sigmoid(x):
+    x = np.asarray(x, dtype=np.float64)
+    return 1.0 / (1.0 + np.exp(-x))
+
+
+def _silu_sign(x):
+    x = np.asarray(x, dtype=np.float64)
+    return x / (1.0 + np.exp(x))
+
+
+def _swiglu_swapped(g, u):
+    return ro.silu(u) * np.asarray(g, dtype=np.float64)
+
+
 MUTANTS = {
+    "silu_is_sigmoid": ("silu", _silu_sigmoid),
+    "silu_sign": ("silu", _silu_sign),
+    "swiglu_swapped": ("swiglu", _swiglu_swapped),
     "pv_scores_over_rows": ("reduced_pv", _pv_scores_rows),
     "pv_scores_l1": ("reduced_pv", _pv_scores_l1),
     "pv_gqa_modulo": ("reduced_pv", _pv_gqa_modulo),
