@@ -110,6 +110,8 @@ def parse():
                    help="skip the separate timing of the fused attention block")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the separate timing of the decode step")
+    p.add_argument("--no-attention-chain", action="store_true",
+                   help="skip the timing of the attention -> o-projection chain")
     p.add_argument("--no-mlp-chain", action="store_true",
                    help="skip the timing of the MLP chain (fused and unfused)")
     p.add_argument("--no-policies", action="store_true",
@@ -738,7 +740,7 @@ def main():
                              ATTN_TRAFFIC, f"{wk.name} r={','.join(str(r) for r in sorted(att))}"),
                          "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, both kernels)"},
         }
-    if not args.no_fused_attention:
+    if not args.no_attention_chain:
         ch = {r: time_attention_chain(L, r, args.steps, args.warmup) for r in sorted(sweep)}
         for r, rec in ch.items():
             print(f"# attention -> o-projection r={r}: fused {rec['fused_us']:.1f} us, unfused "
