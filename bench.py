@@ -75,15 +75,15 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
 # per-kv-head launches, smaller grids, excluded).  Each figure is valid only for the
 # source whose SHA-256 is recorded and for the same launch mix.
 GEMM_TRAFFIC = {"source": GEMM_SOURCE,
-                "sha256": "383f6ce3e5976e9a42786d740c7006cc2d8c619fb1cb354b93eb8020730394a7",
+                "sha256": "9e6a6e7fbc20e617e25077398ad072c3e3f5e8c7bed153fdc04bf8187a35e8ea",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
-                "bytes": round((399437.54 * 2.0 + 172170.95) * 1024)}
+                "bytes": round((399414.80 * 2.0 + 172304.08) * 1024)}
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"source": os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "attn.hip"),
-                "sha256": "e2348a3c4851579e6ae4e805c8094dbcd7b93007e82a311fb9b1d71d822838a7",
+                "sha256": "f4a53d4153da9d1ff39649ac233eecb57ba5203c0f904b339ae0d8a47761fd72",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0",
-                "bytes": round((103617.145 * 2.0 + 65554.17 + 8249.90 * 2.0 + 40960.00) * 1024)}
+                "bytes": round((103398.442 * 2.0 + 65545.42 + 8249.01 * 2.0 + 40960.00) * 1024)}
 
 
 def recorded_traffic(rec, mix):
