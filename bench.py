@@ -205,8 +205,11 @@ def flops(wk, r):
     return proj, qk
 
 
-def run_step(L, r, gemm_events=None):
-    """Enqueue one full step on the current stream (r: a ratio or a policy)."""
+def run_step(L, r, gemm_events=None, diag=None):
+    """Enqueue one full step on the current stream (r: a ratio or a policy).
+    With `diag` (a dict), also record each selection's retained-energy
+    fraction (App. B.4: the share of the input's squared norm on the kept
+    channels, from the step's own energies and sets; synchronises)."""
     import torch
     import paper_2608_13426_amd as rmm
     wk = L.wk
@@ -219,6 +222,8 @@ def run_step(L, r, gemm_events=None):
         if L.idx[name] is None or L.idx[name].numel() != k:
             L.idx[name] = torch.empty(k, dtype=torch.int32, device=L.dev)
         rmm.rmm_select(e, k, L.idx[name])
+        if diag is not None:
+            diag[name] = float(e[L.idx[name].long()].sum() / e.sum())
         if gemm_events is not None:
             ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             ev0.record()
@@ -233,6 +238,10 @@ def run_step(L, r, gemm_events=None):
     if L.qidx is None or L.qidx.numel() != a.H * kq:
         L.qidx = torch.empty(a.H * kq, dtype=torch.int32, device=L.dev)
     rmm.rmm_select(e, kq, L.qidx)
+    if diag is not None:
+        eh = e.view(a.H, a.D)
+        kept = torch.gather(eh, 1, L.qidx.view(a.H, kq).long()).sum(dim=1)
+        diag["qk_heads_mean"] = float((kept / eh.sum(dim=1)).mean())
     rmm.rmm_reduced_qk(L.Q, L.Kc, L.qidx.view(1, a.H, kq), L.S, causal=True)
 
 
@@ -255,6 +264,9 @@ def time_ratio(L, r, steps, warmup):
     gemm_ms = sum(a.elapsed_time(b) for a, b, _ in events)
     gemm_flop = sum(f for _, _, f in events)
     proj, qk = flops(L.wk, r)
+    diag = {}
+    run_step(L, r, diag=diag)                 # untimed: the retained-energy diagnostic
+    torch.cuda.synchronize()
     return {
         "r": r, "ms_per_step": ms, "wall_s": wall,
         "tflops": (proj + qk) / (ms * 1e-3) / 1e12,
@@ -263,6 +275,7 @@ def time_ratio(L, r, steps, warmup):
         "gemm_tflops": gemm_flop / (gemm_ms * 1e-3) / 1e12,
         "gemm_avg_us": gemm_ms * 1e3 / max(len(events), 1),
         "gemm_avg_gflop": gemm_flop / max(len(events), 1) / 1e9,
+        "retained_energy": {n: round(v, 5) for n, v in diag.items()},
     }
 
 

@@ -162,6 +162,24 @@ rmm_status_t rmm_select_tokens(const void *X, rmm_dtype_t dtype, int64_t B, int6
                                int64_t ldx, int64_t k, int32_t *idx, hipStream_t stream);
 
 /*
+ * Index-list check   (Sec. 3.2: I is a subset of [d] of size k; the gathered
+ * products take any such list, e.g. the static variant or the random
+ * selection that Sec. 4 "Baselines" compares against, as caller-made lists).
+ *
+ * bad[b] = 0 when idx[b*k .. b*k + k) is strictly ascending with every value
+ * in [0, K) -- the precondition of rmm_reduced_gemm, rmm_reduced_gemm_kmajor,
+ * rmm_reduced_gemv, rmm_reduced_qk and the attention entry points -- else
+ * 1 + the first position t that breaks it (idx[t] outside [0, K) or
+ * idx[t] <= idx[t-1]).  Lists made by rmm_select / rmm_select_tokens always
+ * pass.
+ * idx : int32 [B*k] (device).   bad : int32 [B] (device), written.
+ * Errors: INVALID_ARGUMENT for null pointers, B, k or K < 1, k > K or
+ *         K > INT32_MAX; UNSUPPORTED for B > INT32_MAX.
+ */
+rmm_status_t rmm_check_indices(const int32_t *idx, int64_t B, int64_t k, int64_t K, int32_t *bad,
+                               hipStream_t stream);
+
+/*
  * Gathered reduced product   (Sec. 3.2: RMM = A[:, I] B[I, :]; Sec. 3.3
  * projections Y~ = X[:, I] W[I, :]).
  *

@@ -59,6 +59,7 @@ _SIGS = {
                                       _i64, _i64, _p, _p, _p, ctypes.c_size_t, _p]),
     "rmm_attention_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64, _i64, _i64]),
     "rmm_gemm_swiglu_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64]),
+    "rmm_check_indices": (ctypes.c_int, [_p, _i64, _i64, _i64, _p, _p]),
     "rmm_reduced_gemm_swiglu_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64,
                                                       _i64, _i64, _p, _i64, _p, _p,
                                                       ctypes.c_size_t, _p]),
@@ -229,6 +230,25 @@ def rmm_reduced_gemm(X: torch.Tensor, W: torch.Tensor, idx: torch.Tensor, Y: tor
         X.data_ptr(), W.data_ptr(), idx.data_ptr(), _dtype_code(X), B, M, N, K, k, ldx, ldw,
         Y.data_ptr(), ldy, _stream(d, stream)))
     return Y
+
+
+def rmm_check_indices(idx: torch.Tensor, K: int, bad: torch.Tensor | None = None,
+                      stream=None) -> torch.Tensor:
+    """Per unit of idx [B, k]: 0 if its list is strictly ascending within
+    [0, K), else 1 + the first position that breaks it (int32 [B])."""
+    if idx.dim() == 1:
+        idx = idx.unsqueeze(0)
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.dim() != 2:
+        raise ValueError("idx must be contiguous int32 [B, k]")
+    B, k = idx.shape
+    if bad is None:
+        bad = torch.empty(B, dtype=torch.int32, device=idx.device)
+    d = _dev(idx, bad)
+    if bad.dtype != torch.int32 or bad.numel() != B or not bad.is_contiguous():
+        raise ValueError("bad must be contiguous int32 [B]")
+    _check("rmm_check_indices", lib.rmm_check_indices(idx.data_ptr(), B, k, int(K), bad.data_ptr(),
+                                                      _stream(d, stream)))
+    return bad
 
 
 def rmm_select_tokens(X: torch.Tensor, k: int, idx: torch.Tensor, stream=None) -> torch.Tensor:

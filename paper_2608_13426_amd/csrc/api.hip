@@ -138,6 +138,14 @@ rmm_status_t rmm_select(const double *energy, int64_t B, int64_t K, int64_t k, i
     return from_hip(rmm::launch_select(energy, B, K, k, idx, stream));
 }
 
+rmm_status_t rmm_check_indices(const int32_t *idx, int64_t B, int64_t k, int64_t K, int32_t *bad,
+                               hipStream_t stream) {
+    if (!idx || !bad) return RMM_ERR_INVALID_ARGUMENT;
+    if (B < 1 || K < 1 || k < 1 || k > K || K > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (B > kInt32Max) return RMM_ERR_UNSUPPORTED;
+    return from_hip(rmm::launch_check_indices(idx, B, k, K, bad, stream));
+}
+
 rmm_status_t rmm_reduced_gemm(const void *X, const void *W, const int32_t *idx, rmm_dtype_t dtype,
                               int64_t B, int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx,
                               int64_t ldw, void *Y, int64_t ldy, hipStream_t stream) {

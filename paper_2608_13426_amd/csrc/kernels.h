@@ -34,6 +34,10 @@ hipError_t launch_select_tokens(const void *X, bool bf16, int64_t B, int64_t K, 
                                 int64_t k, int32_t *idx, hipStream_t stream);
 hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
                          int32_t *idx, hipStream_t stream);
+// bad[b]: 0 if unit b's list is strictly ascending within [0, K), else 1 + the
+// first position that breaks it
+hipError_t launch_check_indices(const int32_t *idx, int64_t B, int64_t k, int64_t K, int32_t *bad,
+                                hipStream_t stream);
 
 // ------------------------------------------------------- gathered GEMM
 hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx,

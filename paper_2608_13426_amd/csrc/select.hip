@@ -356,7 +356,36 @@ hipError_t launch_src(const void *src, int64_t ld, int64_t B, int64_t K, int64_t
     return launch<1024, 1, false, SRC>(src, ld, B, K, k, cpt, idx, stream);
 }
 
+// bad[b] = 0 when unit b's list idx[b*k .. b*k+k) is strictly ascending with
+// every value in [0, K), else 1 + the first position t that breaks it
+// (idx[t] out of range, or idx[t] <= idx[t-1]).  Integer work: the first
+// position is an integer minimum over the threads, order-free.
+__global__ __launch_bounds__(256) void check_indices_kernel(const int32_t *__restrict__ idx,
+                                                            int64_t k, int32_t K,
+                                                            int32_t *__restrict__ bad) {
+    __shared__ int first;
+    const int32_t *I = idx + static_cast<int64_t>(blockIdx.x) * k;
+    if (threadIdx.x == 0) first = 0x7fffffff;
+    __syncthreads();
+    for (int64_t t = threadIdx.x; t < k; t += 256) {
+        const int32_t v = I[t];
+        if (v < 0 || v >= K || (t > 0 && I[t - 1] >= v)) {
+            atomicMin(&first, static_cast<int>(t));      // t grows along a thread's loop
+            break;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) bad[blockIdx.x] = first == 0x7fffffff ? 0 : first + 1;
+}
+
 }  // namespace
+
+hipError_t launch_check_indices(const int32_t *idx, int64_t B, int64_t k, int64_t K, int32_t *bad,
+                                hipStream_t stream) {
+    hipLaunchKernelGGL(check_indices_kernel, dim3(static_cast<unsigned>(B)), dim3(256), 0, stream,
+                       idx, k, static_cast<int32_t>(K), bad);
+    return hipGetLastError();
+}
 
 hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
                          int32_t *idx, hipStream_t stream) {

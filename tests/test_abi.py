@@ -296,6 +296,22 @@ def test_gemm_swiglu_workspace_size():
     assert rmm.rmm_gemm_swiglu_workspace_size(0, 8, 128) == 0
 
 
+def test_check_indices_validation():
+    f = rmm.lib.rmm_check_indices
+    base = [P, 2, 8, 16, P, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    assert call(0, NULL) == INVALID
+    assert call(4, NULL) == INVALID
+    for i, v in ((1, 0), (2, 0), (3, 0), (2, 17), (3, 2 ** 31)):
+        assert call(i, v) == INVALID
+    assert call(1, 2 ** 31) == UNSUPPORTED
+
+
 def test_linear_validation():
     f = rmm.lib.rmm_linear
     need = rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 64, 128, 64)

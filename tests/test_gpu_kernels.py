@@ -452,3 +452,41 @@ def test_linear_is_deterministic():
         rmm.rmm_linear(Xd, Wd, 0.5, Y)
         outs.append(Y.view(torch.int16).clone())
     assert all(torch.equal(outs[0], o) for o in outs[1:])
+
+
+def _first_break(lst, K):
+    """1 + the first position of a list that is not strictly ascending within [0, K), else 0."""
+    for t, v in enumerate(lst):
+        if v < 0 or v >= K or (t > 0 and lst[t - 1] >= v):
+            return t + 1
+    return 0
+
+
+@pytest.mark.parametrize("K,k", [(1000, 300), (40000, 12345), (7, 7), (1, 1)])
+def test_check_indices(K, k):
+    """rmm_check_indices on valid lists (sorted random subsets and the
+    library's own TopK lists) and on lists with planted defects at the first,
+    a middle and the last position."""
+    dev = require_gpu()
+    rng = np.random.default_rng(K + k)
+    B = 8
+    lists = np.stack([np.sort(rng.choice(K, k, replace=False)) for _ in range(B)]).astype(np.int32)
+    if k > 1:
+        lists[1, 0] = -1                         # below range at t = 0
+        lists[2, k - 1] = K                      # past range at the end
+        m = k // 2
+        lists[3, m] = lists[3, m - 1]            # duplicate in the middle
+        lists[4, m - 1], lists[4, m] = lists[4, m], lists[4, m - 1]   # descending pair
+        lists[5, m] = K + 7                      # out of range, then a later defect too
+        lists[5, k - 1] = lists[5, k - 2]
+    else:
+        lists[1, 0] = K
+    want = np.array([_first_break(list(l), K) for l in lists], dtype=np.int32)
+    bad = rmm.rmm_check_indices(torch.from_numpy(lists).to(dev), K)
+    assert np.array_equal(bad.cpu().numpy(), want)
+    assert want[0] == 0 and (k == 1 or np.all(want[1:6] > 0))
+    # the library's own selections always pass
+    e = torch.from_numpy(rng.standard_normal(B * K) ** 2).to(dev)
+    sel = torch.empty(B * k, dtype=torch.int32, device=dev)
+    rmm.rmm_select(e, k, sel)
+    assert int(rmm.rmm_check_indices(sel.view(B, k), K).abs().sum()) == 0
