@@ -166,3 +166,20 @@ def test_layer_8b_chain():
     check_product(from_device(Y[torch.from_numpy(rows).to(dev)]), Y_ref, absprod, k, "bf16")
     del O, Ot, e, Y
     torch.cuda.empty_cache()
+
+
+def test_attn_4k_kmajor():
+    """The 4k attention shape (32 heads, no GQA, heavy-tailed head dims,
+    causal) at r = 0.5: the K-major copy equals the block's output, the
+    energies are exact to float64 rounding."""
+    dev = require_gpu()
+    wk = wl.WORKLOADS["attn_4k"]
+    a = wk.attention
+    q, kk = wl.workload_qk(wk)
+    qb, kb = wl.f32_to_bf16_bits(q), wl.f32_to_bf16_bits(kk)
+    vb = wl.f32_to_bf16_bits(wl.workload_v(wk))
+    del q, kk
+    Q = wl.decode(qb, "bf16").reshape(1, a.H, a.L, a.D)
+    idx = _head_sets(Q, 1, a.H, ro.retained_count(0.5, a.D))
+    O, Ot, e = _both(dev, qb, kb, vb, idx, 1, a.H, a.Hkv, a.L, a.L, a.causal, 8)
+    _check_layout_and_energies(O, Ot, e, 1, a.H, a.L, 8)

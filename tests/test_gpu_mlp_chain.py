@@ -204,3 +204,19 @@ def test_layer_8b_mlp_chain():
     rows = np.array(sorted({0, 1, 255, 256, M - 1} | set(int(v) for v in rng.choice(M, 19, replace=False))))
     _run_chain(dev, X, Xbits, Wg, Wu, Wgbits, Wubits, 0.5, 0, rows=rows, down=(Wd, Wdbits, 0.5))
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("r", [0.25, 0.5, 0.75, 1.0])
+def test_mlp_1b_chain(r):
+    """The 1B-class MLP shapes (2048 tokens, 2048 -> 2 x 8192 -> 2048) at every
+    ratio of the sweep, with every row of H against the oracle."""
+    dev = require_gpu()
+    wk = wl.WORKLOADS["mlp_1b"]
+    Xbits = wl.f32_to_bf16_bits(wl.workload_input(wk, "mlp_in"))
+    X = wl.decode(Xbits, "bf16").astype(np.float64)[None]
+    proj = {p.name: p for p in wk.projections}
+    Wgbits = wl.f32_to_bf16_bits(wl.workload_weight(wk, proj["gate"]))
+    Wubits = wl.f32_to_bf16_bits(wl.workload_weight(wk, proj["up"]))
+    Wdbits = wl.f32_to_bf16_bits(wl.workload_weight(wk, proj["down"]))
+    Wg, Wu, Wd = (wl.decode(w, "bf16").astype(np.float64) for w in (Wgbits, Wubits, Wdbits))
+    _run_chain(dev, X, Xbits, Wg, Wu, Wgbits, Wubits, r, 0, down=(Wd, Wdbits, r))
