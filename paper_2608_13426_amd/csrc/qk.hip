@@ -124,42 +124,45 @@ __global__ __launch_bounds__(WM *WN *kWave) void qk_bf16_kernel(
 }
 
 // ------------------------------------------------------- row-streaming kernel
-// One workgroup per (head, 128-query tile) walks the key tiles of its rows.
+// One workgroup per (head, 128-query tile) walks the key tiles (BT keys:
+// 128 with 4 waves, or 256 with 8 waves) of its rows.
 // Q and K rows (D values, 16-byte chunks) are read whole and staged in LDS
 // with an odd row stride of D/2+1 words, so 32 rows read at one column hit
 // 32 distinct banks; the MFMA operands are gathered from the staged rows at
 // the retained dims (a zeroed pad word stands in for padding positions).
-// Q's fragments are gathered once and kept in registers.  The four waves
-// split the 128x128 tile into KW = 4/WQ key strips and WQ query strips: with
-// few retained dims (KSMAX k-steps) one strip of 32 keys per wave against all
-// 128 queries, so no K fragment is gathered twice; with more, 2x2 strips keep
-// Q's register footprint in bounds.  The product is
+// Q's fragments are gathered once and kept in registers.  The waves split
+// the 128 x BT tile into KW key strips and WQ query strips: with few retained
+// dims (KSMAX k-steps) one strip of 32 keys per wave against all 128
+// queries, so no K fragment is gathered twice; with more, two query strips
+// keep Q's register footprint in bounds.  The product is
 // formed transposed (keys x queries), so each lane holds 4 consecutive keys
 // of one query; tiles are staged through LDS and written as coalesced
-// 16-byte non-temporal stores.  Key tiles wholly above the diagonal are
-// streamed as -inf.
+// 16-byte stores, BT*2-byte row pieces (the longer pieces of the 256-key
+// tiles write faster).  Key tiles wholly above the diagonal are streamed
+// as -inf.
 namespace rowk {
-constexpr int BQ = 128, BT = 128, NT = 256;
-constexpr int OS = BT + 8;    // staged output row: 272 bytes (16-byte aligned)
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+constexpr int BQ = 128;       // queries per block
 // cache policy of the score stores (sc1).  Streaming (nt) stores measured
 // about 25% slower for this pattern of 256-byte row pieces 2*Lk bytes apart.
 constexpr int kStoreAux = 16;
 }  // namespace rowk
 
-template <int D, int KSMAX, int WQ>
-__global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
+template <int D, int KSMAX, int WQ, int NTT, int BTT>
+__global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Kc,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ S, int H, int Hkv, int Lq, int Lk,
     int k, float scale, int causal) {
-    using namespace rowk;
+    constexpr int BQ = rowk::BQ, BT = BTT, NT = NTT;
+    constexpr int OS = BT + 8;             // staged output row (16-byte aligned)
+    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+    constexpr int kStoreAux = rowk::kStoreAux;
     constexpr int RW = D / 2 + 1;          // words per staged row (odd)
     constexpr int CH = D / 8;              // 16-byte chunks per row
     constexpr int PER_T = BT * CH / NT;    // chunks staged per thread
-    constexpr int KW = 4 / WQ;             // waves along keys
+    constexpr int KW = NT / 64 / WQ;       // waves along keys
     constexpr int FI = BT / KW / 32;       // 32-key fragments per wave
     constexpr int FJ = BQ / WQ / 32;       // 32-query fragments per wave
-    static_assert(D % 16 == 0 && BQ == BT && (BT * CH) % NT == 0, "shape");
+    static_assert(D % 16 == 0 && BT % BQ == 0 && (BT * CH) % NT == 0, "shape");
     static_assert(KSMAX * 16 <= D && (WQ == 1 || WQ == 2), "shape");
 
     __shared__ uint32_t rows_lds[BT * RW];
@@ -181,7 +184,8 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
         const int limit = min(q0 + BQ, Lq) - 1 + off;   // largest key any row keeps
         n_compute = limit < 0 ? 0 : min(n_tiles, limit / BT + 1);
     }
-    const int r16 = tid >> 4, c16 = tid & 15;           // store role: rows r16 + 16i, chunk c16
+    constexpr int CPR = BT / 8, RPP = NT / CPR;        // 16-byte chunks per row piece, rows per pass
+    const int r16 = tid / CPR, c16 = tid % CPR;         // store role: rows r16 + RPP*i, chunk c16
     // the block's rows of S; rows at or past Lq fall outside the range and are dropped
     const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
         Sh + static_cast<int64_t>(q0) * Lk, 0, static_cast<uint32_t>(min(BQ, Lq - q0) * Lk * 2),
@@ -301,8 +305,8 @@ __global__ __launch_bounds__(rowk::NT, 2) void qk_bf16_rows_kernel(
                 }
             lds_barrier();
 #pragma unroll
-            for (int i = 0; i < BQ / 16; ++i) {
-                const int r = r16 + 16 * i;
+            for (int i = 0; i < BQ / RPP; ++i) {
+                const int r = r16 + RPP * i;
                 const int col = kt * BT + c16 * 8;
                 // unconditional (a column past Lk goes out of range): a branch
                 // here would make the compiler's wait for the next K rows also
@@ -400,9 +404,15 @@ hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *
         dim3 grid(static_cast<unsigned>((Lq + rowk::BQ - 1) / rowk::BQ),
                   static_cast<unsigned>(batch * H));
         // up to 64 retained dims: one key strip per wave; more: 2x2 strips
-        auto kern = D == 64 ? qk_bf16_rows_kernel<64, 4, 1>
-                  : k <= 64 ? qk_bf16_rows_kernel<128, 4, 1> : qk_bf16_rows_kernel<128, 8, 2>;
-        hipLaunchKernelGGL(kern, grid, dim3(rowk::NT), 0, stream, Q, Kc, idx, S,
+        // up to 96 retained dims: 256-key tiles, one 8-wave block per CU, so
+        // that every stored row piece is 512 bytes; more dims: 128-key tiles,
+        // two 4-wave blocks per CU (the heavier product overlaps better)
+        const bool wide = D == 128 && k <= 96;
+        auto kern = D == 64 ? qk_bf16_rows_kernel<64, 4, 1, 256, 128>
+                  : k <= 64 ? qk_bf16_rows_kernel<128, 4, 1, 512, 256>
+                  : k <= 96 ? qk_bf16_rows_kernel<128, 8, 2, 512, 256>
+                            : qk_bf16_rows_kernel<128, 8, 2, 256, 128>;
+        hipLaunchKernelGGL(kern, grid, dim3(wide ? 512 : 256), 0, stream, Q, Kc, idx, S,
                            static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
                            static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
         return hipGetLastError();
