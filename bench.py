@@ -654,7 +654,13 @@ def main():
     import paper_2608_13426_amd  # noqa: F401  (fails loudly without librmm.so)
     import workloads as wl
     dev = torch.device("cuda:0")
+    if args.workload not in wl.WORKLOADS:
+        sys.exit(f"unknown workload {args.workload!r}; known: {', '.join(sorted(wl.WORKLOADS))}")
     wk = wl.WORKLOADS[args.workload]
+    if wk.attention is None or wk.dtype != "bf16" or \
+            {"attn_in", "o_in", "mlp_in", "down_in"} - set(wk.inputs):
+        sys.exit(f"bench.py times a whole bf16 decoder layer (layer_8b, layer_70b); "
+                 f"{args.workload!r} is a parity-test workload")
     ratios = [float(x) for x in args.ratios.split(",")]
     if HEADLINE_R not in ratios:
         ratios.append(HEADLINE_R)
