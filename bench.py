@@ -75,13 +75,13 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
 # per-kv-head launches, smaller grids, excluded).  Each figure is valid only for the
 # source whose SHA-256 is recorded and for the same launch mix.
 GEMM_TRAFFIC = {"source": GEMM_SOURCE,
-                "sha256": "9e6a6e7fbc20e617e25077398ad072c3e3f5e8c7bed153fdc04bf8187a35e8ea",
+                "sha256": "2a169138d50d7b30535ec331cb40c027f53f3cff503b007020141cef08f61886",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
                 "bytes": round((399414.80 * 2.0 + 172304.08) * 1024)}
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"source": os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "attn.hip"),
-                "sha256": "f4a53d4153da9d1ff39649ac233eecb57ba5203c0f904b339ae0d8a47761fd72",
+                "sha256": "0a90ce58f6afdaf6cca061def81dbdd3b0d28a0cdcc29eaac7532da4dd7c5563",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0",
                 "bytes": round((103398.442 * 2.0 + 65545.42 + 8249.01 * 2.0 + 40960.00) * 1024)}
 
@@ -313,6 +313,24 @@ def time_attention(L, r, steps, warmup):
             "retained_tflops": flop / (ms * 1e-3) / 1e12, "calls": steps}
 
 
+def time_calls(fn, steps, warmup):
+    """Average microseconds of `fn` (launches on the current stream): `warmup`
+    untimed calls, then `steps` calls each bracketed by HIP events."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    return sum(x.elapsed_time(y) for x, y in evs) / steps * 1e3
+
+
 def time_attention_chain(L, r, steps, warmup):
     """The attention block feeding the reduced output projection, both ways,
     at ratio r for the heads' and the projection's selections (the per-head
@@ -361,21 +379,7 @@ def time_attention_chain(L, r, steps, warmup):
         rmm.rmm_select(eo, ko, sel)
         rmm.rmm_reduced_gemm_kmajor(Xt, Wo, sel.view(1, ko), Yo)
 
-    def timed(fn):
-        for _ in range(warmup):
-            fn()
-        torch.cuda.synchronize()
-        evs = []
-        for _ in range(steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            evs.append((e0, e1))
-        torch.cuda.synchronize()
-        return sum(x.elapsed_time(y) for x, y in evs) / steps * 1e3
-
-    us_f, us_u, us_l = timed(fused), timed(unfused), timed(layout)
+    us_f, us_u, us_l = (time_calls(f, steps, warmup) for f in (fused, unfused, layout))
     return {"r": r, "k_heads": kq, "k_o": ko, "fused_us": us_f, "unfused_us": us_u,
             "layout_copy_us": us_l, "unfused_without_copy_us": us_u - us_l,
             "speedup": us_u / us_f, "speedup_without_copy": (us_u - us_l) / us_f, "calls": steps}
@@ -430,21 +434,7 @@ def time_mlp_chain(L, r, steps, warmup):
         rmm.rmm_select(eh, kd, sel)
         rmm.rmm_reduced_gemm_kmajor(Xtd, Wd, sel.view(1, kd), Yd)
 
-    def timed(fn):
-        for _ in range(warmup):
-            fn()
-        torch.cuda.synchronize()
-        evs = []
-        for _ in range(steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            evs.append((e0, e1))
-        torch.cuda.synchronize()
-        return sum(x.elapsed_time(y) for x, y in evs) / steps * 1e3
-
-    us_f, us_u, us_a = timed(fused), timed(unfused), timed(activation)
+    us_f, us_u, us_a = (time_calls(f, steps, warmup) for f in (fused, unfused, activation))
     flop = 2 * M * (2 * F) * k + 2 * M * wk.inputs["mlp_in"][0] * kd
     return {"r": r, "k_gate_up": k, "k_down": kd, "fused_us": us_f, "unfused_us": us_u,
             "activation_us": us_a, "unfused_without_activation_us": us_u - us_a,

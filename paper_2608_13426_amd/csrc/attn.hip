@@ -85,21 +85,6 @@ __device__ __forceinline__ float pair_sum(float x) {
     return x;
 #endif
 }
-// x of the lane whose index within the quad is given by the quad_perm
-// control CTRL (0xB1: lane ^ 1, 0x4E: lane ^ 2), for a float64 value
-template <int CTRL>
-__device__ __forceinline__ double quad_f64(double x) {
-#if defined(__HIP_DEVICE_COMPILE__)
-    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
-    const uint32_t lo = static_cast<uint32_t>(
-        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, 0xF, 0xF, false));
-    const uint32_t hi = static_cast<uint32_t>(
-        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, 0xF, 0xF, false));
-    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
-#else
-    return x;
-#endif
-}
 }  // namespace attk
 
 // Ki[bh][t][j] = K[b][g][t][I_h[j]] for j < k, 0 for k <= j < 16*KS.
@@ -502,8 +487,8 @@ __global__ __launch_bounds__(attk::NT, 1) void attn_fwd_kernel(
                     }
                 }
             }
-            e += quad_f64<0xB1>(e);
-            e += quad_f64<0x4E>(e);
+            e += dpp_f64<0xB1>(e);
+            e += dpp_f64<0x4E>(e);
             if (qa == 0)
                 part[(static_cast<int64_t>(b) * nq + qt) * H * D + static_cast<int64_t>(h) * D + dd] = e;
         }

@@ -75,4 +75,21 @@ __device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rsrc, void *ld
 #endif
 }
 
+// x of the lane that the DPP control CTRL names within its row of 16 lanes
+// (0xB1: lane ^ 1, 0x4E: lane ^ 2, 0x141: the mirror within 8 lanes), for a
+// float64 value (two 32-bit moves); every lane must be active.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+    const uint32_t lo = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, 0xF, 0xF, false));
+    const uint32_t hi = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, 0xF, 0xF, false));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+#else
+    return x;
+#endif
+}
+
 }  // namespace rmm

@@ -525,22 +525,6 @@ __device__ __forceinline__ void wait_vmcnt_le() {
 }
 }  // namespace trk
 
-// x of the lane that the DPP control CTRL names (within a row of 16 lanes),
-// for a float64 value
-template <int CTRL>
-__device__ __forceinline__ double dpp_f64(double x) {
-#if defined(__HIP_DEVICE_COMPILE__)
-    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
-    const uint32_t lo = static_cast<uint32_t>(
-        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, 0xF, 0xF, false));
-    const uint32_t hi = static_cast<uint32_t>(
-        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, 0xF, 0xF, false));
-    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
-#else
-    return x;
-#endif
-}
-
 // bf16(bf16(silu(g)) * u) for bf16 g, u (bits in the low half); silu(g) =
 // g / (1 + e^-g) in fp32 with the hardware exp2 and reciprocal (each about
 // one ulp), far below the bf16 rounding that follows
