@@ -346,6 +346,8 @@ def test_reduced_gemm_strided_operands():
     ("bf16", 1, 4, 1, 130, 136, 128, 0.5, False, 10),  # k = 64: one key strip per wave
     ("bf16", 1, 2, 2, 300, 320, 64, 0.5, True, 11),
     ("bf16", 1, 2, 2, 256, 128, 128, 0.3, True, 12),   # Lq > Lk: leading rows fully masked
+    ("bf16", 2, 8, 2, 520, 520, 128, 0.5, True, 13),   # 256-key tiles: two and a tail of 8
+    ("bf16", 1, 4, 4, 1000, 1000, 128, 0.25, True, 14),  # k = 32, four 256-key tiles, ragged
     ("f32", 1, 4, 2, 100, 130, 128, 0.5, True, 6),
     ("f32", 1, 2, 2, 70, 70, 64, 1.0, False, 7),
 ])
