@@ -116,8 +116,7 @@ def test_chain_into_output_projection():
     sel, Y, k = _o_projection(dev, Ot, e, to_device(Ws, "bf16", dev), L, r)
     e_ref = ro.column_energies(Xo)
     sel_ref = ro.topk_indices(e_ref, k)
-    assert check_index_sets(sel.cpu().numpy()[None], sel_ref[None],
-                            [ro.selection_margin(e_ref, k)], L) == 0
+    assert check_index_sets(sel.cpu().numpy()[None], sel_ref[None], e_ref[None], L) == 0
     Y_ref = ro.reduced_matmul(Xo, W, sel_ref)
     absprod = np.abs(Xo[:, sel_ref]) @ np.abs(W[sel_ref])
     check_product(from_device(Y), Y_ref, absprod, k, "bf16")
@@ -157,8 +156,7 @@ def test_layer_8b_chain():
     sel, Y, k = _o_projection(dev, Ot, e, to_device(Wbits, "bf16", dev), a.L, r)
     e_ref = ro.column_energies(Xo)
     sel_ref = ro.topk_indices(e_ref, k)
-    assert check_index_sets(sel.cpu().numpy()[None], sel_ref[None],
-                            [ro.selection_margin(e_ref, k)], a.L) == 0
+    assert check_index_sets(sel.cpu().numpy()[None], sel_ref[None], e_ref[None], a.L) == 0
     rng = np.random.default_rng(8)
     rows = np.array(sorted({0, 1, 255, 256, a.L - 1} | set(int(v) for v in rng.choice(a.L, 27, replace=False))))
     Y_ref = ro.reduced_matmul(Xo[rows], W, sel_ref)

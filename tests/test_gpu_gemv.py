@@ -32,8 +32,8 @@ def _run(seed, B, M, N, K, r, pad=0, select_on_gpu=False):
         rmm.rmm_score(Xd, e, ws)
         idx = torch.empty(B * k, dtype=torch.int32, device=dev)
         rmm.rmm_select(e, k, idx)
-        margins = [ro.selection_margin(ro.column_energies(X[b]), k) for b in range(B)]
-        assert check_index_sets(idx.cpu().numpy().reshape(B, k), idx_ref, margins, M,
+        e_ref = np.stack([ro.column_energies(X[b]) for b in range(B)])
+        assert check_index_sets(idx.cpu().numpy().reshape(B, k), idx_ref, e_ref, M,
                                 exact_sums=(M == 1)) == 0
     else:
         idx = torch.from_numpy(idx_ref.astype(np.int32)).to(dev)
@@ -113,12 +113,11 @@ def test_layer_8b_decode(B):
             idx = torch.empty(B * k, dtype=torch.int32, device=dev)
             rmm.rmm_select(e, k, idx)
             idx_ref = np.stack([ro.topk_indices(e_ref[b], k) for b in range(B)])
-            margins = [ro.selection_margin(e_ref[b], k) for b in range(B)]
             idx_np = idx.cpu().numpy().reshape(B, k)
             # a single token's energies are exact squares of bf16 values:
             # exact ties are common and resolve to the lower index on both
             # sides, so every set must match bit for bit
-            check_index_sets(idx_np, idx_ref, margins, 1, exact_sums=True)
+            check_index_sets(idx_np, idx_ref, np.stack(e_ref), 1, exact_sums=True)
             rmm.rmm_reduced_gemv(Xd, Wd, idx.view(B, k), Y)
             Yg = from_device(Y)
             for b in range(B):

@@ -45,8 +45,8 @@ def _run(seed, batch, H, Hkv, Lq, Lk, D, r, dtype, causal, pad=0):
     ig = idx.cpu().numpy().reshape(batch * H, kt)
     for b in range(batch):
         O_ref, idx_ref = ro.reduced_pv(P[b], V[b], kt)
-        margins = [ro.selection_margin(ro.column_energies(P[b, h]), kt) for h in range(H)]
-        check_index_sets(ig[b * H:(b + 1) * H], idx_ref, margins, Lq)
+        e_ref = np.stack([ro.column_energies(P[b, h]) for h in range(H)])
+        check_index_sets(ig[b * H:(b + 1) * H], idx_ref, e_ref, Lq)
         for h in range(H):
             g = ro.gqa_kv_head(h, H, Hkv)
             T = idx_ref[h]
@@ -91,3 +91,50 @@ def test_reduced_pv_is_deterministic_and_matches_steps():
                              idx3.view(H, kt)[2 * g:2 * g + 2].contiguous(), O3[0, 2 * g:2 * g + 2])
     a, b = O.float(), O3.float()
     assert torch.max(torch.abs(a - b)).item() <= 2.0 ** -7 * torch.max(torch.abs(b)).item()
+
+
+def _sample_rows(L, n, seed):
+    rng = np.random.default_rng(seed)
+    fixed = {0, 1, 255, 256, L // 2, L - 2, L - 1}
+    return np.array(sorted(fixed | set(int(v) for v in rng.choice(L, size=n, replace=False))))
+
+
+def test_layer_8b_reduced_pv():
+    """The 8B attention shape the benchmark times (32 query / 8 kv heads,
+    8192 tokens, D = 128, causal attention weights): every head's token set
+    bit-exact against the oracle, and every head's output on sampled query
+    rows, at rho_t = 0.25, 0.5 and 1."""
+    from tests import oracle_pool
+    dev = require_gpu()
+    wk = wl.WORKLOADS["layer_8b"]
+    a = wk.attention
+    H, Hkv, L, D = a.H, a.Hkv, a.L, a.D
+    print(f"P [{H} x {L} x {L}] causal weights, V [{Hkv} x {L} x {D}]", flush=True)
+    Pb = wl.attention_score_bits((wk.seed, 203), H, L, L, True, softmax=True)
+    Vb = wl.f32_to_bf16_bits(wl.workload_v(wk))
+    V = wl.decode(Vb, "bf16").astype(np.float64)
+    Pd = torch.from_numpy(Pb.view(np.int16)).to(dev).view(torch.bfloat16).reshape(1, H, L, L)
+    Vd = torch.from_numpy(Vb.view(np.int16)).to(dev).view(torch.bfloat16).reshape(1, Hkv, L, D)
+    e_ref = np.stack([oracle_pool.column_energies(Pb[h], bf16_bits=True) for h in range(H)])
+    rows = _sample_rows(L, 17, 203)
+    rows_d = torch.from_numpy(rows).to(dev)
+    Pr = wl.decode(Pb[:, rows], "bf16").astype(np.float64)          # [H, rows, L]
+    O = torch.empty((1, H, L, D), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(rmm.rmm_workspace_size(rmm.RMM_OP_PV, H, L, L, L), dtype=torch.uint8, device=dev)
+    for r in (0.25, 0.5, 1.0):
+        kt = ro.retained_count(r, L)
+        idx = torch.empty(H * kt, dtype=torch.int32, device=dev)
+        O.fill_(float("nan"))
+        rmm.rmm_reduced_pv(Pd, Vd, kt, O, idx_out=idx, workspace=ws)
+        idx_ref = np.stack([ro.topk_indices(e_ref[h], kt) for h in range(H)])
+        assert check_index_sets(idx.cpu().numpy(), idx_ref, e_ref, L) == 0
+        Og = from_device(O[0][:, rows_d])
+        for h in range(H):
+            g = ro.gqa_kv_head(h, H, Hkv)
+            T = idx_ref[h]
+            ref = ro.reduced_matmul(Pr[h], V[g], T)
+            absprod = np.abs(Pr[h][:, T]) @ np.abs(V[g][T])
+            check_product(Og[h], ref, absprod, kt, "bf16")
+        print(f"rho_t={r}: kt={kt} ok", flush=True)
+    del Pd, Vd, O, ws
+    torch.cuda.empty_cache()

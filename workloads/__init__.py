@@ -32,6 +32,7 @@ __all__ = [
     "f32_to_bf16_bits", "bf16_bits_to_f32", "Projection", "AttentionShape",
     "Workload", "WORKLOADS", "rng_for", "activation", "weight",
     "heavy_tailed_heads", "outlier_heads", "encode", "decode",
+    "attention_score_bits",
 ]
 
 
@@ -163,6 +164,65 @@ def outlier_heads(key, H: int, L: int, D: int, frac: float, scale: float) -> np.
         for c in rng_for(*key).choice(H * D, size=n_out, replace=False):
             z[c // D, :, c % D] *= np.float32(scale)
     return z
+
+
+_SCORE_ROWS = 256
+
+
+def _score_block(key, b_h, h: int, r0: int, r1: int, Lq: int, causal: bool,
+                 spread: float) -> np.ndarray:
+    """Rows r0..r1-1 of head h's synthetic scores (float32), one PCG64 stream
+    per (key, head, row block)."""
+    g = np.random.Generator(np.random.PCG64([*key, h, r0 // _SCORE_ROWS]))
+    s = g.standard_normal(size=(r1 - r0, b_h.shape[0]), dtype=np.float32)
+    s *= np.float32(spread)
+    s += b_h[None, :]
+    if causal:
+        Lk = b_h.shape[0]
+        t = np.arange(Lk)[None, :]
+        i = np.arange(r0, r1)[:, None]
+        s[t > i + (Lk - Lq)] = -np.inf
+    return s
+
+
+def attention_score_bits(key, H: int, Lq: int, Lk: int, causal: bool, spread: float = 2.0,
+                         nu: float = 3.0, softmax: bool = False) -> np.ndarray:
+    """bf16 bits [H x Lq x Lk] of synthetic attention scores, or (with
+    ``softmax``) of the attention weights made from them.
+
+    Scores: ``spread * z + b[h, t]`` with z ~ N(0, 1) per entry and a
+    per-(head, key) salience ``b = |Student-t(nu)|`` (a few keys draw much of
+    every query's weight, as attention sinks do); with ``causal`` the entries
+    t > i + (Lk - Lq) are -inf.  Weights: the row softmax of those float32
+    scores, computed in float32 (masked entries 0).  Made on the host from
+    seeded draws in blocks of 256 rows, each from its own PCG64 stream."""
+    b = np.abs(rng_for(*key).standard_t(nu, size=(H, Lk))).astype(np.float32)
+    out = np.empty((H, Lq, Lk), dtype=np.uint16)
+
+    def block(job):
+        h, r0 = job
+        r1 = min(Lq, r0 + _SCORE_ROWS)
+        s = _score_block(key, b[h], h, r0, r1, Lq, causal, spread)
+        if softmax:
+            m = s.max(axis=1, keepdims=True)
+            m[~np.isfinite(m)] = 0.0                 # rows with every key masked
+            s -= m
+            np.exp(s, out=s)
+            tot = s.sum(axis=1, keepdims=True)
+            tot[tot == 0] = 1.0
+            s /= tot
+        out[h, r0:r1] = _bits_serial(s)
+
+    list(_POOL.map(block, [(h, r0) for h in range(H) for r0 in range(0, Lq, _SCORE_ROWS)]))
+    return out
+
+
+def _bits_serial(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits by round-to-nearest-even for finite values and +-inf
+    (no NaN handling: the score recipes hold none)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u.astype(np.uint64) + 0x7FFF + ((u >> np.uint32(16)) & np.uint32(1))) >> 16
+    return r.astype(np.uint16)
 
 
 # ---------------------------------------------------------------------------
