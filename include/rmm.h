@@ -46,7 +46,8 @@ typedef enum rmm_status {
     RMM_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, r outside (0,1], ... */
     RMM_ERR_UNSUPPORTED = 2,        /* valid but not implemented (dtype, alignment) */
     RMM_ERR_WORKSPACE_TOO_SMALL = 3,
-    RMM_ERR_HIP = 4                 /* a HIP launch failed (no device, bad stream) */
+    RMM_ERR_HIP = 4,                /* a HIP launch failed (no device, bad stream) */
+    RMM_ERR_TOO_LARGE = 5           /* exceeds the fixed scratch of rmm_linear_noalloc */
 } rmm_status_t;
 
 typedef enum rmm_dtype {
@@ -427,6 +428,38 @@ rmm_status_t rmm_reduced_pv(const void *P, const void *V, rmm_dtype_t dtype, int
                             int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
                             int64_t ldp, int64_t kt, void *O, int32_t *idx_out,
                             void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * rmm_linear without a caller workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc.
+ *
+ * Computes exactly what rmm_linear computes (the same kernels in the same
+ * order: bit-identical Y and index sets), with the workspace taken from a
+ * fixed device array inside the library instead of the caller's buffer.
+ * That array holds rmm_noalloc_scratch_bytes() = 64 MiB on every GPU the
+ * library runs on, from the first call on that GPU until the process ends;
+ * the call itself allocates nothing (no hipMalloc, no hipFree, no library
+ * routine that allocates).  rmm_workspace_size(RMM_OP_LINEAR, B, M, K, k)
+ * must not exceed it (e.g. M*K up to about 30 million bf16 activations for
+ * one unit).  Nothing in the array needs to start at zero: every byte a
+ * call reads was written earlier in the same call.
+ *
+ * Every call on one GPU uses that GPU's one array, so calls that overlap in
+ * time on one GPU (concurrent streams, or host threads) race and give
+ * undefined results; serialise them (one stream, or events).  `stream` must
+ * belong to the current device (NULL = its legacy default stream).
+ *
+ * Arguments as rmm_linear, without the workspace.
+ * Errors: as rmm_linear; RMM_ERR_TOO_LARGE (before any HIP call) when the
+ *         workspace rmm_linear would need exceeds the array;
+ *         INVALID_ARGUMENT when `stream` belongs to another device.
+ */
+size_t rmm_noalloc_scratch_bytes(void);
+rmm_status_t rmm_linear_noalloc(const void *X, const void *W, double r, rmm_dtype_t dtype,
+                                int64_t B, int64_t M, int64_t N, int64_t K, int64_t ldx,
+                                int64_t ldw, void *Y, int64_t ldy, int32_t *idx_out,
+                                hipStream_t stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);

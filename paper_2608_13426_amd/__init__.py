@@ -21,7 +21,7 @@ __all__ = [
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
     "rmm_reduced_attention", "rmm_reduced_gemv", "rmm_gemv_workspace_size", "rmm_select_tokens",
-    "EXPORTED_SYMBOLS",
+    "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -48,6 +48,9 @@ _SIGS = {
     "rmm_linear": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
                                   _i64, _i64, _i64, _p, _i64, _p, _p, ctypes.c_size_t, _p]),
     "rmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "rmm_noalloc_scratch_bytes": (ctypes.c_size_t, []),
+    "rmm_linear_noalloc": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
+                                          _i64, _i64, _i64, _p, _i64, _p, _p]),
     "rmm_score_kmajor": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _p, _i64, _p,
                                         ctypes.c_size_t, _p]),
     "rmm_reduced_gemm_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64,
@@ -560,4 +563,33 @@ def rmm_linear(X: torch.Tensor, W: torch.Tensor, r: float, Y: torch.Tensor,
     _check("rmm_linear", lib.rmm_linear(
         X.data_ptr(), W.data_ptr(), float(r), _dtype_code(X), B, M, N, K, ldx, ldw,
         Y.data_ptr(), ldy, _ptr(idx_out), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    return Y
+
+
+def rmm_noalloc_scratch_bytes() -> int:
+    return int(lib.rmm_noalloc_scratch_bytes())
+
+
+def rmm_linear_noalloc(X: torch.Tensor, W: torch.Tensor, r: float, Y: torch.Tensor,
+                       idx_out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """rmm_linear with the library's fixed scratch instead of a workspace:
+    neither this wrapper nor the call allocates device memory (usable under
+    HIP graph capture).  Calls that overlap in time on one GPU race."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, W, Y)
+    if W.dim() != 2 or W.shape[0] != K or W.stride(1) != 1:
+        raise ValueError("W must be [K, N] with contiguous rows")
+    N, ldw = W.shape[1], W.stride(0)
+    By, My, Ny, ldy = _rows(Y, "Y")
+    if (By, My, Ny) != (B, M, N):
+        raise ValueError("Y must be [B, M, N]")
+    if not (X.dtype == W.dtype == Y.dtype):
+        raise TypeError("X, W and Y must share one dtype")
+    k = rmm_retained_count(r, K)
+    if idx_out is not None and (idx_out.dtype != torch.int32 or idx_out.numel() != B * max(k, 0)
+                                or not idx_out.is_contiguous()):
+        raise ValueError("idx_out must be contiguous int32 [B, k]")
+    _check("rmm_linear_noalloc", lib.rmm_linear_noalloc(
+        X.data_ptr(), W.data_ptr(), float(r), _dtype_code(X), B, M, N, K, ldx, ldw,
+        Y.data_ptr(), ldy, _ptr(idx_out), _stream(d, stream)))
     return Y

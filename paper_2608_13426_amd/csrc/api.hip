@@ -425,6 +425,7 @@ const char *rmm_status_string(rmm_status_t status) {
     case RMM_ERR_UNSUPPORTED: return "unsupported argument combination";
     case RMM_ERR_WORKSPACE_TOO_SMALL: return "workspace missing or too small";
     case RMM_ERR_HIP: return "HIP launch failed";
+    case RMM_ERR_TOO_LARGE: return "problem exceeds the library's fixed scratch buffer";
     }
     return "unknown status";
 }

@@ -16,7 +16,7 @@ from oracle import rmm_oracle
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "rmm.h")
 
-OK, INVALID, UNSUPPORTED, WS_SMALL, HIP = 0, 1, 2, 3, 4
+OK, INVALID, UNSUPPORTED, WS_SMALL, HIP, TOO_LARGE = 0, 1, 2, 3, 4, 5
 P = ctypes.c_void_p(0x100000)          # a non-null pointer that is never dereferenced
 NULL = None
 
@@ -67,7 +67,7 @@ def test_workspace_sizes():
 
 
 def test_status_strings():
-    for code in range(5):
+    for code in range(6):
         s = rmm.rmm_status_string(code)
         assert isinstance(s, str) and s
     assert rmm.rmm_status_string(99) == "unknown status"
@@ -419,3 +419,30 @@ def test_select_tokens_validation():
     assert call(5, 0) == INVALID            # k
     assert call(5, 4097) == INVALID         # k > K
     assert call(4, 4095) == INVALID         # ldx < K
+
+
+def test_linear_noalloc_validation():
+    """Argument errors and the scratch limit are reported before any HIP call
+    (this container has no GPU: a call that reached the device would fail
+    with HIP instead)."""
+    f = rmm.lib.rmm_linear_noalloc
+    assert rmm.rmm_noalloc_scratch_bytes() == 64 << 20
+    base = [P, P, 0.5, 1, 1, 64, 32, 128, 128, 32, P, 32, NULL, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    assert call(2, 0.0) == INVALID
+    assert call(2, float("nan")) == INVALID
+    assert call(0, NULL) == INVALID
+    assert call(1, NULL) == INVALID
+    assert call(10, NULL) == INVALID
+    assert call(3, 7) == INVALID             # dtype
+    assert call(8, 100) == INVALID           # ldx < K
+    # 8192 x 4096 bf16 activations: the K-major copy alone is 64 MiB
+    big = [P, P, 0.5, 1, 1, 8192, 4096, 4096, 4096, 4096, P, 4096, NULL, NULL]
+    assert rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 8192, 4096, 2048) > (64 << 20)
+    assert f(*big) == TOO_LARGE
+    assert rmm.rmm_status_string(TOO_LARGE) == "problem exceeds the library's fixed scratch buffer"
