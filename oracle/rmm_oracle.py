@@ -32,6 +32,11 @@ Paper passages followed (arXiv 2608.13426, "Reduced Matrix Multiplication"):
 * The MLP activation between the reduced gate/up and down projections of
   the evaluated LLaMA-family models: silu(gate) * up (used to chain the
   projections; it is the models' own operation, not part of RMM).
+* The normalisation that produces the inputs of the attention and MLP
+  projections in those models, RMSNorm (again the models' own operation,
+  used to chain a producer into a reduced projection), and the attention
+  weights softmax(S + M) whose column norms Sec. 3.3 ranks for the
+  token-axis value product.
 * Appendix A, "Inference setup": the index set is recomputed per affected
   product from the current sequence's activation block (one selection per
   sequence; one per query head on the attention side).
@@ -64,7 +69,7 @@ import numpy as np
 __all__ = [
     "retained_count", "column_energies", "topk_indices", "reduced_matmul",
     "rmm", "rmm_batched", "gqa_kv_head", "reduced_qk", "rmm_qk", "reduced_attention",
-    "reduced_pv",
+    "reduced_pv", "silu", "swiglu", "rmsnorm", "attention_weights",
     "residual_energy", "retained_energy_fraction", "discarded_energy_ratio",
     "rank_one_bound", "factorized_bound", "normalized_bound",
     "selection_margin",
@@ -285,6 +290,41 @@ def silu(x: np.ndarray) -> np.ndarray:
 def swiglu(g: np.ndarray, u: np.ndarray) -> np.ndarray:
     """The down projection's input: silu(g) * u, elementwise, float64."""
     return silu(g) * np.asarray(u, dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# The producers of the reduced products' inputs
+# ---------------------------------------------------------------------------
+
+def rmsnorm(X: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:
+    """RMSNorm of each row of X [n x d] with weight gamma [d], float64:
+    y[i, j] = gamma[j] * X[i, j] / sqrt(mean_j X[i, j]^2 + eps).
+
+    The normalisation in front of the attention and MLP projections of the
+    LLaMA-family models the paper reduces (Sec. 4 setup, Sec. 3.3); its
+    output is the activation block X whose column norms Sec. 3.2 ranks."""
+    X = np.asarray(X, dtype=np.float64)
+    gamma = np.asarray(gamma, dtype=np.float64)
+    ms = np.array([math.fsum((X[i] * X[i]).tolist()) for i in range(X.shape[0])]) / X.shape[1]
+    return X / np.sqrt(ms + float(eps))[:, None] * gamma[None, :]
+
+
+def attention_weights(S: np.ndarray) -> np.ndarray:
+    """P = softmax(S + M) over the last axis, float64 (Sec. 3.3: the
+    attention weights whose column norms rank the tokens of the value
+    product).  Masked entries are -inf in S and get weight 0; a row with
+    every entry masked gets all zeros."""
+    S = np.asarray(S, dtype=np.float64)
+    P = np.zeros_like(S)
+    flat_S, flat_P = S.reshape(-1, S.shape[-1]), P.reshape(-1, S.shape[-1])
+    for i in range(flat_S.shape[0]):
+        s = flat_S[i]
+        keep = s != -np.inf
+        if not keep.any():
+            continue
+        w = np.exp(s[keep] - s[keep].max())
+        flat_P[i, keep] = w / math.fsum(w.tolist())
+    return P
 
 
 # ---------------------------------------------------------------------------

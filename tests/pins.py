@@ -463,6 +463,50 @@ def check_swiglu(o):
     assert np.allclose(o.swiglu(g, u), want, rtol=1e-15, atol=0)
 
 
+def check_rmsnorm(o):
+    # hand-worked: x = (3, 4), gamma = (1, 2), eps = 0: mean of squares 12.5,
+    # y = (3, 8) / sqrt(12.5)
+    y = o.rmsnorm(np.array([[3.0, 4.0]]), np.array([1.0, 2.0]), 0.0)
+    assert np.allclose(y, np.array([[3.0, 8.0]]) / math.sqrt(12.5), rtol=1e-15, atol=0)
+    # with gamma = 1 and eps = 0 every row has mean square exactly 1 (closed
+    # form), whatever its scale; rows are independent of each other
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((6, 10)) * np.array([1e-3, 1, 7, 50, 0.2, 3])[:, None]
+    Y = o.rmsnorm(X, np.ones(10), 0.0)
+    assert np.allclose((Y * Y).mean(axis=1), 1.0, rtol=1e-14, atol=0)
+    assert np.allclose(o.rmsnorm(X * 5.0, np.ones(10), 0.0), Y, rtol=1e-14, atol=0)
+    assert np.allclose(o.rmsnorm(X[3:4], np.ones(10), 0.0), Y[3:4], rtol=1e-15, atol=0)
+    # gamma scales columns (channels), not rows
+    g = np.arange(1.0, 11.0)
+    assert np.allclose(o.rmsnorm(X, g, 0.0), Y * g[None, :], rtol=1e-14, atol=0)
+    # eps sits inside the square root: a constant row c gives c / sqrt(c^2 + eps)
+    y = o.rmsnorm(np.full((1, 4), 2.0), np.ones(4), 5.0)
+    assert np.allclose(y, 2.0 / 3.0, rtol=1e-15, atol=0)
+    # an all-zero row stays zero (eps > 0)
+    assert np.array_equal(o.rmsnorm(np.zeros((1, 3)), np.ones(3), 1e-6), np.zeros((1, 3)))
+
+
+def check_attention_weights(o):
+    # two keys: the weights are the logistic function of the score gap
+    P = o.attention_weights(np.array([[0.0, math.log(3.0)]]))
+    assert np.allclose(P, [[0.25, 0.75]], rtol=1e-15, atol=0)
+    # each row sums to 1 over its kept keys, masked keys get exactly 0, and a
+    # row with every key masked is all zeros
+    S = np.array([[1.0, -np.inf, 2.0, 0.5], [-np.inf] * 4, [3.0, 3.0, 3.0, -np.inf]])
+    P = o.attention_weights(S)
+    assert P[0, 1] == 0.0 and P[2, 3] == 0.0 and np.array_equal(P[1], np.zeros(4))
+    assert np.allclose(P[[0, 2]].sum(axis=1), 1.0, rtol=1e-15, atol=0)
+    assert np.allclose(P[2, :3], 1.0 / 3.0, rtol=1e-15, atol=0)
+    e = np.exp([1.0, 2.0, 0.5])
+    assert np.allclose(P[0, [0, 2, 3]], e / e.sum(), rtol=1e-15, atol=0)
+    # shift invariance per row, and the normalisation runs over keys (last
+    # axis), not over queries
+    rng = np.random.default_rng(6)
+    S = rng.standard_normal((2, 3, 5))
+    assert np.allclose(o.attention_weights(S + 7.0), o.attention_weights(S), rtol=1e-13, atol=0)
+    assert np.allclose(o.attention_weights(S).sum(axis=-1), 1.0, rtol=1e-14, atol=0)
+
+
 def check_margin(o):
     assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
     assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
@@ -472,4 +516,4 @@ def check_margin(o):
 
 ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
               check_bounds, check_worked_example, check_qk, check_attention, check_pv,
-              check_swiglu, check_margin)
+              check_swiglu, check_rmsnorm, check_attention_weights, check_margin)

@@ -223,7 +223,56 @@ def _swiglu_swapped(g, u):
     return ro.silu(u) * np.asarray(g, dtype=np.float64)
 
 
+def _rms_sum(X, gamma, eps):          # sum of squares instead of the mean
+    X = np.asarray(X, dtype=np.float64)
+    return X / np.sqrt((X * X).sum(axis=1) + eps)[:, None] * np.asarray(gamma, dtype=np.float64)
+
+
+def _rms_eps_outside(X, gamma, eps):   # eps added after the square root
+    X = np.asarray(X, dtype=np.float64)
+    return X / (np.sqrt((X * X).mean(axis=1)) + eps)[:, None] * np.asarray(gamma, dtype=np.float64)
+
+
+def _rms_gamma_rows(X, gamma, eps):    # weight applied along rows
+    X = np.asarray(X, dtype=np.float64)
+    y = X / np.sqrt((X * X).mean(axis=1) + eps)[:, None]
+    g = np.asarray(gamma, dtype=np.float64)
+    return y * np.resize(g, X.shape[0])[:, None]
+
+
+def _rms_l1(X, gamma, eps):            # mean absolute value
+    X = np.asarray(X, dtype=np.float64)
+    return X / (np.abs(X).mean(axis=1) + eps)[:, None] * np.asarray(gamma, dtype=np.float64)
+
+
+def _aw_over_queries(S):               # normalised over the query axis
+    S = np.asarray(S, dtype=np.float64)
+    return np.swapaxes(ro_attention_weights(np.swapaxes(S, -1, -2)), -1, -2)
+
+
+def _aw_unnormalised(S):
+    S = np.asarray(S, dtype=np.float64)
+    m = np.max(np.where(np.isfinite(S), S, -1e300), axis=-1, keepdims=True)
+    return np.where(np.isfinite(S), np.exp(S - m), 0.0)
+
+
+def _aw_no_max(S):                     # no shift by the row max and no empty-row rule:
+    S = np.asarray(S, dtype=np.float64)  # a fully masked row divides 0 by 0
+    E = np.where(np.isfinite(S), np.exp(S), 0.0)
+    with np.errstate(invalid="ignore"):
+        return E / E.sum(axis=-1, keepdims=True)
+
+
+ro_attention_weights = ro.attention_weights
+
 MUTANTS = {
+    "rmsnorm_sum_not_mean": ("rmsnorm", _rms_sum),
+    "rmsnorm_eps_outside_sqrt": ("rmsnorm", _rms_eps_outside),
+    "rmsnorm_gamma_on_rows": ("rmsnorm", _rms_gamma_rows),
+    "rmsnorm_l1": ("rmsnorm", _rms_l1),
+    "weights_over_queries": ("attention_weights", _aw_over_queries),
+    "weights_unnormalised": ("attention_weights", _aw_unnormalised),
+    "weights_masked_row_nan": ("attention_weights", _aw_no_max),
     "silu_is_sigmoid": ("silu", _silu_sigmoid),
     "silu_sign": ("silu", _silu_sign),
     "swiglu_swapped": ("swiglu", _swiglu_swapped),
