@@ -116,6 +116,8 @@ def parse():
                    help="skip the timing of the MLP chain (fused and unfused)")
     p.add_argument("--no-policies", action="store_true",
                    help="skip the steps with per-component retention ratios")
+    p.add_argument("--no-norm-chain", action="store_true",
+                   help="skip the timing of the RMSNorm -> projection chains")
     p.add_argument("--no-pv", action="store_true",
                    help="skip the separate timing of the token-axis reduced value product")
     p.add_argument("--copy-probe-mib", type=int, default=0,
@@ -440,6 +442,69 @@ def time_mlp_chain(L, r, steps, warmup):
             "activation_us": us_a, "unfused_without_activation_us": us_u - us_a,
             "speedup": us_u / us_f, "speedup_without_activation": (us_u - us_a) / us_f,
             "retained_tflops_fused": flop / (us_f * 1e-6) / 1e12, "calls": steps}
+
+
+def time_norm_chain(L, name, r, steps, warmup, eps=1e-5):
+    """The normalisation in front of a projection group (attn_in: q|k|v,
+    mlp_in: gate|up) feeding its reduced GEMM at ratio r, both ways, with the
+    layer's activations standing in for the pre-norm hidden state:
+      fused   : rmm_rmsnorm_kmajor (one pass over X: the normalised rows
+                K-major and their column energies) -> TopK -> K-major GEMM;
+      unfused : torch RMSNorm (row-major normalised rows) -> rmm_score_kmajor
+                -> TopK -> K-major GEMM.
+    Every call is bracketed by HIP events; the producer alone and the torch
+    normalisation alone are timed too."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    import workloads as wl
+    wk, M = L.wk, L.M
+    K = wk.inputs[name][0]
+    k = rmm.rmm_retained_count(r, K)
+    X, Xt, e = L.X[name], L.Xt[name], L.energy[:K]
+    g = torch.from_numpy(wl.f32_to_bf16_bits(1.0 + 0.3 * wl.normal_blocks((wk.seed, 77), (1, K))[0])
+                         .view(np.int16)).to(L.dev).view(torch.bfloat16)
+    idx = torch.empty(k, dtype=torch.int32, device=L.dev)
+    Y = torch.empty((M, K), dtype=torch.bfloat16, device=L.dev)
+    ws_n = torch.empty(rmm.rmm_rmsnorm_kmajor_workspace_size(1, M, K), dtype=torch.uint8,
+                       device=L.dev)
+    W, Yo = L.Wcat[name], L.Ycat[name]
+
+    def producer():
+        rmm.rmm_rmsnorm_kmajor(X, g, eps, Xt.view(1, K, M), e, ws_n)
+
+    def torch_norm():
+        xf = X.float()
+        t = (xf * torch.rsqrt(xf.pow(2).mean(dim=-1, keepdim=True) + eps)).to(torch.bfloat16)
+        torch.mul(t, g, out=Y)
+
+    def score():
+        rmm.rmm_score_kmajor(Y, e, Xt, L.ws)
+
+    def tail():
+        rmm.rmm_select(e, k, idx)
+        rmm.rmm_reduced_gemm_kmajor(Xt, W, idx.view(1, k), Yo)
+
+    def fused():
+        producer()
+        tail()
+
+    def unfused():
+        torch_norm()
+        score()
+        tail()
+
+    us = {n: time_calls(f, steps, warmup) for n, f in
+          (("fused", fused), ("unfused", unfused), ("producer", producer),
+           ("torch_norm", torch_norm), ("score_kmajor", score))}
+    nbytes = 2 * M * K * 2 + 8 * K           # read X, write Xt, energies
+    return {"input": name, "r": r, "K": K, "k": k, "fused_us": us["fused"],
+            "unfused_us": us["unfused"], "producer_us": us["producer"],
+            "torch_norm_us": us["torch_norm"], "score_kmajor_us": us["score_kmajor"],
+            "unfused_without_norm_us": us["unfused"] - us["torch_norm"],
+            "speedup": us["unfused"] / us["fused"],
+            "speedup_without_norm": (us["unfused"] - us["torch_norm"]) / us["fused"],
+            "producer_bytes": nbytes, "producer_gbs": nbytes / (us["producer"] * 1e-6) / 1e9,
+            "calls": steps}
 
 
 def attention_weights(L):
@@ -781,6 +846,33 @@ def main():
                         "score_finalize_kernel"],
             "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
                                    for k, v in rec.items()} for r, rec in mc.items()},
+        }
+    if not args.no_norm_chain:
+        nc = {}
+        for name in ("attn_in", "mlp_in"):
+            for r in sorted(sweep):
+                rec = time_norm_chain(L, name, r, args.steps, args.warmup)
+                nc[f"{name}@{r}"] = {k: (round(v, 3) if isinstance(v, float) else v)
+                                     for k, v in rec.items()}
+                print(f"# norm -> {name} projection r={r}: fused {rec['fused_us']:.1f} us, unfused "
+                      f"{rec['unfused_us']:.1f} us (torch norm {rec['torch_norm_us']:.1f} us); "
+                      f"producer {rec['producer_us']:.1f} us ({rec['producer_gbs']:.0f} GB/s), "
+                      f"scoring pass {rec['score_kmajor_us']:.1f} us", file=sys.stderr, flush=True)
+        p_us = sum(v["producer_us"] for v in nc.values())
+        p_b = sum(v["producer_bytes"] for v in nc.values())
+        out["norm_chain"] = {
+            "op": "RMSNorm in front of a projection group feeding its reduced GEMM: fused = "
+                  "rmm_rmsnorm_kmajor writes the normalised rows K-major with their column "
+                  "energies in one pass over X (no scoring pass), unfused = torch RMSNorm, "
+                  "rmm_score_kmajor; both then TopK and the K-major GEMM (q|k|v or gate|up)",
+            "kernels": ["rmsnorm_kmajor_kernel", "score_finalize_kernel", "select_kernel",
+                        "gemm_kmajor_tr_kernel"],
+            "per_input_ratio": nc,
+            "roofline": {"bound": "hbm", "kernel": "rmsnorm_kmajor_kernel (+ score_finalize_kernel)",
+                         "achieved": round(p_b / (p_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(p_b / (p_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                         "bytes_basis": "one read of X + one write of Xt + the energies per call",
+                         "traffic": None},
         }
     if not args.no_decode:
         dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}

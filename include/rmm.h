@@ -129,6 +129,39 @@ rmm_status_t rmm_score_kmajor(const void *X, int64_t B, int64_t M, int64_t K, in
                               void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * RMSNorm producing a reduced projection's input, K-major, with its column
+ * energies   (Sec. 3.2: the retained set is scored on the projection's own
+ * input; Sec. 3.3 reduces the attention and MLP projections, whose inputs
+ * the LLaMA-family models produce with RMSNorm; the Limitations section
+ * names the memory movement of a separate scoring pass as a cost to remove).
+ *
+ * For each unit b and row m of X (bf16):
+ *   r_m          = 1 / sqrt(mean_j X[b][m][j]^2 + eps)      (fp32)
+ *   y[m][j]      = bf16(gamma[j] * bf16(X[b][m][j] * r_m))   (the model's
+ *                  normalised value, rounded as its bf16 output, times the
+ *                  weight, rounded again)
+ *   Xt[b][j][m]  = y[m][j]                                    (K-major)
+ *   energy[b][j] = sum over m < M of y[m][j]^2                (float64 sums
+ *                  of exact squares in a fixed order)
+ * which is what rmm_score_kmajor would compute on the normalised rows, in
+ * one pass over X: feed them to rmm_select and rmm_reduced_gemm_kmajor.
+ *
+ * X     : bf16 [B][M][ldx], ldx >= K.      gamma : bf16 [K] (the norm weight).
+ * Xt    : bf16 [B][K][ldxt], ldxt >= M; columns M..ldxt-1 are not written.
+ * energy: float64 [B][K].   eps >= 0 (finite).
+ * workspace : rmm_rmsnorm_kmajor_workspace_size(B, M, K) bytes, 8-byte
+ *         aligned (per-workgroup partial energies; overwritten by every call).
+ * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, ldx < K, ldxt < M,
+ *         eps negative, infinite or NaN; UNSUPPORTED unless K % 8 == 0,
+ *         K <= 8192, B <= 65535, X, gamma and Xt are 16-byte aligned and
+ *         ldx, ldxt are multiples of 8; WORKSPACE_TOO_SMALL.
+ */
+size_t rmm_rmsnorm_kmajor_workspace_size(int64_t B, int64_t M, int64_t K);
+rmm_status_t rmm_rmsnorm_kmajor(const void *X, const void *gamma, float eps, int64_t B, int64_t M,
+                                int64_t K, int64_t ldx, void *Xt, int64_t ldxt, double *energy,
+                                void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * TopK selection   (Sec. 3.2: I = TopK({s_j}, ceil(rho d))).
  *
  * For each unit b, writes the k indices of the largest energy[b*K + j] to

@@ -21,7 +21,8 @@ __all__ = [
     "rmm_status_string", "rmm_score", "rmm_select", "rmm_reduced_gemm",
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
     "rmm_reduced_attention", "rmm_reduced_gemv", "rmm_gemv_workspace_size", "rmm_select_tokens",
-    "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "EXPORTED_SYMBOLS",
+    "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "rmm_rmsnorm_kmajor",
+    "rmm_rmsnorm_kmajor_workspace_size", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -49,6 +50,9 @@ _SIGS = {
                                   _i64, _i64, _i64, _p, _i64, _p, _p, ctypes.c_size_t, _p]),
     "rmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "rmm_noalloc_scratch_bytes": (ctypes.c_size_t, []),
+    "rmm_rmsnorm_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64]),
+    "rmm_rmsnorm_kmajor": (ctypes.c_int, [_p, _p, ctypes.c_float, _i64, _i64, _i64, _i64, _p, _i64,
+                                          _p, _p, ctypes.c_size_t, _p]),
     "rmm_linear_noalloc": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
                                           _i64, _i64, _i64, _p, _i64, _p, _p]),
     "rmm_score_kmajor": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _p, _p, _i64, _p,
@@ -593,3 +597,34 @@ def rmm_linear_noalloc(X: torch.Tensor, W: torch.Tensor, r: float, Y: torch.Tens
         X.data_ptr(), W.data_ptr(), float(r), _dtype_code(X), B, M, N, K, ldx, ldw,
         Y.data_ptr(), ldy, _ptr(idx_out), _stream(d, stream)))
     return Y
+
+
+def rmm_rmsnorm_kmajor_workspace_size(B: int, M: int, K: int) -> int:
+    return int(lib.rmm_rmsnorm_kmajor_workspace_size(int(B), int(M), int(K)))
+
+
+def rmm_rmsnorm_kmajor(X: torch.Tensor, gamma: torch.Tensor, eps: float, Xt: torch.Tensor,
+                       energy: torch.Tensor, workspace: torch.Tensor | None = None,
+                       stream=None) -> torch.Tensor:
+    """RMSNorm of X [B, M, K] (or [M, K]) with weight gamma [K], written
+    K-major into Xt [B, K, M] (row stride Xt.stride(-2)) with the column
+    energies of the normalised rows in energy (float64 [B*K])."""
+    B, M, K, ldx = _rows(X, "X")
+    d = _dev(X, gamma, Xt, energy)
+    Bt, Kt, Mt, ldxt = _rows(Xt, "Xt")
+    if (Bt, Kt, Mt) != (B, K, M):
+        raise ValueError("Xt must be [B, K, M]")
+    if gamma.numel() != K or not gamma.is_contiguous():
+        raise ValueError("gamma must be a contiguous [K] tensor")
+    if not (X.dtype == gamma.dtype == Xt.dtype == torch.bfloat16):
+        raise TypeError("X, gamma and Xt must be bfloat16")
+    if energy.dtype != torch.float64 or energy.numel() != B * K or not energy.is_contiguous():
+        raise ValueError("energy must be contiguous float64 [B*K]")
+    if workspace is None:
+        workspace = torch.empty(max(rmm_rmsnorm_kmajor_workspace_size(B, M, K), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_rmsnorm_kmajor", lib.rmm_rmsnorm_kmajor(
+        X.data_ptr(), gamma.data_ptr(), float(eps), B, M, K, ldx, Xt.data_ptr(), ldxt,
+        energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    return Xt

@@ -446,3 +446,36 @@ def test_linear_noalloc_validation():
     assert rmm.rmm_workspace_size(rmm.RMM_OP_LINEAR, 1, 8192, 4096, 2048) > (64 << 20)
     assert f(*big) == TOO_LARGE
     assert rmm.rmm_status_string(TOO_LARGE) == "problem exceeds the library's fixed scratch buffer"
+
+
+def test_rmsnorm_kmajor_validation():
+    f = rmm.lib.rmm_rmsnorm_kmajor
+    need = rmm.rmm_rmsnorm_kmajor_workspace_size(1, 64, 128)
+    assert need > 0 and need % 8 == 0
+    assert rmm.rmm_rmsnorm_kmajor_workspace_size(1, 64, 8200) == 0     # K > 8192
+    base = [P, P, 1e-5, 1, 64, 128, 128, P, 64, P, P, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 7, 9):
+        assert call(i, NULL) == INVALID
+    assert call(2, -1.0) == INVALID
+    assert call(2, float("nan")) == INVALID
+    assert call(2, float("inf")) == INVALID
+    assert call(3, 0) == INVALID
+    assert call(6, 100) == INVALID            # ldx < K
+    assert call(8, 63) == INVALID             # ldxt < M
+    def call2(K, ldx):
+        a = list(base)
+        a[5], a[6] = K, ldx
+        return f(*a)
+
+    assert call2(130, 136) == UNSUPPORTED     # K % 8
+    assert call2(8200, 8200) == UNSUPPORTED   # K > 8192
+    assert call(6, 132) == UNSUPPORTED        # ldx % 8
+    assert call(0, ctypes.c_void_p(0x100008)) == UNSUPPORTED   # misaligned X
+    assert call(10, NULL) == WS_SMALL
+    assert call(11, need - 1) == WS_SMALL
