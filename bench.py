@@ -865,10 +865,10 @@ def main():
                   "rmm_rmsnorm_kmajor writes the normalised rows K-major with their column "
                   "energies in one pass over X (no scoring pass), unfused = torch RMSNorm, "
                   "rmm_score_kmajor; both then TopK and the K-major GEMM (q|k|v or gate|up)",
-            "kernels": ["rmsnorm_kmajor_kernel", "score_finalize_kernel", "select_kernel",
-                        "gemm_kmajor_tr_kernel"],
+            "kernels": ["rms_rowscale_kernel", "score_tile_kernel (normalising variant)",
+                        "score_finalize_kernel", "select_kernel", "gemm_kmajor_tr_kernel"],
             "per_input_ratio": nc,
-            "roofline": {"bound": "hbm", "kernel": "rmsnorm_kmajor_kernel (+ score_finalize_kernel)",
+            "roofline": {"bound": "hbm", "kernel": "rmm_rmsnorm_kmajor (all three kernels)",
                          "achieved": round(p_b / (p_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(p_b / (p_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
                          "bytes_basis": "one read of X + one write of Xt + the energies per call",

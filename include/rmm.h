@@ -143,18 +143,19 @@ rmm_status_t rmm_score_kmajor(const void *X, int64_t B, int64_t M, int64_t K, in
  *   Xt[b][j][m]  = y[m][j]                                    (K-major)
  *   energy[b][j] = sum over m < M of y[m][j]^2                (float64 sums
  *                  of exact squares in a fixed order)
- * which is what rmm_score_kmajor would compute on the normalised rows, in
- * one pass over X: feed them to rmm_select and rmm_reduced_gemm_kmajor.
+ * which is what rmm_score_kmajor would compute on the normalised rows,
+ * without writing them row-major first: feed them to rmm_select and
+ * rmm_reduced_gemm_kmajor.
  *
  * X     : bf16 [B][M][ldx], ldx >= K.      gamma : bf16 [K] (the norm weight).
  * Xt    : bf16 [B][K][ldxt], ldxt >= M; columns M..ldxt-1 are not written.
  * energy: float64 [B][K].   eps >= 0 (finite).
- * workspace : rmm_rmsnorm_kmajor_workspace_size(B, M, K) bytes, 8-byte
- *         aligned (per-workgroup partial energies; overwritten by every call).
+ * workspace : rmm_rmsnorm_kmajor_workspace_size(B, M, K) bytes, 256-byte
+ *         aligned (row scales and partial energies; overwritten by every call).
  * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, ldx < K, ldxt < M,
- *         eps negative, infinite or NaN; UNSUPPORTED unless K % 8 == 0,
- *         K <= 8192, B <= 65535, X, gamma and Xt are 16-byte aligned and
- *         ldx, ldxt are multiples of 8; WORKSPACE_TOO_SMALL.
+ *         eps negative, infinite or NaN, a misaligned workspace; UNSUPPORTED
+ *         unless K % 8 == 0, B <= 65535, X, gamma and Xt are 16-byte aligned
+ *         and ldx, ldxt are multiples of 8; WORKSPACE_TOO_SMALL.
  */
 size_t rmm_rmsnorm_kmajor_workspace_size(int64_t B, int64_t M, int64_t K);
 rmm_status_t rmm_rmsnorm_kmajor(const void *X, const void *gamma, float eps, int64_t B, int64_t M,

@@ -131,7 +131,7 @@ rmm_status_t rmm_score_kmajor(const void *X, int64_t B, int64_t M, int64_t K, in
 }
 
 size_t rmm_rmsnorm_kmajor_workspace_size(int64_t B, int64_t M, int64_t K) {
-    if (B < 1 || M < 1 || K < 1 || K > 8192) return 0;
+    if (B < 1 || M < 1 || K < 1) return 0;
     return align256(rmm::rmsnorm_workspace_bytes(B, M, K));
 }
 
@@ -142,16 +142,18 @@ rmm_status_t rmm_rmsnorm_kmajor(const void *X, const void *gamma, float eps, int
     if (B < 1 || M < 1 || K < 1 || ldx < K || ldxt < M) return RMM_ERR_INVALID_ARGUMENT;
     if (!(eps >= 0.f) || std::isinf(eps)) return RMM_ERR_INVALID_ARGUMENT;   // also NaN
     if (M > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
-    if (K % 8 || K > 8192 || B > kGridYZMax) return RMM_ERR_UNSUPPORTED;
+    if (K % 8 || K > kInt32Max || B > kGridYZMax) return RMM_ERR_UNSUPPORTED;
+    // the tile kernel addresses one row split with 32-bit byte offsets
+    if (rmm::score_rows_per_split(B, M, K) * ldx * 2 >= (int64_t(1) << 31)) return RMM_ERR_UNSUPPORTED;
     if (!aligned16(X) || !aligned16(gamma) || !aligned16(Xt) || ldx % 8 || ldxt % 8 ||
         reinterpret_cast<uintptr_t>(energy) % 8)
         return RMM_ERR_UNSUPPORTED;
     const size_t need = rmm_rmsnorm_kmajor_workspace_size(B, M, K);
     if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
-    if (reinterpret_cast<uintptr_t>(workspace) % 8) return RMM_ERR_INVALID_ARGUMENT;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
     return from_hip(rmm::launch_rmsnorm_kmajor(
         static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(gamma), eps, B, M, K, ldx,
-        static_cast<uint16_t *>(Xt), ldxt, energy, static_cast<double *>(workspace), stream));
+        static_cast<uint16_t *>(Xt), ldxt, energy, workspace, stream));
 }
 
 rmm_status_t rmm_select(const double *energy, int64_t B, int64_t K, int64_t k, int32_t *idx,

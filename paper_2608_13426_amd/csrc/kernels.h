@@ -28,15 +28,20 @@ hipError_t launch_score(const void *X, bool bf16, int64_t B, int64_t M, int64_t 
                         int64_t ldx, double *energy, double *partials, uint16_t *Xt,
                         int64_t ldxt, hipStream_t stream);
 
+// The scoring pass over RMSNorm-normalised rows: y = bf16(gamma_j *
+// bf16(x * rscale[m])) (rscale [B][M] floats), energies and K-major copy of y
+// (bf16, 16-byte aligned rows, as for the K-major scoring pass)
+hipError_t launch_score_norm_kmajor(const uint16_t *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                                   const float *rscale, const uint16_t *gamma, double *energy,
+                                   double *partials, uint16_t *Xt, int64_t ldxt, hipStream_t stream);
 // RMSNorm writing the K-major normalised activations and their column
-// energies (bf16, K % 8 == 0, K <= 8192, 16-byte aligned rows; checked by the
-// caller); partials holds rmsnorm_workspace_bytes(B, M, K)
-int rmsnorm_rows_per_block(int64_t K);
-int64_t rmsnorm_workgroups(int64_t B, int64_t M, int64_t K);
+// energies (bf16, K % 8 == 0, 16-byte aligned rows; checked by the caller);
+// the workspace (rmsnorm_workspace_bytes, 256-byte aligned) holds the row
+// scales and the scoring partials
 size_t rmsnorm_workspace_bytes(int64_t B, int64_t M, int64_t K);
 hipError_t launch_rmsnorm_kmajor(const uint16_t *X, const uint16_t *gamma, float eps, int64_t B,
                                  int64_t M, int64_t K, int64_t ldx, uint16_t *Xt, int64_t ldxt,
-                                 double *energy, double *partials, hipStream_t stream);
+                                 double *energy, void *workspace, hipStream_t stream);
 
 // -------------------------------------------------------------- selection
 // TopK of x_j^2 for units of one token (row b of X at b * ldx)

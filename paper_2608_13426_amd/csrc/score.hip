@@ -156,11 +156,16 @@ __global__ __launch_bounds__(kThreads) void score_partial_kernel(
 constexpr int kStrip = 64;      // columns per workgroup that set the split policy
 constexpr int kTileJC = 8;      // 8-column groups per wave (8: 64 x 64 wave tiles)
 
-template <bool XT, int JC>
+// NORM: the values are first normalised as an RMSNorm stores them,
+// y = bf16(gamma[j] * bf16(x * rscale[m])) with the row scale of each row
+// (rscale: one float per row of every unit), and the energies and the
+// K-major copy are those of y.
+template <bool XT, int JC, bool NORM = false>
 __global__ __launch_bounds__(kThreads) void score_tile_kernel(
     const uint16_t *__restrict__ X, int64_t M, int64_t K, int64_t ldx, int64_t rows_per_split,
     double *__restrict__ out, int64_t out_unit_stride, int64_t out_split_stride,
-    uint16_t *__restrict__ Xt, int64_t ldxt) {
+    uint16_t *__restrict__ Xt, int64_t ldxt, const float *__restrict__ rscale = nullptr,
+    const uint16_t *__restrict__ gamma = nullptr) {
     constexpr int MC = 64 / JC, STRIP = 8 * JC, TROWS = 8 * MC;   // wave tile TROWS x STRIP
     __shared__ double red[kThreads / 64][STRIP];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -177,6 +182,12 @@ __global__ __launch_bounds__(kThreads) void score_tile_kernel(
     constexpr uint32_t kOut = 0x80000000u;
     const uint32_t col_off = nvalid > 0 ? static_cast<uint32_t>(j * 2) : kOut;
     uint16_t *xt = XT ? Xt + (unit * K + j) * ldxt + r_begin : nullptr;
+    float gm[8];
+    const float *rsu = NORM ? rscale + unit * M + r_begin : nullptr;
+    if constexpr (NORM) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gm[e] = e < nvalid ? bf16_to_f32(gamma[j + e]) : 0.f;
+    }
 
     double acc[8];
 #pragma unroll
@@ -189,6 +200,21 @@ __global__ __launch_bounds__(kThreads) void score_tile_kernel(
                                : static_cast<uint32_t>((m0 + 8 * mc + r) * ldx * 2) + col_off;
             const auto q = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
             v[r] = make_uint4(q[0], q[1], q[2], q[3]);
+        }
+        if constexpr (NORM) {
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int m = m0 + 8 * mc + r;
+                const float sc = m < rows ? rsu[m] : 0.f;
+                uint32_t w[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float xa = __uint_as_float(w[e] << 16), xb = __uint_as_float(w[e] & 0xffff0000u);
+                    w[e] = pack_bf16x2(bf16_to_f32(f32_to_bf16(xa * sc)) * gm[2 * e],
+                                       bf16_to_f32(f32_to_bf16(xb * sc)) * gm[2 * e + 1]);
+                }
+                v[r] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
         }
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
@@ -274,6 +300,19 @@ hipError_t launch_tiles(const uint16_t *X, int64_t B, int64_t M, int64_t K, int6
     return hipGetLastError();
 }
 
+hipError_t launch_tiles_norm(const uint16_t *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                             int64_t S, double *out, int64_t unit_stride, int64_t split_stride,
+                             uint16_t *Xt, int64_t ldxt, const float *rscale, const uint16_t *gamma,
+                             hipStream_t stream) {
+    const int64_t rps = score_rows_per_split(B, M, K);
+    constexpr int strip = 8 * kTileJC;
+    dim3 grid(static_cast<unsigned>((K + strip - 1) / strip), static_cast<unsigned>(S),
+              static_cast<unsigned>(B));
+    hipLaunchKernelGGL((score_tile_kernel<true, kTileJC, true>), grid, dim3(kThreads), 0, stream, X, M,
+                       K, ldx, rps, out, unit_stride, split_stride, Xt, ldxt, rscale, gamma);
+    return hipGetLastError();
+}
+
 template <typename T, int VEC, bool XT>
 hipError_t launch_partial(const T *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
                           int64_t S, double *out, int64_t unit_stride, int64_t split_stride,
@@ -310,6 +349,17 @@ int64_t score_splits(int64_t B, int64_t M, int64_t K) {
 size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K) {
     const int64_t s = score_splits(B, M, K);
     return s > 1 ? static_cast<size_t>(B * s * K) * sizeof(double) : 0;
+}
+
+hipError_t launch_score_norm_kmajor(const uint16_t *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
+                                   const float *rscale, const uint16_t *gamma, double *energy,
+                                   double *partials, uint16_t *Xt, int64_t ldxt, hipStream_t stream) {
+    const int64_t S = score_splits(B, M, K);
+    double *out = S > 1 ? partials : energy;
+    hipError_t err = launch_tiles_norm(X, B, M, K, ldx, S, out, S * K, K, Xt, ldxt, rscale, gamma,
+                                       stream);
+    if (err != hipSuccess || S == 1) return err;
+    return launch_score_finalize(partials, B, S, K, energy, stream);
 }
 
 hipError_t launch_score_finalize(const double *partials, int64_t B, int64_t S, int64_t K,

@@ -452,7 +452,6 @@ def test_rmsnorm_kmajor_validation():
     f = rmm.lib.rmm_rmsnorm_kmajor
     need = rmm.rmm_rmsnorm_kmajor_workspace_size(1, 64, 128)
     assert need > 0 and need % 8 == 0
-    assert rmm.rmm_rmsnorm_kmajor_workspace_size(1, 64, 8200) == 0     # K > 8192
     base = [P, P, 1e-5, 1, 64, 128, 128, P, 64, P, P, need, NULL]
 
     def call(i, v):
@@ -474,8 +473,8 @@ def test_rmsnorm_kmajor_validation():
         return f(*a)
 
     assert call2(130, 136) == UNSUPPORTED     # K % 8
-    assert call2(8200, 8200) == UNSUPPORTED   # K > 8192
     assert call(6, 132) == UNSUPPORTED        # ldx % 8
     assert call(0, ctypes.c_void_p(0x100008)) == UNSUPPORTED   # misaligned X
     assert call(10, NULL) == WS_SMALL
     assert call(11, need - 1) == WS_SMALL
+    assert call(10, ctypes.c_void_p(0x100008)) == INVALID     # workspace not 256-byte aligned

@@ -89,13 +89,13 @@ def _run(dev, Xbits, gbits, eps, pad=0, rows=None, project=None):
 
 
 @pytest.mark.parametrize("B,M,K,eps,pad,seed", [
-    (1, 300, 4096, 1e-5, 0, 0),      # 16-row blocks, ragged last block
-    (2, 70, 2048, 1e-6, 8, 1),       # 32-row blocks, two units, padded Xt rows
-    (1, 33, 8192, 1e-5, 0, 2),       # 8-row blocks, two channel groups per thread
+    (1, 300, 4096, 1e-5, 0, 0),      # ragged last 64-row tile
+    (2, 70, 2048, 1e-6, 8, 1),       # two units, padded Xt rows
+    (1, 33, 8192, 1e-5, 0, 2),       # fewer rows than one tile, 8192 channels
     (1, 1, 512, 0.0, 0, 3),          # one token, eps = 0
-    (1, 130, 520, 10.0, 0, 4),       # K not a multiple of 64 lanes; a large eps
-    (4, 2000, 1024, 1e-5, 0, 5),     # 63 blocks per unit: a workgroup count not a multiple of 8
-    (1, 9000, 256, 1e-5, 0, 6),      # more blocks than workgroups: two rounds, the last partial
+    (1, 130, 520, 10.0, 0, 4),       # K not a multiple of 64 (partial column strip); a large eps
+    (4, 2000, 1024, 1e-5, 0, 5),     # four units, several row splits each
+    (1, 9000, 256, 1e-5, 0, 6),      # many row splits of a narrow input
 ])
 def test_rmsnorm_kmajor(B, M, K, eps, pad, seed):
     dev = require_gpu()
