@@ -422,6 +422,14 @@ rmm_status_t rmm_reduced_pv(const void *P, const void *V, rmm_dtype_t dtype, int
     e = rmm::launch_select(energy, U, Lk, kt, idx, stream);
     if (e != hipSuccess) return RMM_ERR_HIP;
     const size_t esz = bf16 ? 2 : 4;
+    if (kmajor) {
+        // one launch over every query head, each reading its kv head's rows of V
+        e = rmm::launch_gemm_kmajor_grouped_bf16(Pt, static_cast<const uint16_t *>(V), idx, U, Lq, D,
+                                                 Lk, kt, xt_ld(Lq), D, static_cast<uint16_t *>(O), D,
+                                                 Lk * D, static_cast<int>(grp), stream);
+        if (e != hipErrorNotSupported) return from_hip(e);
+        e = hipSuccess;
+    }
     for (int64_t b = 0; b < batch && e == hipSuccess; ++b)
         for (int64_t g = 0; g < Hkv && e == hipSuccess; ++g) {
             const int64_t u0 = b * H + g * grp;

@@ -544,28 +544,40 @@ __device__ __forceinline__ uint32_t swiglu_bf16(uint32_t gb, uint32_t ub) {
 // and part[(unit * tiles_m + m0/256) * N/2 + c] = sum over its rows m < M of
 // Ht[unit][c][m]^2 in float64 (one row tile's share of that input's column
 // energies).
-template <int NW, int BKS, int S, int EPI = 0>
-__global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
+//
+// BNT is the tile's width in n: 256 (eight waves, one workgroup per CU), or
+// 128 (four waves of the same 128 x 64 wave tile, 72 KiB of LDS, two
+// workgroups per CU whose barriers and epilogues need not coincide).  With
+// BNT = 128 a staged W row is 256 bytes and one wave instruction stages four
+// of them.  OCC is the waves per SIMD the register budget is sized for.
+template <int NW, int BKS, int S, int EPI = 0, int BNT = 256, int OCC = NW / 4>
+__global__ __launch_bounds__(NW * 64, OCC) void gemm_kmajor_tr_kernel(
     const uint16_t *__restrict__ Xt, const uint16_t *__restrict__ W,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int k,
     int64_t ldxt, int64_t ldw, int64_t ldy, int64_t xt_bytes, int64_t w_bytes, int tiles_m,
-    int tiles_n, int vec_y, double *__restrict__ part) {
+    int tiles_n, int vec_y, double *__restrict__ part, int64_t w_ustride = 0, int w_ugroup = 1) {
     using namespace trk;
-    constexpr int ASZ = BKS * ROWB;      // one operand, one stage
-    constexpr int PPW = BKS / 2 / NW;    // staged row pairs per wave per operand
+    constexpr int ASZ = BKS * ROWB;      // X operand, one stage
+    constexpr int ROWBB = BNT * 2;       // bytes per staged W row
+    constexpr int BSZ = BKS * ROWBB;     // W operand, one stage
+    constexpr int PPW = BKS / 2 / NW;    // staged X row pairs per wave
+    constexpr int RPB = 1024 / ROWBB;    // W rows one wave instruction stages
+    constexpr int BLD = BKS / RPB / NW;  // W loads per wave per stage
     constexpr int WN = NW / 2;           // waves: 2 along m, NW/2 along n
-    constexpr int TWN = BT / WN;
+    constexpr int TWN = BNT / WN;
     constexpr int FM = 4, FN = TWN / 32;
     constexpr int D = S - 1;             // stages in flight ahead of the MFMAs
-    constexpr int PER_STAGE = 2 * PPW;   // loads per wave per stage
+    constexpr int PER_STAGE = PPW + BLD; // loads per wave per stage
     static_assert((NW == 4 || NW == 8) && PPW * NW * 2 == BKS && PPW >= 1, "wave layout");
-    static_assert(BKS % 16 == 0 && S >= 2 && S <= 4 && 2 * S * ASZ <= 160 * 1024, "stages");
+    static_assert((BNT == 256 || BNT == 128) && BLD * RPB * NW == BKS && BLD >= 1 && FN >= 1,
+                  "W staging layout");
+    static_assert(BKS % 16 == 0 && S >= 2 && S <= 4 && S * (ASZ + BSZ) <= 160 * 1024, "stages");
     static_assert((D - 1) * PER_STAGE < 64, "vmcnt range");
     // One LDS object per stage and operand: the compiler then sees that a
     // fragment read of one stage cannot alias the loads still landing in the
     // others, and waits only for the loads of the stage it reads.
     __shared__ __attribute__((aligned(1024))) char sA0[ASZ], sA1[ASZ], sA2[ASZ], sA3[ASZ];
-    __shared__ __attribute__((aligned(1024))) char sB0[ASZ], sB1[ASZ], sB2[ASZ], sB3[ASZ];
+    __shared__ __attribute__((aligned(1024))) char sB0[BSZ], sB1[BSZ], sB2[BSZ], sB3[BSZ];
     auto stage_a = [&](auto I) -> char * {
         constexpr int i = decltype(I)::value;
         if constexpr (i == 0) return sA0;
@@ -588,7 +600,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     const int first_m = (lin / gsz) * big::GROUP_M;
     const int gm = min(big::GROUP_M, tiles_m - first_m);
     const int m0 = (first_m + (lin % gsz) % gm) * BT;
-    const int n0 = ((lin % gsz) / gm) * BT;
+    const int n0 = ((lin % gsz) / gm) * BNT;
     const int64_t unit = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -598,8 +610,11 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t *>(Xt + unit * (xt_bytes / 2)), 0, static_cast<uint32_t>(xt_bytes),
         0x00020000);
+    // units u read weights W + (u / w_ugroup) * w_ustride (one matrix for all
+    // units unless the caller groups them, e.g. query heads sharing a value head)
     const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t *>(W), 0, static_cast<uint32_t>(w_bytes), 0x00020000);
+        const_cast<uint16_t *>(W + (unit / w_ugroup) * w_ustride), 0, static_cast<uint32_t>(w_bytes),
+        0x00020000);
     const uint32_t arow = static_cast<uint32_t>(ldxt) * 2u, brow = static_cast<uint32_t>(ldw) * 2u;
 
     // DMA role: row pair P = wave*PPW + q of a stage holds retained rows
@@ -613,6 +628,10 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
         acol[e] = static_cast<uint32_t>(m0 + 8 * src) * 2u;
         bcol[e] = static_cast<uint32_t>(n0 + 8 * src) * 2u;
     }
+    // BNT = 128: lane l fills chunk position l % 16 of staged W row l / 16 of
+    // its instruction's four, with source chunk (l % 16) ^ 4*(row % 4)
+    const int bq = lane >> 4;
+    const uint32_t bcol4 = static_cast<uint32_t>(n0 + 8 * ((lane & 15) ^ (4 * bq))) * 2u;
     // the wave's 2*PPW retained positions of stage st, read as scalars
     // (clamped into the list; positions past k are masked below)
     auto stage_idx = [&](int st, int32_t (&r)[2 * PPW]) {
@@ -629,9 +648,24 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
             const uint32_t j = static_cast<uint32_t>(h ? r[2 * q + 1] : r[2 * q]);
             const int P = wave * PPW + q;
             const uint32_t ao = in ? j * arow + acol[P & 1] : kOut;
-            const uint32_t bo = in ? j * brow + bcol[P & 1] : kOut;
             lds_load16(ar, la + P * 1024, ao);
-            lds_load16(br, lb + P * 1024, bo);
+            if constexpr (BNT == 256) {
+                const uint32_t bo = in ? j * brow + bcol[P & 1] : kOut;
+                lds_load16(br, lb + P * 1024, bo);
+            }
+        }
+        if constexpr (BNT == 128) {
+#pragma unroll
+            for (int q = 0; q < BLD; ++q) {
+                const int local = RPB * q + bq;           // row within the wave's 2*PPW
+                const bool in = base + local < k;
+                uint32_t j = static_cast<uint32_t>(r[0]);
+#pragma unroll
+                for (int e = 1; e < 2 * PPW; ++e)
+                    if (local == e) j = static_cast<uint32_t>(r[e]);
+                const uint32_t bo = in ? j * brow + bcol4 : kOut;
+                lds_load16(br, lb + (wave * BLD + q) * 1024, bo);
+            }
         }
     };
 
@@ -640,19 +674,21 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     const int wm = wave / WN, wn = wave % WN;
     const int g = lane >> 4, s16 = lane & 15;
     const int f4 = (s16 >> 2) & 3;
-    const int lane_off = (8 * (g >> 1) + (s16 >> 2)) * ROWB + (2 * (g & 1) + ((s16 & 3) >> 1)) * 16 +
-                         8 * (s16 & 1);
+    const int col_off = (2 * (g & 1) + ((s16 & 3) >> 1)) * 16 + 8 * (s16 & 1);
+    const int lane_off = (8 * (g >> 1) + (s16 >> 2)) * ROWB + col_off;
+    const int lane_off_b = (8 * (g >> 1) + (s16 >> 2)) * ROWBB + col_off;
     int aoff[FM], boff[FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i) aoff[i] = lane_off + 64 * (4 * wm + (i ^ f4));
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int q = (wn * TWN) / 32 + j;
-        boff[j] = lane_off + 64 * ((q & ~3) + ((q & 3) ^ f4));
+        boff[j] = lane_off_b + 64 * ((q & ~3) + ((q & 3) ^ f4));
     }
-    auto frag = [&](const char *base) -> bf16x8_t {
+    auto frag = [&](const char *base, auto RB) -> bf16x8_t {
+        constexpr int rb = decltype(RB)::value;
         const s16x4_t lo = lds_read_tr16(base);
-        const s16x4_t hi = lds_read_tr16(base + 4 * ROWB);
+        const s16x4_t hi = lds_read_tr16(base + 4 * rb);
         typedef short s16x8_t __attribute__((ext_vector_type(8)));
         const s16x8_t v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         return __builtin_bit_cast(bf16x8_t, v);
@@ -704,11 +740,12 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
 #pragma unroll
         for (int ks = 0; ks < BKS / 16; ++ks) {
             bf16x8_t a[FM], b[FN];
-            const int kb = ks * 16 * ROWB;
+            using RA = std::integral_constant<int, ROWB>;
+            using RBB = std::integral_constant<int, ROWBB>;
 #pragma unroll
-            for (int i = 0; i < FM; ++i) a[i] = frag(la + aoff[i] + kb);
+            for (int i = 0; i < FM; ++i) a[i] = frag(la + aoff[i] + ks * 16 * ROWB, RA{});
 #pragma unroll
-            for (int j = 0; j < FN; ++j) b[j] = frag(lb + boff[j] + kb);
+            for (int j = 0; j < FN; ++j) b[j] = frag(lb + boff[j] + ks * 16 * ROWBB, RBB{});
 #pragma unroll
             for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -736,7 +773,8 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     //                      m = m0 + wm*128 + 32i + lane%32
     const int lr = lane & 31, lh = lane >> 5;
     if constexpr (EPI == 1) {
-        static_assert(NW == 8 && FM == 4 && FN == 2 && BT == 256 && BKS >= 32, "SwiGLU epilogue layout");
+        static_assert(NW == 8 && FM == 4 && FN == 2 && BT == 256 && BNT == 256 && BKS >= 32,
+                      "SwiGLU epilogue layout");
         typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
         typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
         auto obj = [&](int q) -> char * {
@@ -847,13 +885,13 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
     const int rows = min(BT, M - m0);
     const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
         Yu + static_cast<int64_t>(m0) * ldy, 0, static_cast<uint32_t>(rows * ldy * 2), 0x00020000);
-    if (vec_y == 2 && n0 + BT <= N) {
+    if (BNT == 256 && vec_y == 2 && n0 + BT <= N) {
         // Whole-width tile with 16-byte aligned rows: the tile goes out in two
         // passes through the (now idle) ring, so that every store writes 16
         // bytes of a 512-byte row run.  Pass p holds fragments i = 2p, 2p+1 of
         // every wave: 128 rows, 32 per ring object; within a row the 16-byte
         // chunk c sits at position c ^ (row % 32).
-        static_assert(FM == 4 && BT == 256, "staged epilogue layout");
+        static_assert(FM == 4 && BT == 256 && (BNT == 256 || BNT == 128), "staged epilogue layout");
         auto obj = [&](int q) -> char * {
             return q == 0 ? sA0 : q == 1 ? sA1 : q == 2 ? sB0 : sB1;
         };
@@ -894,7 +932,7 @@ __global__ __launch_bounds__(NW * 64, NW / 4) void gemm_kmajor_tr_kernel(
         }
         return;
     }
-    const bool full_n = vec_y && n0 + BT <= N;
+    const bool full_n = vec_y && n0 + BNT <= N;
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -1019,23 +1057,42 @@ hipError_t launch_gemm_bf16(const uint16_t *X, const uint16_t *W, const int32_t 
 constexpr int kKmajorWaves = 8;
 constexpr int kTrWaves = 8, kTrRows = 32, kTrStages = 3;
 
-hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
-                                  int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
-                                  int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
-                                  hipStream_t stream) {
+namespace {
+
+// The K-major GEMM over B units; units u read W + (u / w_ugroup) * w_ustride.
+// Returns hipErrorNotSupported (launching nothing) when grouped weights are
+// asked of the kernels without that addressing (fewer than 128 large tiles).
+hipError_t kmajor_dispatch(const uint16_t *Xt, const uint16_t *W, const int32_t *idx, int64_t B,
+                           int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldxt, int64_t ldw,
+                           uint16_t *Y, int64_t ldy, int64_t w_ustride, int w_ugroup,
+                           hipStream_t stream) {
     const int64_t xt_bytes = K * ldxt * 2, w_bytes = K * ldw * 2;
     const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+    const bool grouped = w_ustride != 0 && w_ugroup < B;
     // Y rows of one 256-row tile are addressed with 32-bit byte offsets
     if (t256 * B >= 128 && ldy < (int64_t(1) << 23)) {
-        const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
         const int vec_y = (reinterpret_cast<uintptr_t>(Y) % 16 == 0 && ldy % 8 == 0) ? 2
                           : (reinterpret_cast<uintptr_t>(Y) % 8 == 0 && ldy % 4 == 0) ? 1 : 0;
+        const int tm = static_cast<int>((M + 255) / 256);
+        if (N <= 128) {
+            // 256 x 128 tiles: no half-empty tile, two workgroups per CU
+            hipLaunchKernelGGL((gemm_kmajor_tr_kernel<4, kTrRows, kTrStages, 0, 128, 2>),
+                               dim3(tm, static_cast<unsigned>(B)), dim3(4 * 64), 0, stream,
+                               Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
+                               static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, 1, vec_y,
+                               nullptr, w_ustride, w_ugroup);
+            return hipGetLastError();
+        }
+        const int tn = static_cast<int>((N + 255) / 256);
         hipLaunchKernelGGL((gemm_kmajor_tr_kernel<kTrWaves, kTrRows, kTrStages>),
                            dim3(tm * tn, static_cast<unsigned>(B)), dim3(kTrWaves * 64), 0, stream,
                            Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
                            static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, tn, vec_y,
-                           nullptr);
-    } else if (t256 * B >= 128) {
+                           nullptr, w_ustride, w_ugroup);
+        return hipGetLastError();
+    }
+    if (grouped) return hipErrorNotSupported;
+    if (t256 * B >= 128) {
         const int tm = static_cast<int>((M + 255) / 256), tn = static_cast<int>((N + 255) / 256);
         hipLaunchKernelGGL((gemm_kmajor_bf16_kernel<256, kKmajorWaves>),
                            dim3(tm * tn, static_cast<unsigned>(B)), dim3(kKmajorWaves * 64), 0, stream, Xt, W, idx, Y, static_cast<int>(M),
@@ -1049,6 +1106,22 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                            ldw, ldy, xt_bytes, w_bytes, tm, tn);
     }
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
+                                  int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                                  int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
+                                  hipStream_t stream) {
+    return kmajor_dispatch(Xt, W, idx, B, M, N, K, k, ldxt, ldw, Y, ldy, 0, 1, stream);
+}
+
+hipError_t launch_gemm_kmajor_grouped_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
+                                          int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                                          int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
+                                          int64_t w_ustride, int w_ugroup, hipStream_t stream) {
+    return kmajor_dispatch(Xt, W, idx, B, M, N, K, k, ldxt, ldw, Y, ldy, w_ustride, w_ugroup, stream);
 }
 
 hipError_t launch_gemm_swiglu_kmajor_bf16(const uint16_t *Xt, const uint16_t *W,

@@ -65,6 +65,13 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                                   int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                                   int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
                                   hipStream_t stream);
+// the same product with per-unit weights: unit u reads W + (u / w_ugroup) *
+// w_ustride elements; hipErrorNotSupported (nothing launched) when the
+// problem is too small for the large-tile kernels that address them so
+hipError_t launch_gemm_kmajor_grouped_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
+                                          int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
+                                          int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
+                                          int64_t w_ustride, int w_ugroup, hipStream_t stream);
 // the gate|up product with the SwiGLU epilogue: W [K][ldw] holds 2F columns
 // in 128-column blocks (gate, then up, of the same 128 channels); writes the
 // down projection's K-major input Ht [B][F][ldht] and its column energies

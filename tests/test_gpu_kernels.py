@@ -258,6 +258,8 @@ def test_reduced_gemm_large_tiles(B, M, N, K, k, ldw_pad, seed):
     (2, 2048, 2048, 4096, 2048, 51),
     (1, 4096, 2048, 1024, 1, 53),
     (1, 2048, 4096, 1024, 1024, 54),
+    (4, 8000, 128, 3000, 1111, 60),   # 256 x 128 tiles (N <= 128), ragged M and k
+    (5, 6500, 72, 500, 333, 61),      # 256 x 128 tiles, N and M ragged
 ])
 def test_reduced_gemm_kmajor(B, M, N, K, k, seed):
     """Oracle parity, and bit-identity with the row-major gather (same k order)."""
