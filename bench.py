@@ -68,31 +68,45 @@ HEADLINE_R = 0.5
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (no sparsity)
 PEAK_HBM_GBS = 8000.0
 GEMM_KERNEL = "gemm_kmajor_tr_kernel"
-GEMM_SOURCE = os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "gemm.hip")
-# HBM bytes per launch from two rocprofv3 --pmc runs of the default ratio mix
-# (FETCH_SIZE x2.0, WRITE_SIZE x1.0: the factors a 512 MiB device copy reads),
-# averaged over the kernel's dispatches of the layer step (the value product's
-# per-kv-head launches, smaller grids, excluded).  Each figure is valid only for the
-# source whose SHA-256 is recorded and for the same launch mix.
-GEMM_TRAFFIC = {"source": GEMM_SOURCE,
-                "sha256": "2a169138d50d7b30535ec331cb40c027f53f3cff503b007020141cef08f61886",
-                "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
-                "bytes": round((399414.80 * 2.0 + 172304.08) * 1024)}
-# per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
-# plus attn_compact_k_kernel
-ATTN_TRAFFIC = {"source": os.path.join(ROOT, "paper_2608_13426_amd", "csrc", "attn.hip"),
-                "sha256": "0a90ce58f6afdaf6cca061def81dbdd3b0d28a0cdcc29eaac7532da4dd7c5563",
-                "mix": "layer_8b r=0.25,0.5,0.75,1.0",
-                "bytes": round((103398.442 * 2.0 + 65545.42 + 8249.01 * 2.0 + 40960.00) * 1024)}
+CSRC = os.path.join(ROOT, "paper_2608_13426_amd", "csrc")
+BUILD_SCRIPT = os.path.join(ROOT, "paper_2608_13426_amd", "build.py")
+
+
+def _sources(main):
+    """A kernel's translation unit, the headers it includes, and the build
+    script (its compiler flags): what the HBM counter figures depend on."""
+    return [os.path.join(CSRC, main), os.path.join(CSRC, "device_common.h"),
+            os.path.join(CSRC, "kernels.h"), BUILD_SCRIPT]
+
+
+# HBM bytes per launch (or call) from two rocprofv3 --pmc runs of the default
+# ratio mix (FETCH_SIZE x2.0, WRITE_SIZE x1.0: the factors a 512 MiB device
+# copy reads), averaged over the kernel's dispatches of the measured command.
+# A figure is reported only while the SHA-256 of its sources (the kernel's
+# file, the shared headers and the build script) is the one it was measured
+# with, and for the same launch mix; re-run the counters after any change.
+GEMM_TRAFFIC = {"sources": _sources("gemm.hip"), "sha256": None,
+                "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped", "bytes": None}
+ATTN_TRAFFIC = {"sources": _sources("attn.hip"), "sha256": None,
+                "mix": "layer_8b r=0.25,0.5,0.75,1.0", "bytes": None}
+NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip")], "sha256": None,
+                "mix": "layer_8b attn_in,mlp_in r=0.25,0.5,0.75,1.0", "bytes": None}
+
+
+def sources_sha256(paths):
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(hashlib.sha256(f.read()).digest())
+    return h.hexdigest()
 
 
 def recorded_traffic(rec, mix):
-    """A recorded HBM byte count, if its source and launch mix are the ones measured."""
-    if rec is None or rec["mix"] != mix:
+    """A recorded HBM byte count, if its sources and launch mix are the ones measured."""
+    if rec is None or rec["bytes"] is None or rec["mix"] != mix:
         return None
-    with open(rec["source"], "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != rec["sha256"]:
-            return None
+    if sources_sha256(rec["sources"]) != rec["sha256"]:
+        return None
     return rec["bytes"]
 
 
@@ -103,8 +117,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--ratios", default="0.25,0.5,0.75,1.0")
     p.add_argument("--workload", default="layer_8b")
-    p.add_argument("--cpu-tokens", type=int, default=6144,
-                   help="tokens of the bounded CPU-oracle sample")
+    p.add_argument("--cpu-tokens", type=int, default=0,
+                   help="tokens of the CPU-oracle sample (default: the whole layer)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-fused-attention", action="store_true",
                    help="skip the separate timing of the fused attention block")
@@ -665,7 +679,9 @@ def time_decode(L, r, steps, warmup, B=1):
 # ---------------------------------------------------------- CPU baseline
 
 def cpu_baseline(wk, tokens, r):
-    """The CPU oracle on the first `tokens` tokens of the same workload."""
+    """The CPU oracle on the first `tokens` tokens of the same workload (all
+    of them by default): the seven projections, then the per-head QK^T, each
+    timed on its own."""
     import oracle.rmm_oracle as ro
     import workloads as wl
     try:
@@ -680,21 +696,39 @@ def cpu_baseline(wk, tokens, r):
     q, k = wl.workload_qk(wk, L=tokens)
     Q = wl.decode(wl.f32_to_bf16_bits(q), "bf16")
     Kc = wl.decode(wl.f32_to_bf16_bits(k), "bf16")
+    del q, k
     a = wk.attention
-    flop = 0
     t0 = time.perf_counter()
+    f_proj = 0
     for p in wk.projections:
         Y, idx, _ = ro.rmm(X[p.input_name], W[p.name], r)
-        flop += 2 * tokens * p.N * len(idx)
-    H, Hkv = a.H, a.Hkv
+        f_proj += 2 * tokens * p.N * len(idx)
+        del Y
+    t1 = time.perf_counter()
     S, qidx, _ = ro.rmm_qk(Q, Kc, r, True)
-    flop += 2 * H * (tokens * (tokens + 1) // 2) * qidx.shape[1]
-    dt = time.perf_counter() - t0
-    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(blas_threads),
+    f_qk = 2 * a.H * (tokens * (tokens + 1) // 2) * qidx.shape[1]
+    del S
+    t2 = time.perf_counter()
+    dt = t2 - t0
+    scope = "all" if tokens == wk.M else f"the first {tokens} of {wk.M}"
+    return {"value": (f_proj + f_qk) / dt / 1e12, "unit": "TFLOP/s", "cores": int(blas_threads),
             "kind": "oracle",
-            "sample": (f"first {tokens} of {wk.M} tokens of the same layer (all 7 projections "
-                       f"+ per-head QK^T, r={r}); {flop / 1e9:.1f} retained GFLOP in {dt:.1f} s; "
+            "projections": {"gflop": round(f_proj / 1e9, 1), "s": round(t1 - t0, 2),
+                            "tflops": round(f_proj / (t1 - t0) / 1e12, 4)},
+            "qk": {"gflop": round(f_qk / 1e9, 1), "s": round(t2 - t1, 2),
+                   "tflops": round(f_qk / (t2 - t1) / 1e12, 4)},
+            "sample": (f"{scope} tokens of the same layer (all 7 projections + per-head QK^T, "
+                       f"r={r}); {(f_proj + f_qk) / 1e9:.1f} retained GFLOP in {dt:.1f} s; "
                        f"float64, BLAS threads={blas_threads}, host cpus={os.cpu_count()}")}
+
+
+def child_processes():
+    """Processes this run started that are still alive (none expected)."""
+    try:
+        import psutil
+        return [f"{c.pid}:{c.name()}" for c in psutil.Process().children(recursive=True)]
+    except Exception as e:                              # psutil missing
+        return [f"unknown ({type(e).__name__})"]
 
 
 # ------------------------------------------------------------------ main
@@ -761,7 +795,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wk.name}: {wk.description}", "seq_len": wk.M, "batch": 1,
                    "r": HEADLINE_R, "projections": [p.name for p in wk.projections],
-                   "attention": "per-head reduced QK^T, causal, 32 q / 8 kv heads, d=128"},
+                   "attention": f"per-head reduced QK^T, causal, {wk.attention.H} q / "
+                                f"{wk.attention.Hkv} kv heads, d={wk.attention.D}"},
         "speedup_vs_r1": round(head["speedup_vs_r1"], 3) if base else None,
         "sweep": {str(r): {k: (round(v, 4) if isinstance(v, float) else v)
                            for k, v in rec.items()} for r, rec in sweep.items()},
@@ -801,7 +836,8 @@ def main():
         a_h, a_1 = att.get(HEADLINE_R), att.get(1.0)
         out["fused_attention"] = {
             "op": "softmax(reduced QK^T + causal mask) V per head, S never written; "
-                  "32 q / 8 kv heads, seq 8192, d=128, V dense",
+                  f"{wk.attention.H} q / {wk.attention.Hkv} kv heads, seq {wk.M}, "
+                  f"d={wk.attention.D}, V dense",
             "kernels": ["attn_compact_k_kernel", "attn_fwd_kernel"],
             "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
                                    for k, v in rec.items()} for r, rec in att.items()},
@@ -872,7 +908,9 @@ def main():
                          "achieved": round(p_b / (p_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(p_b / (p_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
                          "bytes_basis": "one read of X + one write of Xt + the energies per call",
-                         "traffic": None},
+                         "traffic": recorded_traffic(
+                             NORM_TRAFFIC, f"{wk.name} attn_in,mlp_in r={','.join(str(r) for r in sorted(sweep))}"),
+                         "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, all three kernels)"},
         }
     if not args.no_decode:
         dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}
@@ -919,7 +957,8 @@ def main():
         out["pv_token"] = {
             "op": "token-axis reduced value product per query head: TopK of the column norms "
                   "of the attention weights P (softmax of the layer's causal scores), then "
-                  "P[:, T] V[T, :]; 32 q / 8 kv heads, seq 8192, d=128",
+                  f"P[:, T] V[T, :]; {wk.attention.H} q / {wk.attention.Hkv} kv heads, "
+                  f"seq {wk.M}, d={wk.attention.D}",
             "kernels": ["score_tile_kernel", "score_finalize_kernel", "select_kernel",
                         "gemm_kmajor_tr_kernel"],
             "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
@@ -933,8 +972,10 @@ def main():
                          "bytes_basis": "one read of P + kept V rows + O per call"},
         }
     if not args.no_cpu_baseline:
-        print(f"# CPU oracle on {args.cpu_tokens} tokens ...", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wk, args.cpu_tokens, HEADLINE_R)
+        tokens = args.cpu_tokens or wk.M
+        print(f"# CPU oracle on {tokens} tokens ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wk, tokens, HEADLINE_R)
+    out["children_at_exit"] = child_processes()
     print(json.dumps(out), flush=True)
 
 
