@@ -132,6 +132,8 @@ def parse():
                    help="skip the steps with per-component retention ratios")
     p.add_argument("--no-norm-chain", action="store_true",
                    help="skip the timing of the RMSNorm -> projection chains")
+    p.add_argument("--no-pv-chain", action="store_true",
+                   help="skip the timing of the scores -> weights -> token-axis value product chain")
     p.add_argument("--no-pv", action="store_true",
                    help="skip the separate timing of the token-axis reduced value product")
     p.add_argument("--copy-probe-mib", type=int, default=0,
@@ -519,6 +521,58 @@ def time_norm_chain(L, name, r, steps, warmup, eps=1e-5):
             "speedup_without_norm": (us["unfused"] - us["torch_norm"]) / us["fused"],
             "producer_bytes": nbytes, "producer_gbs": nbytes / (us["producer"] * 1e-6) / 1e9,
             "calls": steps}
+
+
+def time_pv_chain(L, r, steps, warmup, bufs):
+    """The value product fed by its producer, on the layer's causal scores S
+    (the sweep's last ratio: r = 1 in the default run) and values V:
+      reduced : rmm_attention_weights_kmajor (softmax weights written K-major
+                with their token energies; the masked half of S is never
+                read) -> TopK of the token energies per head ->
+                rmm_reduced_pv_kmajor (kept token rows, causal row tiles
+                stopped at their last visible token);
+      dense   : torch softmax of S (row-major weights) -> torch P @ V (V
+                repeated over each kv head's query heads).
+    Every call is bracketed by HIP events; the producer and the product are
+    also timed alone."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    a = L.wk.attention
+    kt = rmm.rmm_retained_count(r, a.L)
+    Pt, e, ws, P, Vr = bufs["Pt"], bufs["e"], bufs["ws"], bufs["P"], bufs["Vr"]
+    idx = torch.empty(a.H * kt, dtype=torch.int32, device=L.dev)
+
+    def producer():
+        rmm.rmm_attention_weights_kmajor(L.S, Pt, e, causal=True, workspace=ws)
+
+    def product():
+        rmm.rmm_reduced_pv_kmajor(Pt, L.V, idx.view(a.H, kt), L.O, causal=True)
+
+    def reduced():
+        producer()
+        rmm.rmm_select(e, kt, idx)
+        product()
+
+    def dense():
+        torch.softmax(L.S[0], dim=-1, out=P)
+        torch.matmul(P, Vr, out=bufs["Od"])
+
+    us = {n: time_calls(f, steps, warmup) for n, f in
+          (("reduced", reduced), ("producer", producer), ("product", product))}
+    # bytes of the producer: the causal part of S read once, the part of Pt
+    # it stores (the lower triangle and, above the diagonal, the zeros of the
+    # 256-query block holding each column's diagonal), the energies
+    pairs = a.L * (a.L + 1) // 2
+    stored = sum(a.L - 256 * (t // 256) for t in range(a.L))
+    nbytes = a.H * (pairs * 2 + stored * 2 + a.L * 8)
+    rec = {"r": r, "kt": kt, "reduced_us": us["reduced"], "producer_us": us["producer"],
+           "product_us": us["product"], "producer_bytes": nbytes,
+           "producer_gbs": nbytes / (us["producer"] * 1e-6) / 1e9, "calls": steps}
+    if bufs.get("dense_us") is None:
+        bufs["dense_us"] = time_calls(dense, steps, warmup)
+    rec["dense_torch_us"] = bufs["dense_us"]
+    rec["speedup_vs_dense_torch"] = bufs["dense_us"] / us["reduced"]
+    return rec
 
 
 def attention_weights(L):
@@ -935,6 +989,48 @@ def main():
             "roofline": {"bound": "hbm", "kernel": "gemv_partial_kernel (+ gemv_reduce_kernel)",
                          "achieved": round(d_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(d_ach / PEAK_HBM_GBS, 4), "traffic": None},
+        }
+    if not args.no_pv_chain:
+        import torch
+        import paper_2608_13426_amd as rmm
+        a = wk.attention
+        bufs = {"Pt": torch.empty((1, a.H, a.L, a.L), dtype=torch.bfloat16, device=L.dev),
+                "e": torch.empty(a.H * a.L, dtype=torch.float64, device=L.dev),
+                "ws": torch.empty(rmm.rmm_attention_weights_kmajor_workspace_size(1, a.H, a.L, a.L),
+                                  dtype=torch.uint8, device=L.dev),
+                "P": torch.empty((a.H, a.L, a.L), dtype=torch.bfloat16, device=L.dev),
+                "Vr": L.V[0].repeat_interleave(a.H // a.Hkv, dim=0).contiguous(),
+                "Od": torch.empty((a.H, a.L, a.D), dtype=torch.bfloat16, device=L.dev)}
+        pc = {r: time_pv_chain(L, r, args.steps, args.warmup, bufs) for r in sorted(sweep)}
+        del bufs
+        torch.cuda.empty_cache()
+        for r, rec in pc.items():
+            print(f"# PV chain r={r}: reduced {rec['reduced_us']:.1f} us (producer "
+                  f"{rec['producer_us']:.1f} us at {rec['producer_gbs']:.0f} GB/s, product "
+                  f"{rec['product_us']:.1f} us); dense torch softmax + P@V {rec['dense_torch_us']:.1f} us",
+                  file=sys.stderr, flush=True)
+        c_h, c_1 = pc.get(HEADLINE_R), pc.get(1.0)
+        p_us = sum(v["producer_us"] for v in pc.values())
+        p_b = sum(v["producer_bytes"] for v in pc.values())
+        out["pv_chain"] = {
+            "op": "scores -> attention weights -> token-axis reduced value product per query head: "
+                  "reduced = rmm_attention_weights_kmajor (weights K-major + token energies, the "
+                  "causally masked half of S not read), TopK per head, rmm_reduced_pv_kmajor (kept "
+                  "token rows, causal row tiles trimmed); dense = torch softmax + torch P @ V; "
+                  f"{a.H} q / {a.Hkv} kv heads, seq {wk.M}, d={a.D}",
+            "kernels": ["softmax_rowstats_kernel", "score_tile_kernel (softmax variant)",
+                        "score_finalize_kernel", "select_kernel", "gemm_kmajor_tr_kernel (256x128)"],
+            "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
+                                   for k, v in rec.items()} for r, rec in pc.items()},
+            "speedup_vs_r1": round(c_1["reduced_us"] / c_h["reduced_us"], 3) if c_1 and c_h else None,
+            "speedup_vs_dense_torch": round(c_h["speedup_vs_dense_torch"], 3) if c_h else None,
+            "roofline": {"bound": "hbm", "kernel": "rmm_attention_weights_kmajor (all three kernels)",
+                         "achieved": round(p_b / (p_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(p_b / (p_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                         "bytes_basis": "the causal part of S read once + the stored part of Pt + "
+                                        "energies per call (the implementation reads S twice: row "
+                                        "statistics, then the weights)",
+                         "traffic": None},
         }
     if not args.no_pv:
         import torch

@@ -495,6 +495,69 @@ rmm_status_t rmm_linear_noalloc(const void *X, const void *W, double r, rmm_dtyp
                                 int64_t ldw, void *Y, int64_t ldy, int32_t *idx_out,
                                 hipStream_t stream);
 
+/*
+ * Attention weights written K-major with their token energies   (Sec. 3.3,
+ * attention: the token-axis reduction of the value product ranks tokens by
+ * the column norms of the attention weights P = softmax(S + M); the
+ * Limitations section names the memory movement of a separate scoring pass
+ * as a cost to remove).
+ *
+ * For every unit u = b*H + h (query head) and query row i:
+ *   kept(i, t)   = S[u][i][t] > -inf, and t <= i + (Lk - Lq) when causal
+ *   rmax_i       = max over kept t of S[u][i][t],   rsum_i = sum over kept t
+ *                  of exp(S[u][i][t] - rmax_i)                          (fp32)
+ *   Pt[u][t][i]  = bf16(exp(S[u][i][t] - rmax_i) / rsum_i) where kept, else 0
+ *                  (a row with nothing kept is all zero); with the causal
+ *                  mask the zeros above the diagonal are written only where
+ *                  i >= 256 * floor((t - (Lk - Lq)) / 256), the 256-query
+ *                  block holding column t's diagonal (what
+ *                  rmm_reduced_pv_kmajor reads); Pt[u][t][i] for smaller i
+ *                  is left as it was
+ *   energy[u][t] = sum over i < Lq of Pt[u][t][i]^2    (float64 sums of exact
+ *                  squares in a fixed order; orders tokens like ||P[:, t]||)
+ * With the causal mask the masked scores are never read.  Feed the energies
+ * to rmm_select (B = batch*H, K = Lk) and the sets to rmm_reduced_pv_kmajor.
+ *
+ * S     : bf16 [batch][H][Lq][lds], lds >= Lk (e.g. rmm_reduced_qk's output).
+ * Pt    : bf16 [batch][H][Lk][ldpt], ldpt >= Lq; columns Lq.. are not written.
+ * energy: float64 [batch*H*Lk].
+ * workspace : rmm_attention_weights_kmajor_workspace_size(batch, H, Lq, Lk)
+ *         bytes, 256-byte aligned (row statistics and partial energies).
+ * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, lds < Lk, ldpt < Lq,
+ *         a misaligned workspace; UNSUPPORTED unless S and Pt are 16-byte
+ *         aligned, lds and ldpt are multiples of 8 and batch*H <= 65535;
+ *         WORKSPACE_TOO_SMALL.
+ */
+size_t rmm_attention_weights_kmajor_workspace_size(int64_t batch, int64_t H, int64_t Lq, int64_t Lk);
+rmm_status_t rmm_attention_weights_kmajor(const void *S, int64_t batch, int64_t H, int64_t Lq,
+                                          int64_t Lk, int64_t lds, int causal, void *Pt,
+                                          int64_t ldpt, double *energy, void *workspace,
+                                          size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Token-axis reduced value product from K-major weights   (Sec. 3.3: O =
+ * P[:, T] V[T, :] with the kept tokens T of each query head; App. D: its
+ * MACs scale with rho_t).
+ *
+ *   O[u][i][d] = sum over t in T_u of Pt[u][t][i] * V[v(u)][t][d]
+ *
+ * with T_u = idx[u*kt .. u*kt + kt) (ascending, from rmm_select on the
+ * energies of rmm_attention_weights_kmajor) and v(u) = b*Hkv + h/(H/Hkv).
+ * With causal != 0 the caller states that Pt[u][t][i] = 0 for t > i + (Lk -
+ * Lq) (true of rmm_attention_weights_kmajor's causal output); the products
+ * of those zeros are then skipped, whole 256-query tiles at a time.
+ *
+ * Pt : bf16 [batch][H][Lk][ldpt], ldpt >= Lq.   V : bf16 [batch][Hkv][Lk][D].
+ * O  : bf16 [batch][H][Lq][D], written.
+ * Errors: INVALID_ARGUMENT for null pointers, sizes < 1, H % Hkv != 0, kt
+ *         outside [1, Lk], ldpt < Lq; UNSUPPORTED unless Pt and V are 16-byte
+ *         aligned, ldpt and D are multiples of 8, Lk*ldpt*2 and Lk*D*2 are
+ *         below 2^31 and batch*H <= 65535.
+ */
+rmm_status_t rmm_reduced_pv_kmajor(const void *Pt, const void *V, const int32_t *idx, int64_t batch,
+                                   int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                                   int64_t kt, int64_t ldpt, int causal, void *O, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);
 

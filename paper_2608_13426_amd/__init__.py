@@ -22,7 +22,8 @@ __all__ = [
     "rmm_reduced_qk", "rmm_linear", "rmm_score_kmajor", "rmm_reduced_gemm_kmajor",
     "rmm_reduced_attention", "rmm_reduced_gemv", "rmm_gemv_workspace_size", "rmm_select_tokens",
     "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "rmm_rmsnorm_kmajor",
-    "rmm_rmsnorm_kmajor_workspace_size", "EXPORTED_SYMBOLS",
+    "rmm_rmsnorm_kmajor_workspace_size", "rmm_attention_weights_kmajor",
+    "rmm_attention_weights_kmajor_workspace_size", "rmm_reduced_pv_kmajor", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -51,6 +52,11 @@ _SIGS = {
     "rmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "rmm_noalloc_scratch_bytes": (ctypes.c_size_t, []),
     "rmm_rmsnorm_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64]),
+    "rmm_attention_weights_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64]),
+    "rmm_attention_weights_kmajor": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _i64, ctypes.c_int,
+                                                    _p, _i64, _p, _p, ctypes.c_size_t, _p]),
+    "rmm_reduced_pv_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
+                                             _i64, ctypes.c_int, _p, _p]),
     "rmm_rmsnorm_kmajor": (ctypes.c_int, [_p, _p, ctypes.c_float, _i64, _i64, _i64, _i64, _p, _i64,
                                           _p, _p, ctypes.c_size_t, _p]),
     "rmm_linear_noalloc": (ctypes.c_int, [_p, _p, ctypes.c_double, ctypes.c_int, _i64, _i64, _i64,
@@ -628,3 +634,63 @@ def rmm_rmsnorm_kmajor(X: torch.Tensor, gamma: torch.Tensor, eps: float, Xt: tor
         X.data_ptr(), gamma.data_ptr(), float(eps), B, M, K, ldx, Xt.data_ptr(), ldxt,
         energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
     return Xt
+
+
+def rmm_attention_weights_kmajor_workspace_size(batch: int, H: int, Lq: int, Lk: int) -> int:
+    return int(lib.rmm_attention_weights_kmajor_workspace_size(batch, H, Lq, Lk))
+
+
+def rmm_attention_weights_kmajor(S: torch.Tensor, Pt: torch.Tensor, energy: torch.Tensor,
+                                 causal: bool = True, workspace: torch.Tensor | None = None,
+                                 stream=None) -> torch.Tensor:
+    """Softmax weights of the scores S [batch, H, Lq, Lk] written K-major into
+    Pt [batch, H, Lk, Lq] (row stride Pt.stride(-2)), with their token
+    energies (float64 [batch*H*Lk])."""
+    if S.dim() != 4 or Pt.dim() != 4:
+        raise ValueError("S and Pt must be 4-D")
+    batch, H, Lq, Lk = S.shape
+    d = _dev(S, Pt, energy)
+    if tuple(Pt.shape) != (batch, H, Lk, Lq):
+        raise ValueError("Pt must be [batch, H, Lk, Lq]")
+    if S.stride(3) != 1 or S.stride(1) != Lq * S.stride(2) or S.stride(0) != H * Lq * S.stride(2):
+        raise ValueError("S rows must be contiguous and its heads packed")
+    if Pt.stride(3) != 1 or Pt.stride(1) != Lk * Pt.stride(2) or Pt.stride(0) != H * Lk * Pt.stride(2):
+        raise ValueError("Pt rows must be contiguous and its heads packed")
+    if not (S.dtype == Pt.dtype == torch.bfloat16):
+        raise TypeError("S and Pt must be bfloat16")
+    if energy.dtype != torch.float64 or energy.numel() != batch * H * Lk or not energy.is_contiguous():
+        raise ValueError("energy must be contiguous float64 [batch*H*Lk]")
+    if workspace is None:
+        workspace = torch.empty(max(rmm_attention_weights_kmajor_workspace_size(batch, H, Lq, Lk), 1),
+                                dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_attention_weights_kmajor", lib.rmm_attention_weights_kmajor(
+        S.data_ptr(), batch, H, Lq, Lk, S.stride(2), 1 if causal else 0, Pt.data_ptr(), Pt.stride(2),
+        energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    return Pt
+
+
+def rmm_reduced_pv_kmajor(Pt: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, O: torch.Tensor,
+                          causal: bool = True, stream=None) -> torch.Tensor:
+    """O[b, h] = Pt[b, h][T, :]^T V[b, h // (H/Hkv)][T, :] with the token sets
+    idx [batch*H, kt] (ascending)."""
+    if Pt.dim() != 4 or V.dim() != 4 or O.dim() != 4:
+        raise ValueError("Pt, V and O must be 4-D")
+    batch, H, Lk, Lq = Pt.shape
+    _, Hkv, Lkv, D = V.shape
+    d = _dev(Pt, V, idx, O)
+    if Lkv != Lk or tuple(O.shape) != (batch, H, Lq, D) or H % Hkv:
+        raise ValueError("shapes: Pt [b, H, Lk, Lq], V [b, Hkv, Lk, D], O [b, H, Lq, D]")
+    if Pt.stride(3) != 1 or Pt.stride(1) != Lk * Pt.stride(2) or Pt.stride(0) != H * Lk * Pt.stride(2):
+        raise ValueError("Pt rows must be contiguous and its heads packed")
+    if not (V.is_contiguous() and O.is_contiguous()):
+        raise ValueError("V and O must be contiguous")
+    if not (Pt.dtype == V.dtype == O.dtype == torch.bfloat16):
+        raise TypeError("Pt, V and O must be bfloat16")
+    if idx.dtype != torch.int32 or not idx.is_contiguous() or idx.numel() % (batch * H):
+        raise ValueError("idx must be contiguous int32 [batch*H, kt]")
+    kt = idx.numel() // (batch * H)
+    _check("rmm_reduced_pv_kmajor", lib.rmm_reduced_pv_kmajor(
+        Pt.data_ptr(), V.data_ptr(), idx.data_ptr(), batch, H, Hkv, Lq, Lk, D, kt, Pt.stride(2),
+        1 if causal else 0, O.data_ptr(), _stream(d, stream)))
+    return O

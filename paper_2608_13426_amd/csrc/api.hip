@@ -426,9 +426,8 @@ rmm_status_t rmm_reduced_pv(const void *P, const void *V, rmm_dtype_t dtype, int
         // one launch over every query head, each reading its kv head's rows of V
         e = rmm::launch_gemm_kmajor_grouped_bf16(Pt, static_cast<const uint16_t *>(V), idx, U, Lq, D,
                                                  Lk, kt, xt_ld(Lq), D, static_cast<uint16_t *>(O), D,
-                                                 Lk * D, static_cast<int>(grp), stream);
-        if (e != hipErrorNotSupported) return from_hip(e);
-        e = hipSuccess;
+                                                 Lk * D, static_cast<int>(grp), 0, 0, stream);
+        return e == hipErrorNotSupported ? RMM_ERR_UNSUPPORTED : from_hip(e);
     }
     for (int64_t b = 0; b < batch && e == hipSuccess; ++b)
         for (int64_t g = 0; g < Hkv && e == hipSuccess; ++g) {
@@ -450,6 +449,52 @@ rmm_status_t rmm_reduced_pv(const void *P, const void *V, rmm_dtype_t dtype, int
                                          ldp, D, reinterpret_cast<float *>(Og), D, stream);
         }
     return from_hip(e);
+}
+
+size_t rmm_attention_weights_kmajor_workspace_size(int64_t batch, int64_t H, int64_t Lq, int64_t Lk) {
+    if (batch < 1 || H < 1 || Lq < 1 || Lk < 1) return 0;
+    return align256(rmm::weights_workspace_bytes(batch * H, Lq, Lk));
+}
+
+rmm_status_t rmm_attention_weights_kmajor(const void *S, int64_t batch, int64_t H, int64_t Lq,
+                                          int64_t Lk, int64_t lds, int causal, void *Pt,
+                                          int64_t ldpt, double *energy, void *workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+    if (!S || !Pt || !energy) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Lq < 1 || Lk < 1 || lds < Lk || ldpt < Lq) return RMM_ERR_INVALID_ARGUMENT;
+    if (Lq > kInt32Max || Lk > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    const int64_t U = batch * H;
+    if (U > kGridYZMax) return RMM_ERR_UNSUPPORTED;
+    if (!aligned16(S) || !aligned16(Pt) || lds % 8 || ldpt % 8 ||
+        reinterpret_cast<uintptr_t>(energy) % 8)
+        return RMM_ERR_UNSUPPORTED;
+    // the tile kernel addresses one row split with 32-bit byte offsets
+    if (rmm::score_rows_per_split(U, Lq, Lk) * lds * 2 >= (int64_t(1) << 31)) return RMM_ERR_UNSUPPORTED;
+    const size_t need = rmm_attention_weights_kmajor_workspace_size(batch, H, Lq, Lk);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
+    return from_hip(rmm::launch_attention_weights_kmajor(
+        static_cast<const uint16_t *>(S), U, Lq, Lk, lds, causal != 0, static_cast<uint16_t *>(Pt), ldpt,
+        energy, workspace, stream));
+}
+
+rmm_status_t rmm_reduced_pv_kmajor(const void *Pt, const void *V, const int32_t *idx, int64_t batch,
+                                   int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                                   int64_t kt, int64_t ldpt, int causal, void *O, hipStream_t stream) {
+    if (!Pt || !V || !idx || !O) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (H % Hkv != 0 || kt < 1 || kt > Lk || ldpt < Lq) return RMM_ERR_INVALID_ARGUMENT;
+    if (Lq > kInt32Max || Lk > kInt32Max || D > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    const int64_t U = batch * H, grp = H / Hkv;
+    if (U > kGridYZMax || !kmajor_ok(Pt, V, U, Lq, Lk, ldpt, D)) return RMM_ERR_UNSUPPORTED;
+    const uint16_t *pt = static_cast<const uint16_t *>(Pt), *v = static_cast<const uint16_t *>(V);
+    uint16_t *o = static_cast<uint16_t *>(O);
+    // one launch over every query head; with the causal mask each row tile
+    // stops at the last kept token any of its queries can see
+    const hipError_t e = rmm::launch_gemm_kmajor_grouped_bf16(
+        pt, v, idx, U, Lq, D, Lk, kt, ldpt, D, o, D, Lk * D, static_cast<int>(grp), causal != 0, Lk - Lq,
+        stream);
+    return e == hipErrorNotSupported ? RMM_ERR_UNSUPPORTED : from_hip(e);
 }
 
 const char *rmm_status_string(rmm_status_t status) {

@@ -555,7 +555,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void gemm_kmajor_tr_kernel(
     const uint16_t *__restrict__ Xt, const uint16_t *__restrict__ W,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ Y, int M, int N, int k,
     int64_t ldxt, int64_t ldw, int64_t ldy, int64_t xt_bytes, int64_t w_bytes, int tiles_m,
-    int tiles_n, int vec_y, double *__restrict__ part, int64_t w_ustride = 0, int w_ugroup = 1) {
+    int tiles_n, int vec_y, double *__restrict__ part, int64_t w_ustride = 0, int w_ugroup = 1,
+    int trim = 0, int64_t trim_off = 0) {
     using namespace trk;
     constexpr int ASZ = BKS * ROWB;      // X operand, one stage
     constexpr int ROWBB = BNT * 2;       // bytes per staged W row
@@ -605,6 +606,19 @@ __global__ __launch_bounds__(NW * 64, OCC) void gemm_kmajor_tr_kernel(
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int32_t *I = idx + unit * k;
+    // trim: X is zero at (m, j) for j > m + trim_off (a causal operand), so
+    // the retained indices past this tile's last row's limit add nothing and
+    // the K loop stops before them (I is ascending: a binary search)
+    int kk = k;
+    if (trim) {
+        const int64_t jmax = static_cast<int64_t>(m0) + BT - 1 + trim_off;
+        int lo = 0, hi = k;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (static_cast<int64_t>(I[mid]) <= jmax) lo = mid + 1; else hi = mid;
+        }
+        kk = __builtin_amdgcn_readfirstlane(lo);
+    }
 
     constexpr uint32_t kOut = 0x80000000u;
     const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
@@ -637,14 +651,14 @@ __global__ __launch_bounds__(NW * 64, OCC) void gemm_kmajor_tr_kernel(
     auto stage_idx = [&](int st, int32_t (&r)[2 * PPW]) {
         const int base = st * BKS + 2 * wave * PPW;
 #pragma unroll
-        for (int e = 0; e < 2 * PPW; ++e) r[e] = I[min(base + e, k - 1)];
+        for (int e = 0; e < 2 * PPW; ++e) r[e] = I[min(base + e, k - 1)];   // positions >= kk: masked
     };
     auto dma = [&](auto slot, int st, const int32_t (&r)[2 * PPW]) {
         char *la = stage_a(slot), *lb = stage_b(slot);
         const int base = st * BKS + 2 * wave * PPW;
 #pragma unroll
         for (int q = 0; q < PPW; ++q) {
-            const bool in = base + 2 * q + h < k;
+            const bool in = base + 2 * q + h < kk;
             const uint32_t j = static_cast<uint32_t>(h ? r[2 * q + 1] : r[2 * q]);
             const int P = wave * PPW + q;
             const uint32_t ao = in ? j * arow + acol[P & 1] : kOut;
@@ -658,7 +672,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void gemm_kmajor_tr_kernel(
 #pragma unroll
             for (int q = 0; q < BLD; ++q) {
                 const int local = RPB * q + bq;           // row within the wave's 2*PPW
-                const bool in = base + local < k;
+                const bool in = base + local < kk;
                 uint32_t j = static_cast<uint32_t>(r[0]);
 #pragma unroll
                 for (int e = 1; e < 2 * PPW; ++e)
@@ -702,7 +716,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void gemm_kmajor_tr_kernel(
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.f;
 
-    const int nT = (k + BKS - 1) / BKS;
+    const int nT = (kk + BKS - 1) / BKS;
     int32_t r[2 * PPW];
     // a barrier that orders this wave's LDS accesses around it but, unlike
     // __syncthreads(), does not wait for the loads still landing in LDS
@@ -1060,17 +1074,18 @@ constexpr int kTrWaves = 8, kTrRows = 32, kTrStages = 3;
 namespace {
 
 // The K-major GEMM over B units; units u read W + (u / w_ugroup) * w_ustride.
-// Returns hipErrorNotSupported (launching nothing) when grouped weights are
-// asked of the kernels without that addressing (fewer than 128 large tiles).
+// Grouped weights and K-loop trimming exist only in the large-tile kernel,
+// which then serves small problems too; hipErrorNotSupported (nothing
+// launched) when they are asked for with Y rows too long for its addressing.
 hipError_t kmajor_dispatch(const uint16_t *Xt, const uint16_t *W, const int32_t *idx, int64_t B,
                            int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldxt, int64_t ldw,
                            uint16_t *Y, int64_t ldy, int64_t w_ustride, int w_ugroup,
-                           hipStream_t stream) {
+                           int trim, int64_t trim_off, hipStream_t stream) {
     const int64_t xt_bytes = K * ldxt * 2, w_bytes = K * ldw * 2;
     const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
-    const bool grouped = w_ustride != 0 && w_ugroup < B;
+    const bool grouped = (w_ustride != 0 && w_ugroup < B) || trim;
     // Y rows of one 256-row tile are addressed with 32-bit byte offsets
-    if (t256 * B >= 128 && ldy < (int64_t(1) << 23)) {
+    if ((t256 * B >= 128 || grouped) && ldy < (int64_t(1) << 23)) {
         const int vec_y = (reinterpret_cast<uintptr_t>(Y) % 16 == 0 && ldy % 8 == 0) ? 2
                           : (reinterpret_cast<uintptr_t>(Y) % 8 == 0 && ldy % 4 == 0) ? 1 : 0;
         const int tm = static_cast<int>((M + 255) / 256);
@@ -1080,7 +1095,7 @@ hipError_t kmajor_dispatch(const uint16_t *Xt, const uint16_t *W, const int32_t 
                                dim3(tm, static_cast<unsigned>(B)), dim3(4 * 64), 0, stream,
                                Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
                                static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, 1, vec_y,
-                               nullptr, w_ustride, w_ugroup);
+                               nullptr, w_ustride, w_ugroup, trim, trim_off);
             return hipGetLastError();
         }
         const int tn = static_cast<int>((N + 255) / 256);
@@ -1088,7 +1103,7 @@ hipError_t kmajor_dispatch(const uint16_t *Xt, const uint16_t *W, const int32_t 
                            dim3(tm * tn, static_cast<unsigned>(B)), dim3(kTrWaves * 64), 0, stream,
                            Xt, W, idx, Y, static_cast<int>(M), static_cast<int>(N),
                            static_cast<int>(k), ldxt, ldw, ldy, xt_bytes, w_bytes, tm, tn, vec_y,
-                           nullptr, w_ustride, w_ugroup);
+                           nullptr, w_ustride, w_ugroup, trim, trim_off);
         return hipGetLastError();
     }
     if (grouped) return hipErrorNotSupported;
@@ -1114,14 +1129,16 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                                   int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                                   int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
                                   hipStream_t stream) {
-    return kmajor_dispatch(Xt, W, idx, B, M, N, K, k, ldxt, ldw, Y, ldy, 0, 1, stream);
+    return kmajor_dispatch(Xt, W, idx, B, M, N, K, k, ldxt, ldw, Y, ldy, 0, 1, 0, 0, stream);
 }
 
 hipError_t launch_gemm_kmajor_grouped_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
                                           int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                                           int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
-                                          int64_t w_ustride, int w_ugroup, hipStream_t stream) {
-    return kmajor_dispatch(Xt, W, idx, B, M, N, K, k, ldxt, ldw, Y, ldy, w_ustride, w_ugroup, stream);
+                                          int64_t w_ustride, int w_ugroup, int trim, int64_t trim_off,
+                                          hipStream_t stream) {
+    return kmajor_dispatch(Xt, W, idx, B, M, N, K, k, ldxt, ldw, Y, ldy, w_ustride, w_ugroup, trim,
+                           trim_off, stream);
 }
 
 hipError_t launch_gemm_swiglu_kmajor_bf16(const uint16_t *Xt, const uint16_t *W,

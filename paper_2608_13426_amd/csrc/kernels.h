@@ -66,12 +66,30 @@ hipError_t launch_gemm_kmajor_bf16(const uint16_t *Xt, const uint16_t *W, const 
                                   int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
                                   hipStream_t stream);
 // the same product with per-unit weights: unit u reads W + (u / w_ugroup) *
-// w_ustride elements; hipErrorNotSupported (nothing launched) when the
-// problem is too small for the large-tile kernels that address them so
+// w_ustride elements; with trim, Xt is known to be zero at (m, j) for
+// j > m + trim_off and each row tile stops its K loop there;
+// hipErrorNotSupported (nothing launched) when ldy >= 2^23 (the large-tile
+// kernel that implements these addresses Y rows with 32-bit offsets)
 hipError_t launch_gemm_kmajor_grouped_bf16(const uint16_t *Xt, const uint16_t *W, const int32_t *idx,
                                           int64_t B, int64_t M, int64_t N, int64_t K, int64_t k,
                                           int64_t ldxt, int64_t ldw, uint16_t *Y, int64_t ldy,
-                                          int64_t w_ustride, int w_ugroup, hipStream_t stream);
+                                          int64_t w_ustride, int w_ugroup, int trim, int64_t trim_off,
+                                          hipStream_t stream);
+// the transposing scoring pass over attention scores: Pt = the K-major
+// softmax weights exp(s - rmax[m]) * rinv[m] (zero where causal drops j > m +
+// coff), and their column energies
+hipError_t launch_score_softmax_kmajor(const uint16_t *S, int64_t B, int64_t M, int64_t K, int64_t ld,
+                                      const float *rmax, const float *rinv, int64_t coff,
+                                      int causal, double *energy, double *partials, uint16_t *Pt,
+                                      int64_t ldpt, hipStream_t stream);
+// softmax weights of attention scores written K-major with their token
+// energies (bf16 S rows 16-byte aligned; checked by the caller); the
+// workspace (weights_workspace_bytes, 256-byte aligned) holds the row
+// statistics and the scoring partials
+size_t weights_workspace_bytes(int64_t U, int64_t Lq, int64_t Lk);
+hipError_t launch_attention_weights_kmajor(const uint16_t *S, int64_t U, int64_t Lq, int64_t Lk,
+                                           int64_t lds, int causal, uint16_t *Pt, int64_t ldpt,
+                                           double *energy, void *workspace, hipStream_t stream);
 // the gate|up product with the SwiGLU epilogue: W [K][ldw] holds 2F columns
 // in 128-column blocks (gate, then up, of the same 128 channels); writes the
 // down projection's K-major input Ht [B][F][ldht] and its column energies

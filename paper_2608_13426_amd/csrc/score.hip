@@ -156,16 +156,25 @@ __global__ __launch_bounds__(kThreads) void score_partial_kernel(
 constexpr int kStrip = 64;      // columns per workgroup that set the split policy
 constexpr int kTileJC = 8;      // 8-column groups per wave (8: 64 x 64 wave tiles)
 
-// NORM: the values are first normalised as an RMSNorm stores them,
-// y = bf16(gamma[j] * bf16(x * rscale[m])) with the row scale of each row
-// (rscale: one float per row of every unit), and the energies and the
-// K-major copy are those of y.
-template <bool XT, int JC, bool NORM = false>
+// MODE 1 (RMSNorm): the values are first normalised as an RMSNorm stores
+// them, y = bf16(gamma[j] * bf16(x * rscale[m])) with the row scale of each
+// row (rscale: one float per row of every unit).  MODE 2 (softmax): the rows
+// are attention scores and y = bf16(exp(x - rmax[m]) * rinv[m]) (rscale holds
+// rmax, rinv2 the reciprocal row sums; rows of every unit in turn), zero
+// where the causal mask drops (m, j) (causal != 0 and j > m + coff), whose
+// scores are then never read; such zeros are stored in the K-major copy at
+// least where m >= 256 * floor((j - coff) / 256) (the 256-row block of the
+// column's diagonal: what a causal value product reads) and may be left
+// unwritten before it (wave tiles wholly there store nothing).  The energies and the K-major copy are those
+// of y.
+template <bool XT, int JC, int MODE = 0>
 __global__ __launch_bounds__(kThreads) void score_tile_kernel(
     const uint16_t *__restrict__ X, int64_t M, int64_t K, int64_t ldx, int64_t rows_per_split,
     double *__restrict__ out, int64_t out_unit_stride, int64_t out_split_stride,
     uint16_t *__restrict__ Xt, int64_t ldxt, const float *__restrict__ rscale = nullptr,
-    const uint16_t *__restrict__ gamma = nullptr) {
+    const uint16_t *__restrict__ gamma = nullptr, const float *__restrict__ rinv2 = nullptr,
+    int64_t coff = 0, int causal = 0) {
+    constexpr bool NORM = MODE == 1, SOFTMAX = MODE == 2;
     constexpr int MC = 64 / JC, STRIP = 8 * JC, TROWS = 8 * MC;   // wave tile TROWS x STRIP
     __shared__ double red[kThreads / 64][STRIP];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -183,7 +192,8 @@ __global__ __launch_bounds__(kThreads) void score_tile_kernel(
     const uint32_t col_off = nvalid > 0 ? static_cast<uint32_t>(j * 2) : kOut;
     uint16_t *xt = XT ? Xt + (unit * K + j) * ldxt + r_begin : nullptr;
     float gm[8];
-    const float *rsu = NORM ? rscale + unit * M + r_begin : nullptr;
+    const float *rsu = MODE ? rscale + unit * M + r_begin : nullptr;
+    const float *riu = SOFTMAX ? rinv2 + unit * M + r_begin : nullptr;
     if constexpr (NORM) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) gm[e] = e < nvalid ? bf16_to_f32(gamma[j + e]) : 0.f;
@@ -194,9 +204,20 @@ __global__ __launch_bounds__(kThreads) void score_tile_kernel(
     for (int e = 0; e < 8; ++e) acc[e] = 0.0;
     for (int m0 = wave * TROWS; m0 < rows; m0 += 4 * TROWS) {
         uint4 v[8];
+        // softmax with the causal mask: a wave tile whose every key lies
+        // past its last query's limit reads nothing
+        const int64_t j_first = static_cast<int64_t>(blockIdx.x) * STRIP;
+        const bool skip = SOFTMAX && causal && j_first > r_begin + m0 + TROWS - 1 + coff;
+        // ... and one wholly before its columns' diagonal blocks stores nothing
+        bool unstored = false;
+        if constexpr (SOFTMAX) {
+            const int64_t d = j_first - coff;
+            const int64_t blk = d >= 0 ? d / 256 : -((-d + 255) / 256);
+            unstored = causal && r_begin + m0 + TROWS - 1 < 256 * blk;
+        }
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-            const uint32_t off = col_off == kOut ? kOut
+            const uint32_t off = (col_off == kOut || skip) ? kOut
                                : static_cast<uint32_t>((m0 + 8 * mc + r) * ldx * 2) + col_off;
             const auto q = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
             v[r] = make_uint4(q[0], q[1], q[2], q[3]);
@@ -216,6 +237,25 @@ __global__ __launch_bounds__(kThreads) void score_tile_kernel(
                 v[r] = make_uint4(w[0], w[1], w[2], w[3]);
             }
         }
+        if constexpr (SOFTMAX) {
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int m = m0 + 8 * mc + r;
+                const bool live = m < rows;
+                const float mx = live ? rsu[m] : 0.f, li = live ? riu[m] : 0.f;
+                // keys j + e with j + e <= (r_begin + m) + coff are kept
+                const int64_t lim = causal ? r_begin + m + coff - j : 8;
+                uint32_t w[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float sa = __uint_as_float(w[e] << 16), sb = __uint_as_float(w[e] & 0xffff0000u);
+                    const float pa = (2 * e <= lim && li > 0.f) ? __expf(sa - mx) * li : 0.f;
+                    const float pb = (2 * e + 1 <= lim && li > 0.f) ? __expf(sb - mx) * li : 0.f;
+                    w[e] = pack_bf16x2(pa, pb);
+                }
+                v[r] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
             const uint32_t w[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
@@ -227,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void score_tile_kernel(
                 acc[e] = fma(x, x, acc[e]);
             }
         }
-        if constexpr (XT) {
+        if (XT && !unstored) {
             // column e of the 8 x 8 block becomes one 16-byte vector of Xt row j + e
             const int mrow = m0 + 8 * mc;
 #pragma unroll
@@ -308,8 +348,22 @@ hipError_t launch_tiles_norm(const uint16_t *X, int64_t B, int64_t M, int64_t K,
     constexpr int strip = 8 * kTileJC;
     dim3 grid(static_cast<unsigned>((K + strip - 1) / strip), static_cast<unsigned>(S),
               static_cast<unsigned>(B));
-    hipLaunchKernelGGL((score_tile_kernel<true, kTileJC, true>), grid, dim3(kThreads), 0, stream, X, M,
+    hipLaunchKernelGGL((score_tile_kernel<true, kTileJC, 1>), grid, dim3(kThreads), 0, stream, X, M,
                        K, ldx, rps, out, unit_stride, split_stride, Xt, ldxt, rscale, gamma);
+    return hipGetLastError();
+}
+
+hipError_t launch_tiles_softmax(const uint16_t *S, int64_t B, int64_t M, int64_t K, int64_t ld,
+                                int64_t splits, double *out, int64_t unit_stride, int64_t split_stride,
+                                uint16_t *Pt, int64_t ldpt, const float *rmax, const float *rinv,
+                                int64_t coff, int causal, hipStream_t stream) {
+    const int64_t rps = score_rows_per_split(B, M, K);
+    constexpr int strip = 8 * kTileJC;
+    dim3 grid(static_cast<unsigned>((K + strip - 1) / strip), static_cast<unsigned>(splits),
+              static_cast<unsigned>(B));
+    hipLaunchKernelGGL((score_tile_kernel<true, kTileJC, 2>), grid, dim3(kThreads), 0, stream, S, M, K,
+                       ld, rps, out, unit_stride, split_stride, Pt, ldpt, rmax, nullptr, rinv, coff,
+                       causal);
     return hipGetLastError();
 }
 
@@ -360,6 +414,18 @@ hipError_t launch_score_norm_kmajor(const uint16_t *X, int64_t B, int64_t M, int
                                        stream);
     if (err != hipSuccess || S == 1) return err;
     return launch_score_finalize(partials, B, S, K, energy, stream);
+}
+
+hipError_t launch_score_softmax_kmajor(const uint16_t *S, int64_t B, int64_t M, int64_t K, int64_t ld,
+                                      const float *rmax, const float *rinv, int64_t coff,
+                                      int causal, double *energy, double *partials, uint16_t *Pt,
+                                      int64_t ldpt, hipStream_t stream) {
+    const int64_t splits = score_splits(B, M, K);
+    double *out = splits > 1 ? partials : energy;
+    hipError_t err = launch_tiles_softmax(S, B, M, K, ld, splits, out, splits * K, K, Pt, ldpt, rmax,
+                                          rinv, coff, causal, stream);
+    if (err != hipSuccess || splits == 1) return err;
+    return launch_score_finalize(partials, B, splits, K, energy, stream);
 }
 
 hipError_t launch_score_finalize(const double *partials, int64_t B, int64_t S, int64_t K,

@@ -478,3 +478,42 @@ def test_rmsnorm_kmajor_validation():
     assert call(10, NULL) == WS_SMALL
     assert call(11, need - 1) == WS_SMALL
     assert call(10, ctypes.c_void_p(0x100008)) == INVALID     # workspace not 256-byte aligned
+
+
+def test_attention_weights_kmajor_validation():
+    f = rmm.lib.rmm_attention_weights_kmajor
+    need = rmm.rmm_attention_weights_kmajor_workspace_size(1, 2, 64, 96)
+    assert need > 0 and need % 256 == 0
+    base = [P, 1, 2, 64, 96, 96, 1, P, 64, P, P, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 7, 9):
+        assert call(i, NULL) == INVALID
+    assert call(5, 90) == INVALID             # lds < Lk
+    assert call(8, 60) == INVALID             # ldpt < Lq
+    assert call(5, 100) == UNSUPPORTED        # lds % 8
+    assert call(10, NULL) == WS_SMALL
+    assert call(11, need - 1) == WS_SMALL
+    assert call(10, ctypes.c_void_p(0x100008)) == INVALID
+
+
+def test_reduced_pv_kmajor_validation():
+    f = rmm.lib.rmm_reduced_pv_kmajor
+    base = [P, P, P, 1, 4, 2, 64, 96, 128, 48, 64, 1, P, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 12):
+        assert call(i, NULL) == INVALID
+    assert call(5, 3) == INVALID              # H % Hkv
+    assert call(9, 0) == INVALID              # kt
+    assert call(9, 97) == INVALID
+    assert call(10, 60) == INVALID            # ldpt < Lq
+    assert call(10, 68) == UNSUPPORTED        # ldpt % 8
