@@ -672,6 +672,15 @@ def time_decode(L, r, steps, warmup, B=1):
             rmm.rmm_select_tokens(p["X"], p["k"], p["idx"])
             rmm.rmm_reduced_gemv(p["X"], p["W"], p["idx"].view(B, p["k"]), p["Y"], workspace=p["ws"])
 
+    # the same step as one grouped call: selection, products and slice
+    # reductions of the four groups in three launches
+    groups = [(p["X"].view(B, p["K"]), p["W"], p["k"], p["idx"], p["Y"].view(B, p["N"])) for p in parts]
+    gws = torch.empty(max(rmm.rmm_decode_step_workspace_size(groups), 1), dtype=torch.uint8,
+                      device=L.dev)
+
+    def grouped():
+        rmm.rmm_decode_step(groups, workspace=gws)
+
     def captured(fn):
         g = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
@@ -705,6 +714,25 @@ def time_decode(L, r, steps, warmup, B=1):
         graph.replay()
     end.record()
     torch.cuda.synchronize()
+    us_sep = start.elapsed_time(end) * 1e3 / steps
+    for _ in range(warmup):
+        grouped()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        grouped()
+    end.record()
+    torch.cuda.synchronize()
+    us_grouped_eager = start.elapsed_time(end) * 1e3 / steps
+    ggraph = captured(grouped)
+    for _ in range(warmup):
+        ggraph.replay()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        ggraph.replay()
+    end.record()
+    torch.cuda.synchronize()
     us = start.elapsed_time(end) * 1e3 / steps
     R = 10
     g_us = g_bytes = 0.0
@@ -724,7 +752,9 @@ def time_decode(L, r, steps, warmup, B=1):
         torch.cuda.synchronize()
         g_us += start.elapsed_time(end) * 1e3 / (steps * R)
         g_bytes += B * p["k"] * p["N"] * 2 + B * (p["K"] + p["N"]) * 2 + 4 * B * p["k"]
-    return {"r": r, "batch": B, "us_per_step": us, "us_per_step_eager": us_eager,
+    return {"r": r, "batch": B, "us_per_step": min(us, us_grouped_eager), "us_per_step_grouped_graph": us,
+            "us_per_step_grouped_eager": us_grouped_eager,
+            "us_per_step_separate": us_sep, "us_per_step_separate_eager": us_eager,
             "gemv_calls_per_step": len(parts),
             "gemv_us_per_step": g_us, "gemv_bytes_per_step": g_bytes,
             "gemv_gbs": g_bytes / (g_us * 1e-6) / 1e9}
@@ -969,8 +999,9 @@ def main():
     if not args.no_decode:
         dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}
         for r, rec in dec.items():
-            print(f"# decode step r={r}: {rec['us_per_step']:.1f} us as a graph "
-                  f"({rec['us_per_step_eager']:.1f} us eager), reduced products "
+            print(f"# decode step r={r}: {rec['us_per_step_grouped_graph']:.1f} us grouped as a graph "
+                  f"({rec['us_per_step_grouped_eager']:.1f} us eager; separate calls "
+                  f"{rec['us_per_step_separate']:.1f} us as a graph), reduced products "
                   f"{rec['gemv_us_per_step']:.1f} us ({rec['gemv_gbs']:.0f} GB/s)",
                   file=sys.stderr, flush=True)
         d_us = sum(rec["gemv_us_per_step"] * args.steps for rec in dec.values())
@@ -980,9 +1011,12 @@ def main():
         out["decode"] = {
             "op": "one decode step, batch 1: per projection group of the layer (q|k|v, o, "
                   "gate|up, down) TopK of the token's squared activations, reduced product "
-                  "over the retained weight rows; us_per_step replays the step as one HIP "
-                  "graph, us_per_step_eager launches it call by call",
-            "kernels": ["select_token16_kernel", "gemv_partial_kernel", "gemv_reduce_kernel"],
+                  "over the retained weight rows (the four groups taken as independent); "
+                  "rmm_decode_step runs all groups in three launches (us_per_step: the faster "
+                  "of its eager launches and its HIP-graph replay); us_per_step_separate "
+                  "replays the per-group calls (three launches each) as a graph",
+            "kernels": ["select_token16_grouped_kernel", "gemv_partial_grouped_kernel",
+                        "gemv_reduce_grouped_kernel"],
             "per_ratio": {str(r): {k: (round(v, 3) if isinstance(v, float) else v)
                                    for k, v in rec.items()} for r, rec in dec.items()},
             "speedup_vs_r1": round(d_1["us_per_step"] / d_h["us_per_step"], 3) if d_1 else None,

@@ -558,6 +558,45 @@ rmm_status_t rmm_reduced_pv_kmajor(const void *Pt, const void *V, const int32_t 
                                    int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
                                    int64_t kt, int64_t ldpt, int causal, void *O, hipStream_t stream);
 
+/*
+ * A decode step's reduced products, several at once   (Sec. 3.2 TopK of the
+ * column norms and the reduced product; App. A: in decoding the retained
+ * set follows the current token).
+ *
+ * For each group g and sequence b (one token per sequence), exactly what
+ * rmm_select_tokens followed by rmm_reduced_gemv (M = 1) compute:
+ *   idx_g[b] = TopK over j < K_g of X_g[b][j]^2   (ascending; ties to the
+ *              lower index, NaN above +inf above every finite value)
+ *   Y_g[b][n] = sum over t of X_g[b][idx_g[b][t]] * W_g[idx_g[b][t]][n]
+ * in three launches for all groups together (selection, products, the
+ * fixed-order reduction of split lists) instead of three per group.  The
+ * groups must be independent of each other (no group reads another's Y);
+ * within a model's layer step those are products whose inputs are ready
+ * together.
+ *
+ * groups   : host array of ngroups (1..8) descriptions; per group X bf16
+ *            [B][ldx] (16-byte aligned, ldx % 8 == 0, ldx >= K, K <= 16384),
+ *            W bf16 [K][ldw] (16-byte aligned, ldw % 8 == 0, ldw >= N),
+ *            idx int32 [B][k] written, Y bf16 [B][ldy] written, 1 <= k <= K.
+ * workspace: rmm_decode_step_workspace_size(groups, ngroups, B) bytes,
+ *            256-byte aligned, or NULL when that is 0 (fp32 partial sums).
+ * Errors   : INVALID_ARGUMENT for null pointers, sizes < 1, k outside
+ *            [1, K], ld too small, a misaligned workspace; UNSUPPORTED for
+ *            more than 8 groups, B > 65535, K > 16384, misaligned X or W,
+ *            ldx or ldw not multiples of 8, K*ldw*2 >= 2^31;
+ *            WORKSPACE_TOO_SMALL.
+ */
+typedef struct rmm_decode_group {
+    const void *X;
+    const void *W;
+    int32_t *idx;
+    void *Y;
+    int64_t K, N, k, ldx, ldw, ldy;
+} rmm_decode_group_t;
+size_t rmm_decode_step_workspace_size(const rmm_decode_group_t *groups, int ngroups, int64_t B);
+rmm_status_t rmm_decode_step(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                             void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);
 

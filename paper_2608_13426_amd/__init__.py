@@ -23,7 +23,8 @@ __all__ = [
     "rmm_reduced_attention", "rmm_reduced_gemv", "rmm_gemv_workspace_size", "rmm_select_tokens",
     "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "rmm_rmsnorm_kmajor",
     "rmm_rmsnorm_kmajor_workspace_size", "rmm_attention_weights_kmajor",
-    "rmm_attention_weights_kmajor_workspace_size", "rmm_reduced_pv_kmajor", "EXPORTED_SYMBOLS",
+    "rmm_attention_weights_kmajor_workspace_size", "rmm_reduced_pv_kmajor", "rmm_decode_step",
+    "rmm_decode_step_workspace_size", "DecodeGroup", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -33,6 +34,12 @@ RMM_OP_SCORE, RMM_OP_SELECT, RMM_OP_LINEAR, RMM_OP_ATTENTION, RMM_OP_PV = 0, 1, 
 
 _p = ctypes.c_void_p
 _i64 = ctypes.c_int64
+
+
+class DecodeGroup(ctypes.Structure):
+    """rmm_decode_group_t: one projection group of a decode step."""
+    _fields_ = [("X", _p), ("W", _p), ("idx", _p), ("Y", _p), ("K", _i64), ("N", _i64),
+                ("k", _i64), ("ldx", _i64), ("ldw", _i64), ("ldy", _i64)]
 _SIGS = {
     "rmm_retained_count": (_i64, [ctypes.c_double, _i64]),
     "rmm_workspace_size": (ctypes.c_size_t, [ctypes.c_int, _i64, _i64, _i64, _i64]),
@@ -55,6 +62,10 @@ _SIGS = {
     "rmm_attention_weights_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64]),
     "rmm_attention_weights_kmajor": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _i64, ctypes.c_int,
                                                     _p, _i64, _p, _p, ctypes.c_size_t, _p]),
+    "rmm_decode_step_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(DecodeGroup), ctypes.c_int,
+                                                         _i64]),
+    "rmm_decode_step": (ctypes.c_int, [ctypes.POINTER(DecodeGroup), ctypes.c_int, _i64, _p,
+                                       ctypes.c_size_t, _p]),
     "rmm_reduced_pv_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
                                              _i64, ctypes.c_int, _p, _p]),
     "rmm_rmsnorm_kmajor": (ctypes.c_int, [_p, _p, ctypes.c_float, _i64, _i64, _i64, _i64, _p, _i64,
@@ -694,3 +705,45 @@ def rmm_reduced_pv_kmajor(Pt: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, 
         Pt.data_ptr(), V.data_ptr(), idx.data_ptr(), batch, H, Hkv, Lq, Lk, D, kt, Pt.stride(2),
         1 if causal else 0, O.data_ptr(), _stream(d, stream)))
     return O
+
+
+def _decode_groups(groups):
+    """[(X [B, K], W [K, N], k, idx [B*k] int32, Y [B, N])] -> ctypes array, B."""
+    arr = (DecodeGroup * len(groups))()
+    B = None
+    for i, (X, W, k, idx, Y) in enumerate(groups):
+        if X.dim() != 2 or W.dim() != 2 or Y.dim() != 2:
+            raise ValueError("X [B, K], W [K, N] and Y [B, N] must be 2-D")
+        if B is None:
+            B = X.shape[0]
+        if X.shape[0] != B or Y.shape[0] != B or W.shape[0] != X.shape[1] or Y.shape[1] != W.shape[1]:
+            raise ValueError("group shapes disagree: X [B, K], W [K, N], Y [B, N]")
+        if X.stride(1) != 1 or W.stride(1) != 1 or Y.stride(1) != 1:
+            raise ValueError("rows must be contiguous")
+        if not (X.dtype == W.dtype == Y.dtype == torch.bfloat16):
+            raise TypeError("X, W and Y must be bfloat16")
+        if idx.dtype != torch.int32 or idx.numel() != B * k or not idx.is_contiguous():
+            raise ValueError("idx must be contiguous int32 [B*k]")
+        _dev(X, W, idx, Y)
+        arr[i] = DecodeGroup(X.data_ptr(), W.data_ptr(), idx.data_ptr(), Y.data_ptr(), X.shape[1],
+                             W.shape[1], int(k), X.stride(0), W.stride(0), Y.stride(0))
+    return arr, B
+
+
+def rmm_decode_step_workspace_size(groups) -> int:
+    arr, B = _decode_groups(groups)
+    return int(lib.rmm_decode_step_workspace_size(arr, len(groups), B))
+
+
+def rmm_decode_step(groups, workspace: torch.Tensor | None = None, stream=None):
+    """For each group (X [B, K], W [K, N], k, idx [B*k], Y [B, N]): idx = the
+    TopK of each token's squared activations, Y = the reduced product; all
+    groups in three launches."""
+    arr, B = _decode_groups(groups)
+    d = groups[0][0].device
+    need = int(lib.rmm_decode_step_workspace_size(arr, len(groups), B))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=d)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("rmm_decode_step", lib.rmm_decode_step(arr, len(groups), B, _ptr(workspace), ws_bytes,
+                                                  _stream(d, stream)))

@@ -497,6 +497,73 @@ rmm_status_t rmm_reduced_pv_kmajor(const void *Pt, const void *V, const int32_t 
     return e == hipErrorNotSupported ? RMM_ERR_UNSUPPORTED : from_hip(e);
 }
 
+// The grouped decode step's kernel arguments from the caller's groups (shapes
+// validated), with each group's partials carved from the workspace when ws is
+// given; returns the workspace bytes needed.
+static size_t decode_groups(const rmm_decode_group_t *groups, int n, int64_t B, void *ws,
+                            rmm::GemvGroups *G) {
+    size_t off = 0;
+    G->n = n;
+    for (int i = 0; i < n; ++i) {
+        const rmm_decode_group_t &d = groups[i];
+        rmm::GemvGroup &q = G->g[i];
+        q.X = static_cast<const uint16_t *>(d.X);
+        q.W = static_cast<const uint16_t *>(d.W);
+        q.idx = d.idx;
+        q.idx_out = d.idx;
+        q.Y = static_cast<uint16_t *>(d.Y);
+        q.N = static_cast<int>(d.N);
+        q.K = static_cast<int>(d.K);
+        q.k = static_cast<int>(d.k);
+        q.ldx = d.ldx;
+        q.ldw = d.ldw;
+        q.ldy = d.ldy;
+        int SR, S;
+        rmm::gemv_slices(B, d.N, d.k, &SR, &S);
+        q.P = (S > 1 && ws) ? reinterpret_cast<float *>(static_cast<char *>(ws) + off) : nullptr;
+        if (S > 1) off += align256(static_cast<size_t>(B) * S * d.N * sizeof(float));
+    }
+    return off;
+}
+
+static rmm_status_t check_decode_groups(const rmm_decode_group_t *groups, int n, int64_t B) {
+    if (!groups || n < 1 || B < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (n > rmm::kMaxGemvGroups || B > kGridYZMax) return RMM_ERR_UNSUPPORTED;
+    for (int i = 0; i < n; ++i) {
+        const rmm_decode_group_t &d = groups[i];
+        if (!d.X || !d.W || !d.idx || !d.Y) return RMM_ERR_INVALID_ARGUMENT;
+        if (d.K < 1 || d.N < 1 || d.k < 1 || d.k > d.K) return RMM_ERR_INVALID_ARGUMENT;
+        if (d.ldx < d.K || d.ldw < d.N || d.ldy < d.N) return RMM_ERR_INVALID_ARGUMENT;
+        if (d.N > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+        if (d.K > 16384 || !aligned16(d.X) || d.ldx % 8 || !aligned16(d.W) || d.ldw % 8)
+            return RMM_ERR_UNSUPPORTED;
+        if (d.K * d.ldw * 2 >= (int64_t(1) << 31)) return RMM_ERR_UNSUPPORTED;
+    }
+    return RMM_OK;
+}
+
+size_t rmm_decode_step_workspace_size(const rmm_decode_group_t *groups, int ngroups, int64_t B) {
+    if (check_decode_groups(groups, ngroups, B) != RMM_OK) return 0;
+    rmm::GemvGroups G;
+    return decode_groups(groups, ngroups, B, nullptr, &G);
+}
+
+rmm_status_t rmm_decode_step(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                             void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    rmm_status_t st = check_decode_groups(groups, ngroups, B);
+    if (st != RMM_OK) return st;
+    rmm::GemvGroups G;
+    const size_t need = decode_groups(groups, ngroups, B, nullptr, &G);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+        if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
+    }
+    decode_groups(groups, ngroups, B, workspace, &G);
+    hipError_t e = rmm::launch_select_tokens_grouped(G, B, stream);
+    if (e != hipSuccess) return RMM_ERR_HIP;
+    return from_hip(rmm::launch_gemv_grouped_bf16(G, B, stream));
+}
+
 const char *rmm_status_string(rmm_status_t status) {
     switch (status) {
     case RMM_OK: return "success";

@@ -28,11 +28,13 @@ constexpr int TARGET_BLOCKS = 512;
 constexpr int MIN_SLICE = 64;      // retained rows per slice at least
 }  // namespace gv
 
-template <int MR, bool VEC, bool DIRECT>
-__global__ __launch_bounds__(gv::NT) void gemv_partial_kernel(
+// One workgroup's share: columns chunk*CW .., slice s of unit b's retained
+// list; DIRECT writes Y, otherwise the slice's fp32 partials.
+template <int MR, bool VEC>
+__device__ __forceinline__ void gemv_tile(
     const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, const int32_t *__restrict__ idx,
     float *__restrict__ P, uint16_t *__restrict__ Y, int M, int N, int K, int k, int64_t ldx,
-    int64_t ldw, int64_t ldy, int SR, int S) {
+    int64_t ldw, int64_t ldy, int SR, int S, int chunk, int s, int b, bool DIRECT) {
     using namespace gv;
     __shared__ uint32_t roff[RB];              // byte offset of each staged row in W
     __shared__ float xs[RB][MR];               // its activation value per row m
@@ -40,7 +42,6 @@ __global__ __launch_bounds__(gv::NT) void gemv_partial_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int chunk = blockIdx.x, s = blockIdx.y, b = blockIdx.z;
     const int n0 = chunk * CW;
     const int t0 = s * SR, t1 = min(k, t0 + SR);
     const int32_t *I = idx + static_cast<int64_t>(b) * k;
@@ -139,6 +140,27 @@ __global__ __launch_bounds__(gv::NT) void gemv_partial_kernel(
     }
 }
 
+template <int MR, bool VEC, bool DIRECT>
+__global__ __launch_bounds__(gv::NT) void gemv_partial_kernel(
+    const uint16_t *__restrict__ X, const uint16_t *__restrict__ W, const int32_t *__restrict__ idx,
+    float *__restrict__ P, uint16_t *__restrict__ Y, int M, int N, int K, int k, int64_t ldx,
+    int64_t ldw, int64_t ldy, int SR, int S) {
+    gemv_tile<MR, VEC>(X, W, idx, P, Y, M, N, K, k, ldx, ldw, ldy, SR, S, blockIdx.x, blockIdx.y,
+                       blockIdx.z, DIRECT);
+}
+
+// Several independent one-row products in one launch: the workgroups of
+// group g are g's (chunk, slice, unit) triples, numbered from first[g].
+__global__ __launch_bounds__(gv::NT) void gemv_partial_grouped_kernel(GemvGroups G) {
+    int g = 0;
+    while (g + 1 < G.n && static_cast<int>(blockIdx.x) >= G.g[g + 1].first) ++g;
+    const GemvGroup &q = G.g[g];
+    const int local = static_cast<int>(blockIdx.x) - q.first;
+    const int chunk = local % q.chunks, s = (local / q.chunks) % q.S, b = local / (q.chunks * q.S);
+    gemv_tile<1, true>(q.X, q.W, q.idx, q.P, q.Y, 1, q.N, q.K, q.k, q.ldx, q.ldw, q.ldy, q.SR, q.S,
+                       chunk, s, b, q.S == 1);
+}
+
 // Y[b][m][n] = sum over slices s, in order, of P[b][s][m][n]
 __global__ __launch_bounds__(256) void gemv_reduce_kernel(const float *__restrict__ P,
                                                           uint16_t *__restrict__ Y, int M, int N,
@@ -159,6 +181,31 @@ __global__ __launch_bounds__(256) void gemv_reduce_kernel(const float *__restric
     }
     for (; s < S; ++s) sum += p[s * st];
     Y[(static_cast<int64_t>(b) * M + m) * ldy + n] = f32_to_bf16(sum);
+}
+
+// the slice reduction of every group with more than one slice: workgroup
+// blockIdx.x of group g covers 256 columns of one unit, numbered from rfirst[g]
+__global__ __launch_bounds__(256) void gemv_reduce_grouped_kernel(GemvGroups G) {
+    int g = -1;
+    for (int i = 0; i < G.n; ++i)
+        if (G.g[i].S > 1 && static_cast<int>(blockIdx.x) >= G.g[i].rfirst) g = i;
+    const GemvGroup &q = G.g[g];
+    const int local = static_cast<int>(blockIdx.x) - q.rfirst;
+    const int nb = (q.N + 255) / 256;
+    const int b = local / nb, n = (local % nb) * 256 + static_cast<int>(threadIdx.x);
+    if (n >= q.N) return;
+    const float *p = q.P + static_cast<int64_t>(b) * q.S * q.N + n;
+    float sum = 0.f;
+    int s = 0;
+    for (; s + 8 <= q.S; s += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = p[static_cast<int64_t>(s + u) * q.N];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += v[u];
+    }
+    for (; s < q.S; ++s) sum += p[static_cast<int64_t>(s) * q.N];
+    q.Y[static_cast<int64_t>(b) * q.ldy + n] = f32_to_bf16(sum);
 }
 
 template <int MR, bool VEC>
@@ -214,6 +261,26 @@ size_t gemv_workspace_bytes(int64_t B, int64_t M, int64_t N, int64_t k) {
     int SR, S;
     gemv_slices(B, N, k, &SR, &S);
     return S == 1 ? 0 : static_cast<size_t>(B) * S * M * N * sizeof(float);
+}
+
+hipError_t launch_gemv_grouped_bf16(GemvGroups G, int64_t B, hipStream_t stream) {
+    int blocks = 0, rblocks = 0;
+    for (int i = 0; i < G.n; ++i) {
+        GemvGroup &q = G.g[i];
+        gemv_slices(B, q.N, q.k, &q.SR, &q.S);
+        q.chunks = (q.N + gv::CW - 1) / gv::CW;
+        q.first = blocks;
+        blocks += q.chunks * q.S * static_cast<int>(B);
+        q.rfirst = rblocks;
+        if (q.S > 1) rblocks += (q.N + 255) / 256 * static_cast<int>(B);
+    }
+    hipLaunchKernelGGL(gemv_partial_grouped_kernel, dim3(static_cast<unsigned>(blocks)), dim3(gv::NT), 0,
+                       stream, G);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || rblocks == 0) return e;
+    hipLaunchKernelGGL(gemv_reduce_grouped_kernel, dim3(static_cast<unsigned>(rblocks)), dim3(256), 0,
+                       stream, G);
+    return hipGetLastError();
 }
 
 hipError_t launch_gemv_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx, int64_t B,

@@ -105,6 +105,31 @@ hipError_t launch_gemm_f32(const float *X, const float *W, const int32_t *idx,
                            int64_t ldx, int64_t ldw, float *Y, int64_t ldy,
                            hipStream_t stream);
 
+// Independent one-row-per-unit products of a decode step, passed by value
+// to the grouped kernels (at most kMaxGemvGroups).  The launchers fill in
+// the split (SR, S, chunks) and the workgroup numbering (first, rfirst).
+constexpr int kMaxGemvGroups = 8;
+struct GemvGroup {
+    const uint16_t *X;      // [B][ldx] bf16, one token per unit
+    const uint16_t *W;      // [K][ldw] bf16, 16-byte aligned, ldw % 8 == 0
+    const int32_t *idx;     // [B][k] the retained lists the product reads
+    int32_t *idx_out;       // [B][k] the lists the selection writes (same memory)
+    uint16_t *Y;            // [B][ldy] bf16
+    float *P;               // [B][S][N] fp32 partials when S > 1
+    int N, K, k;
+    int64_t ldx, ldw, ldy;
+    int SR, S, chunks, first, rfirst;
+};
+struct GemvGroups {
+    GemvGroup g[kMaxGemvGroups];
+    int n;
+};
+// TopK of x^2 for every unit of every group (bf16 tokens, K <= 16384, 16-byte
+// aligned rows; checked by the caller)
+hipError_t launch_select_tokens_grouped(const GemvGroups &G, int64_t B, hipStream_t stream);
+// the groups' reduced products (one launch) and slice reductions (one launch)
+hipError_t launch_gemv_grouped_bf16(GemvGroups G, int64_t B, hipStream_t stream);
+
 // reduced product with M <= 8 rows per unit (decode); workspace holds the
 // per-slice fp32 partials when the retained list is split
 void gemv_slices(int64_t B, int64_t N, int64_t k, int *SR, int *S);

@@ -226,16 +226,13 @@ __global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src
 // number of kept keys before it, i.e. keys above before it plus
 // min(ties before it, ties kept).
 template <int NT, int C>
-__global__ __launch_bounds__(NT) void select_token16_kernel(const uint16_t *__restrict__ X,
-                                                            int64_t ldx, int K, int k,
-                                                            int32_t *__restrict__ idx) {
+__device__ __forceinline__ void select_token16(const uint16_t *__restrict__ x, int K, int k,
+                                               int32_t *__restrict__ out) {
     static_assert(C % 8 == 0 && C <= 16 && NT >= 256 && NT <= 1024, "chunk");
     __shared__ uint32_t hist[256];
     __shared__ uint32_t scan_buf[NT / kWave];
     __shared__ int s_thr, s_need;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
-    const uint16_t *x = X + static_cast<int64_t>(blockIdx.x) * ldx;
-    int32_t *out = idx + static_cast<int64_t>(blockIdx.x) * k;
     if (k == K) {                       // everything is kept
         for (int j = tid; j < K; j += NT) out[j] = j;
         return;
@@ -326,6 +323,22 @@ __global__ __launch_bounds__(NT) void select_token16_kernel(const uint16_t *__re
 }
 
 template <int NT, int C>
+__global__ __launch_bounds__(NT) void select_token16_kernel(const uint16_t *__restrict__ X,
+                                                            int64_t ldx, int K, int k,
+                                                            int32_t *__restrict__ idx) {
+    select_token16<NT, C>(X + static_cast<int64_t>(blockIdx.x) * ldx, K, k,
+                          idx + static_cast<int64_t>(blockIdx.x) * k);
+}
+
+// the token selection of several groups in one launch: workgroup (b, g)
+// takes unit b of group g
+__global__ __launch_bounds__(1024) void select_token16_grouped_kernel(GemvGroups G) {
+    const GemvGroup &q = G.g[blockIdx.y];
+    select_token16<1024, 16>(q.X + static_cast<int64_t>(blockIdx.x) * q.ldx, q.K, q.k,
+                             q.idx_out + static_cast<int64_t>(blockIdx.x) * q.k);
+}
+
+template <int NT, int C>
 hipError_t launch_token16(const void *X, int64_t ldx, int64_t B, int64_t K, int64_t k, int32_t *idx,
                           hipStream_t stream) {
     hipLaunchKernelGGL((select_token16_kernel<NT, C>), dim3(static_cast<unsigned>(B)), dim3(NT), 0, stream,
@@ -390,6 +403,12 @@ hipError_t launch_check_indices(const int32_t *idx, int64_t B, int64_t k, int64_
 hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
                          int32_t *idx, hipStream_t stream) {
     return launch_src<kEnergy>(energy, K, B, K, k, idx, stream);
+}
+
+hipError_t launch_select_tokens_grouped(const GemvGroups &G, int64_t B, hipStream_t stream) {
+    hipLaunchKernelGGL(select_token16_grouped_kernel, dim3(static_cast<unsigned>(B), static_cast<unsigned>(G.n)),
+                       dim3(1024), 0, stream, G);
+    return hipGetLastError();
 }
 
 hipError_t launch_select_tokens(const void *X, bool bf16, int64_t B, int64_t K, int64_t ldx,

@@ -517,3 +517,30 @@ def test_reduced_pv_kmajor_validation():
     assert call(9, 97) == INVALID
     assert call(10, 60) == INVALID            # ldpt < Lq
     assert call(10, 68) == UNSUPPORTED        # ldpt % 8
+
+
+def test_decode_step_validation():
+    G = rmm.DecodeGroup
+    f = rmm.lib.rmm_decode_step
+
+    def arr(**kw):
+        d = dict(X=0x100000, W=0x100000, idx=0x100000, Y=0x100000, K=4096, N=1024, k=2048,
+                 ldx=4096, ldw=1024, ldy=1024)
+        d.update(kw)
+        return (G * 1)(G(**d))
+
+    assert f(None, 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(), 0, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(), 1, 0, NULL, 0, NULL) == INVALID
+    assert f(arr(X=None), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(k=0), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(k=4097), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(ldw=1000), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(K=20000, ldx=20000), 1, 1, NULL, 0, NULL) == UNSUPPORTED
+    assert f(arr(X=0x100008), 1, 1, NULL, 0, NULL) == UNSUPPORTED
+    nine = (G * 9)(*[arr()[0]] * 9)
+    assert f(nine, 9, 1, NULL, 0, NULL) == UNSUPPORTED
+    need = rmm.lib.rmm_decode_step_workspace_size(arr(), 1, 1)
+    assert need > 0                                    # one token: the list is split over slices
+    assert f(arr(), 1, 1, NULL, 0, NULL) == WS_SMALL
+    assert f(arr(), 1, 1, P, need - 1, NULL) == WS_SMALL

@@ -225,3 +225,64 @@ def test_decode_step_graph_replay():
         for (ie, ye), (*_, idx, Y) in zip(eager, parts):
             assert torch.equal(idx, ie), rep
             assert torch.equal(Y.view(torch.int16), ye.view(torch.int16)), rep
+
+
+def _decode_case(dev, groups_np, B, r):
+    """groups_np: [(X bits [B, K], W bits [K, N])].  rmm_decode_step against
+    the separate calls (bit for bit) and the oracle."""
+    groups, sep = [], []
+    for Xb, Wb in groups_np:
+        K, N = Wb.shape
+        k = ro.retained_count(r, K)
+        Xd = torch.from_numpy(Xb.view(np.int16)).to(dev).view(torch.bfloat16)
+        Wd = torch.from_numpy(Wb.view(np.int16)).to(dev).view(torch.bfloat16)
+        idx = torch.full((B * k,), -1, dtype=torch.int32, device=dev)
+        Y = torch.full((B, N), 9.0, dtype=torch.bfloat16, device=dev)
+        groups.append((Xd, Wd, k, idx, Y))
+        i2 = torch.empty_like(idx)
+        Y2 = torch.empty_like(Y)
+        rmm.rmm_select_tokens(Xd, k, i2)
+        rmm.rmm_reduced_gemv(Xd.view(B, 1, K), Wd, i2.view(B, k), Y2.view(B, 1, N))
+        sep.append((i2, Y2))
+    rmm.rmm_decode_step(groups)
+    for (Xd, Wd, k, idx, Y), (i2, Y2), (Xb, Wb) in zip(groups, sep, groups_np):
+        assert torch.equal(idx, i2), "sets differ from rmm_select_tokens"
+        assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16)), "products differ from rmm_reduced_gemv"
+        X = wl.decode(Xb, "bf16").astype(np.float64)
+        W = wl.decode(Wb, "bf16").astype(np.float64)
+        e_ref = X * X                                   # one row: the exact energies
+        idx_ref = np.stack([ro.topk_indices(e_ref[b], k) for b in range(B)])
+        check_index_sets(idx.cpu().numpy(), idx_ref, e_ref, 1, exact_sums=True)
+        Yg = from_device(Y)
+        for b in range(B):
+            I = idx_ref[b]
+            check_product(Yg[b][None], ro.reduced_matmul(X[b][None], W, I),
+                          np.abs(X[b][None][:, I]) @ np.abs(W[I]), k, "bf16")
+
+
+@pytest.mark.parametrize("B,r,seed", [(1, 0.5, 0), (3, 0.25, 1), (2, 1.0, 2), (5, 0.001, 3)])
+def test_decode_step_groups(B, r, seed):
+    """Ragged groups (K, N not multiples of the chunk; a single-slice group)."""
+    dev = require_gpu()
+    shapes = [(1000, 1536), (4096, 520), (264, 72), (2048, 3000)]
+    groups = [(wl.random_case(seed + 10 * i, (B, K), "bf16", n_outlier=max(1, K // 100)),
+               wl.random_case(seed + 10 * i + 1, (K, N), "bf16", std=0.02)) for i, (K, N) in enumerate(shapes)]
+    _decode_case(dev, groups, B, r)
+
+
+@pytest.mark.parametrize("B", [1, 16])
+def test_layer_8b_decode_step(B):
+    """The 8B layer's four projection groups (q|k|v, o, gate|up, down) as one
+    grouped decode step at every ratio, B sequences."""
+    dev = require_gpu()
+    wk = wl.WORKLOADS["layer_8b"]
+    by = {}
+    for p in wk.projections:
+        by.setdefault(p.input_name, []).append(p)
+    groups = []
+    for name, projs in by.items():
+        Xb = wl.f32_to_bf16_bits(wl.workload_input(wk, name, M=B))
+        Wb = np.concatenate([wl.f32_to_bf16_bits(wl.workload_weight(wk, p)) for p in projs], axis=1)
+        groups.append((Xb, Wb))
+    for r in (0.25, 0.5, 0.75, 1.0):
+        _decode_case(dev, groups, B, r)
