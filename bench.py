@@ -85,12 +85,23 @@ def _sources(main):
 # A figure is reported only while the SHA-256 of its sources (the kernel's
 # file, the shared headers and the build script) is the one it was measured
 # with, and for the same launch mix; re-run the counters after any change.
-GEMM_TRAFFIC = {"sources": _sources("gemm.hip"), "sha256": None,
-                "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped", "bytes": None}
-ATTN_TRAFFIC = {"sources": _sources("attn.hip"), "sha256": None,
-                "mix": "layer_8b r=0.25,0.5,0.75,1.0", "bytes": None}
-NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip")], "sha256": None,
-                "mix": "layer_8b attn_in,mlp_in r=0.25,0.5,0.75,1.0", "bytes": None}
+GEMM_TRAFFIC = {"sources": _sources("gemm.hip"),
+                "sha256": "46521fd8443677785dd42eeb429fb82a7e6f5cbf4a313acdb25c8f08134be0f6",
+                "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
+                "bytes": round((399487.78 * 2.0 + 172205.10) * 1024)}
+# per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
+# plus attn_compact_k_kernel
+ATTN_TRAFFIC = {"sources": _sources("attn.hip"),
+                "sha256": "79e5d1b3403e7f09ad5106e4faae95093d6e9e88e435f6c921e6da50f7e12dd3",
+                "mix": "layer_8b r=0.25,0.5,0.75,1.0",
+                "bytes": round((103417.58 * 2.0 + 65545.13 + 8249.04 * 2.0 + 40960.00) * 1024)}
+# per rmm_rmsnorm_kmajor call (8192 x 4096): rms_rowscale_kernel, the
+# normalising score_tile_kernel and its score_finalize_kernel
+NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip")],
+                "sha256": "5cc677544347de159e47c3c26c8f7e6530f3de50ea6b970e79e54b04ec79030f",
+                "mix": "layer_8b attn_in,mlp_in r=0.25,0.5,0.75,1.0",
+                "bytes": round((32784.54 * 2.0 + 64.06 + 32983.86 * 2.0 + 66560.00 +
+                                532.50 * 2.0 + 32.00) * 1024)}
 
 
 def sources_sha256(paths):
