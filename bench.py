@@ -544,14 +544,23 @@ def time_pv_chain(L, r, steps, warmup, bufs):
                 stopped at their last visible token);
       dense   : torch softmax of S (row-major weights) -> torch P @ V (V
                 repeated over each kv head's query heads).
-    Every call is bracketed by HIP events; the producer and the product are
+    From the scores' producer on, two ways (S rewritten with the same
+    values by the layer's own selection):
+      from_qk          : rmm_reduced_qk -> the reduced chain above;
+      from_qk_rowstats : rmm_reduced_qk_rowstats (S with its softmax row
+                         statistics) -> rmm_attention_weights_kmajor_rowstats
+                         (S read once) -> TopK -> rmm_reduced_pv_kmajor.
+    Every call is bracketed by HIP events; the producers and the product are
     also timed alone."""
     import torch
     import paper_2608_13426_amd as rmm
     a = L.wk.attention
     kt = rmm.rmm_retained_count(r, a.L)
     Pt, e, ws, P, Vr = bufs["Pt"], bufs["e"], bufs["ws"], bufs["P"], bufs["Vr"]
+    rmax, rinv = bufs["rmax"], bufs["rinv"]
     idx = torch.empty(a.H * kt, dtype=torch.int32, device=L.dev)
+    kq = L.qidx.numel() // a.H
+    qidx = L.qidx.view(1, a.H, kq)
 
     def producer():
         rmm.rmm_attention_weights_kmajor(L.S, Pt, e, causal=True, workspace=ws)
@@ -568,8 +577,33 @@ def time_pv_chain(L, r, steps, warmup, bufs):
         torch.softmax(L.S[0], dim=-1, out=P)
         torch.matmul(P, Vr, out=bufs["Od"])
 
+    def qk():
+        rmm.rmm_reduced_qk(L.Q, L.Kc, qidx, L.S, causal=True)
+
+    def qk_rowstats():
+        rmm.rmm_reduced_qk_rowstats(L.Q, L.Kc, qidx, L.S, rmax, rinv, causal=True)
+
+    def producer_rowstats():
+        rmm.rmm_attention_weights_kmajor(L.S, Pt, e, causal=True, workspace=ws, row_max=rmax,
+                                         row_rinv=rinv)
+
+    def from_qk():
+        qk()
+        reduced()
+
+    def from_qk_rowstats():
+        qk_rowstats()
+        producer_rowstats()
+        rmm.rmm_select(e, kt, idx)
+        product()
+
     us = {n: time_calls(f, steps, warmup) for n, f in
-          (("reduced", reduced), ("producer", producer), ("product", product))}
+          (("reduced", reduced), ("producer", producer), ("product", product),
+           ("from_qk", from_qk), ("from_qk_rowstats", from_qk_rowstats))}
+    if bufs.get("qk_us") is None:
+        bufs["qk_us"] = time_calls(qk, steps, warmup)
+        bufs["qk_rowstats_us"] = time_calls(qk_rowstats, steps, warmup)
+        bufs["producer_rowstats_us"] = time_calls(producer_rowstats, steps, warmup)
     # bytes of the producer: the causal part of S read once, the part of Pt
     # it stores (the lower triangle and, above the diagonal, the zeros of the
     # 256-query block holding each column's diagonal), the energies
@@ -578,7 +612,12 @@ def time_pv_chain(L, r, steps, warmup, bufs):
     nbytes = a.H * (pairs * 2 + stored * 2 + a.L * 8)
     rec = {"r": r, "kt": kt, "reduced_us": us["reduced"], "producer_us": us["producer"],
            "product_us": us["product"], "producer_bytes": nbytes,
-           "producer_gbs": nbytes / (us["producer"] * 1e-6) / 1e9, "calls": steps}
+           "producer_gbs": nbytes / (us["producer"] * 1e-6) / 1e9,
+           "qk_k": kq, "qk_us": bufs["qk_us"], "qk_rowstats_us": bufs["qk_rowstats_us"],
+           "producer_rowstats_us": bufs["producer_rowstats_us"],
+           "producer_rowstats_gbs": nbytes / (bufs["producer_rowstats_us"] * 1e-6) / 1e9,
+           "from_qk_us": us["from_qk"], "from_qk_rowstats_us": us["from_qk_rowstats"],
+           "rowstats_speedup": us["from_qk"] / us["from_qk_rowstats"], "calls": steps}
     if bufs.get("dense_us") is None:
         bufs["dense_us"] = time_calls(dense, steps, warmup)
     rec["dense_torch_us"] = bufs["dense_us"]
@@ -1045,15 +1084,20 @@ def main():
                                   dtype=torch.uint8, device=L.dev),
                 "P": torch.empty((a.H, a.L, a.L), dtype=torch.bfloat16, device=L.dev),
                 "Vr": L.V[0].repeat_interleave(a.H // a.Hkv, dim=0).contiguous(),
-                "Od": torch.empty((a.H, a.L, a.D), dtype=torch.bfloat16, device=L.dev)}
+                "Od": torch.empty((a.H, a.L, a.D), dtype=torch.bfloat16, device=L.dev),
+                "rmax": torch.empty(a.H * a.L, dtype=torch.float32, device=L.dev),
+                "rinv": torch.empty(a.H * a.L, dtype=torch.float32, device=L.dev)}
         pc = {r: time_pv_chain(L, r, args.steps, args.warmup, bufs) for r in sorted(sweep)}
         del bufs
         torch.cuda.empty_cache()
         for r, rec in pc.items():
             print(f"# PV chain r={r}: reduced {rec['reduced_us']:.1f} us (producer "
                   f"{rec['producer_us']:.1f} us at {rec['producer_gbs']:.0f} GB/s, product "
-                  f"{rec['product_us']:.1f} us); dense torch softmax + P@V {rec['dense_torch_us']:.1f} us",
-                  file=sys.stderr, flush=True)
+                  f"{rec['product_us']:.1f} us); dense torch softmax + P@V {rec['dense_torch_us']:.1f} us; "
+                  f"from QK: {rec['from_qk_us']:.1f} us, with QK row statistics "
+                  f"{rec['from_qk_rowstats_us']:.1f} us (QK {rec['qk_us']:.1f} -> "
+                  f"{rec['qk_rowstats_us']:.1f} us, producer {rec['producer_rowstats_us']:.1f} us at "
+                  f"{rec['producer_rowstats_gbs']:.0f} GB/s)", file=sys.stderr, flush=True)
         c_h, c_1 = pc.get(HEADLINE_R), pc.get(1.0)
         p_us = sum(v["producer_us"] for v in pc.values())
         p_b = sum(v["producer_bytes"] for v in pc.values())
@@ -1076,6 +1120,15 @@ def main():
                                         "energies per call (the implementation reads S twice: row "
                                         "statistics, then the weights)",
                          "traffic": None},
+            "rowstats_speedup_from_qk": round(c_h["rowstats_speedup"], 3) if c_h else None,
+            "roofline_rowstats": {
+                "bound": "hbm",
+                "kernel": "rmm_attention_weights_kmajor_rowstats (score_tile_kernel softmax variant "
+                          "+ score_finalize_kernel; row statistics from rmm_reduced_qk_rowstats)",
+                "achieved": round(c_h["producer_rowstats_gbs"], 1) if c_h else None,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(c_h["producer_rowstats_gbs"] / PEAK_HBM_GBS, 4) if c_h else None,
+                "bytes_basis": "as roofline (S read once by this pass)", "traffic": None},
         }
     if not args.no_pv:
         import torch

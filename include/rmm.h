@@ -307,6 +307,30 @@ rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx,
                             hipStream_t stream);
 
 /*
+ * Reduced attention scores with their softmax row statistics   (Sec. 3.3,
+ * Attention: the reduced scores feed softmax(S~ + M); the Limitations
+ * section names the memory movement of separate passes as a cost to remove).
+ *
+ * S exactly as rmm_reduced_qk writes it (bf16), and for each query row i of
+ * each unit u = b*H + h:
+ *   row_max[u*Lq + i]  = max over kept t of S[u][i][t]   (kept: not -inf)
+ *   row_rinv[u*Lq + i] = 1 / sum over kept t of exp(S[u][i][t] - row_max)
+ * in fp32 over the stored bf16 scores, summed in a fixed order; 0 and 0 for
+ * a row with nothing kept (only when causal and Lq > Lk).  These are the
+ * statistics rmm_attention_weights_kmajor computes in a pass of its own over
+ * S; rmm_attention_weights_kmajor_rowstats takes them instead.
+ * Q, Kc, idx, scale, causal as rmm_reduced_qk; bf16 only.
+ * row_max, row_rinv : float [batch*H*Lq], 4-byte aligned, written.
+ * Errors: INVALID_ARGUMENT as rmm_reduced_qk or for null statistics;
+ *         UNSUPPORTED unless D is 64 or 128, Lk % 8 == 0, Lk <= 2^22, S is
+ *         16-byte aligned and batch*H <= 65535.
+ */
+rmm_status_t rmm_reduced_qk_rowstats(const void *Q, const void *Kc, const int32_t *idx, int64_t batch,
+                                     int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                                     int64_t k, float scale, int causal, void *S, float *row_max,
+                                     float *row_rinv, hipStream_t stream);
+
+/*
  * Reduced attention block   (Sec. 3.3 "Attention": the reduced scores feed
  * the softmax of the attention block, which then weights the value rows).
  *
@@ -533,6 +557,28 @@ rmm_status_t rmm_attention_weights_kmajor(const void *S, int64_t batch, int64_t 
                                           int64_t Lk, int64_t lds, int causal, void *Pt,
                                           int64_t ldpt, double *energy, void *workspace,
                                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The same weights and energies from row statistics computed by the
+ * producer of S   (Sec. 3.3, attention; the Limitations section's memory
+ * movement of separate passes): rmax_i and rsum_i of
+ * rmm_attention_weights_kmajor are replaced by the caller's
+ *   Pt[u][t][i] = bf16(exp(S[u][i][t] - row_max[u*Lq + i]) * row_rinv[u*Lq + i])
+ * where kept (zeros and energies as there), so that S is read once, by the
+ * weights pass only.  With the statistics of rmm_reduced_qk_rowstats for
+ * the same S the result agrees with rmm_attention_weights_kmajor up to the
+ * order of the fp32 exponential sum.
+ * row_max, row_rinv : float [batch*H*Lq], 4-byte aligned, read.
+ * Other arguments, workspace and errors as rmm_attention_weights_kmajor
+ * (the same workspace size), plus INVALID_ARGUMENT for null statistics and
+ * UNSUPPORTED for misaligned ones.
+ */
+rmm_status_t rmm_attention_weights_kmajor_rowstats(const void *S, int64_t batch, int64_t H, int64_t Lq,
+                                                   int64_t Lk, int64_t lds, int causal,
+                                                   const float *row_max, const float *row_rinv,
+                                                   void *Pt, int64_t ldpt, double *energy,
+                                                   void *workspace, size_t workspace_bytes,
+                                                   hipStream_t stream);
 
 /*
  * Token-axis reduced value product from K-major weights   (Sec. 3.3: O =

@@ -69,7 +69,7 @@ import numpy as np
 __all__ = [
     "retained_count", "column_energies", "topk_indices", "reduced_matmul",
     "rmm", "rmm_batched", "gqa_kv_head", "reduced_qk", "rmm_qk", "reduced_attention",
-    "reduced_pv", "silu", "swiglu", "rmsnorm", "attention_weights",
+    "reduced_pv", "silu", "swiglu", "rmsnorm", "attention_weights", "softmax_row_stats",
     "residual_energy", "retained_energy_fraction", "discarded_energy_ratio",
     "rank_one_bound", "factorized_bound", "normalized_bound",
     "selection_margin",
@@ -325,6 +325,26 @@ def attention_weights(S: np.ndarray) -> np.ndarray:
         w = np.exp(s[keep] - s[keep].max())
         flat_P[i, keep] = w / math.fsum(w.tolist())
     return P
+
+
+def softmax_row_stats(S: np.ndarray):
+    """The two numbers per row that define softmax(S + M) over the last axis
+    (Sec. 3.3, attention): the largest kept score m and the reciprocal of the
+    sum over kept keys of exp(s - m), in float64, as (m, rinv) with the
+    leading shape of S.  Masked entries are -inf and not kept; a row with
+    every entry masked gets (0, 0)."""
+    S = np.asarray(S, dtype=np.float64)
+    flat = S.reshape(-1, S.shape[-1])
+    m = np.zeros(flat.shape[0])
+    rinv = np.zeros(flat.shape[0])
+    for i in range(flat.shape[0]):
+        s = flat[i]
+        keep = s != -np.inf
+        if not keep.any():
+            continue
+        m[i] = s[keep].max()
+        rinv[i] = 1.0 / math.fsum(np.exp(s[keep] - m[i]).tolist())
+    return m.reshape(S.shape[:-1]), rinv.reshape(S.shape[:-1])
 
 
 # ---------------------------------------------------------------------------

@@ -24,7 +24,8 @@ __all__ = [
     "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "rmm_rmsnorm_kmajor",
     "rmm_rmsnorm_kmajor_workspace_size", "rmm_attention_weights_kmajor",
     "rmm_attention_weights_kmajor_workspace_size", "rmm_reduced_pv_kmajor", "rmm_decode_step",
-    "rmm_decode_step_workspace_size", "DecodeGroup", "EXPORTED_SYMBOLS",
+    "rmm_decode_step_workspace_size", "DecodeGroup", "rmm_reduced_qk_rowstats",
+    "rmm_attention_weights_kmajor_rowstats", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librmm.so")
@@ -62,6 +63,11 @@ _SIGS = {
     "rmm_attention_weights_kmajor_workspace_size": (ctypes.c_size_t, [_i64, _i64, _i64, _i64]),
     "rmm_attention_weights_kmajor": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _i64, ctypes.c_int,
                                                     _p, _i64, _p, _p, ctypes.c_size_t, _p]),
+    "rmm_reduced_qk_rowstats": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
+                                               ctypes.c_float, ctypes.c_int, _p, _p, _p, _p]),
+    "rmm_attention_weights_kmajor_rowstats": (ctypes.c_int, [_p, _i64, _i64, _i64, _i64, _i64,
+                                                             ctypes.c_int, _p, _p, _p, _i64, _p, _p,
+                                                             ctypes.c_size_t, _p]),
     "rmm_decode_step_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(DecodeGroup), ctypes.c_int,
                                                          _i64]),
     "rmm_decode_step": (ctypes.c_int, [ctypes.POINTER(DecodeGroup), ctypes.c_int, _i64, _p,
@@ -428,6 +434,37 @@ def rmm_reduced_qk(Q: torch.Tensor, Kc: torch.Tensor, idx: torch.Tensor, S: torc
     return S
 
 
+def rmm_reduced_qk_rowstats(Q: torch.Tensor, Kc: torch.Tensor, idx: torch.Tensor, S: torch.Tensor,
+                            row_max: torch.Tensor, row_rinv: torch.Tensor, causal: bool = True,
+                            scale: float | None = None, stream=None) -> torch.Tensor:
+    """rmm_reduced_qk (bf16) that also writes each score row's softmax
+    statistics: row_max and row_rinv, float32 [batch*H*Lq]."""
+    if Q.dim() != 4 or Kc.dim() != 4 or S.dim() != 4:
+        raise ValueError("Q, Kc and S must be 4-D")
+    batch, H, Lq, D = Q.shape
+    bk, Hkv, Lk, Dk = Kc.shape
+    d = _dev(Q, Kc, idx, S, row_max, row_rinv)
+    if bk != batch or Dk != D or tuple(S.shape) != (batch, H, Lq, Lk):
+        raise ValueError("shapes: Q [b, H, Lq, D], Kc [b, Hkv, Lk, D], S [b, H, Lq, Lk]")
+    for t, n in ((Q, "Q"), (Kc, "Kc"), (S, "S"), (idx, "idx")):
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    if not (Q.dtype == Kc.dtype == S.dtype == torch.bfloat16):
+        raise TypeError("Q, Kc and S must be bfloat16")
+    for t, n in ((row_max, "row_max"), (row_rinv, "row_rinv")):
+        if t.dtype != torch.float32 or t.numel() != batch * H * Lq or not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous float32 [batch*H*Lq]")
+    if idx.dtype != torch.int32 or idx.numel() % (batch * H):
+        raise ValueError("idx must be int32 [batch, H, k]")
+    k = idx.numel() // (batch * H)
+    if scale is None:
+        scale = D ** -0.5
+    _check("rmm_reduced_qk_rowstats", lib.rmm_reduced_qk_rowstats(
+        Q.data_ptr(), Kc.data_ptr(), idx.data_ptr(), batch, H, Hkv, Lq, Lk, D, k, float(scale),
+        1 if causal else 0, S.data_ptr(), row_max.data_ptr(), row_rinv.data_ptr(), _stream(d, stream)))
+    return S
+
+
 def rmm_reduced_attention(Q: torch.Tensor, Kc: torch.Tensor, V: torch.Tensor, idx: torch.Tensor,
                           O: torch.Tensor, causal: bool = True, scale: float | None = None,
                           workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
@@ -653,10 +690,13 @@ def rmm_attention_weights_kmajor_workspace_size(batch: int, H: int, Lq: int, Lk:
 
 def rmm_attention_weights_kmajor(S: torch.Tensor, Pt: torch.Tensor, energy: torch.Tensor,
                                  causal: bool = True, workspace: torch.Tensor | None = None,
-                                 stream=None) -> torch.Tensor:
+                                 stream=None, row_max: torch.Tensor | None = None,
+                                 row_rinv: torch.Tensor | None = None) -> torch.Tensor:
     """Softmax weights of the scores S [batch, H, Lq, Lk] written K-major into
     Pt [batch, H, Lk, Lq] (row stride Pt.stride(-2)), with their token
-    energies (float64 [batch*H*Lk])."""
+    energies (float64 [batch*H*Lk]).  With row_max and row_rinv (float32
+    [batch*H*Lq], e.g. from rmm_reduced_qk_rowstats) the weights use those
+    row statistics (rmm_attention_weights_kmajor_rowstats)."""
     if S.dim() != 4 or Pt.dim() != 4:
         raise ValueError("S and Pt must be 4-D")
     batch, H, Lq, Lk = S.shape
@@ -675,9 +715,21 @@ def rmm_attention_weights_kmajor(S: torch.Tensor, Pt: torch.Tensor, energy: torc
         workspace = torch.empty(max(rmm_attention_weights_kmajor_workspace_size(batch, H, Lq, Lk), 1),
                                 dtype=torch.uint8, device=d)
     ws_bytes = workspace.numel() * workspace.element_size()
-    _check("rmm_attention_weights_kmajor", lib.rmm_attention_weights_kmajor(
-        S.data_ptr(), batch, H, Lq, Lk, S.stride(2), 1 if causal else 0, Pt.data_ptr(), Pt.stride(2),
-        energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+    if (row_max is None) != (row_rinv is None):
+        raise ValueError("give both row_max and row_rinv, or neither")
+    if row_max is None:
+        _check("rmm_attention_weights_kmajor", lib.rmm_attention_weights_kmajor(
+            S.data_ptr(), batch, H, Lq, Lk, S.stride(2), 1 if causal else 0, Pt.data_ptr(),
+            Pt.stride(2), energy.data_ptr(), workspace.data_ptr(), ws_bytes, _stream(d, stream)))
+        return Pt
+    _dev(S, row_max, row_rinv)
+    for t, n in ((row_max, "row_max"), (row_rinv, "row_rinv")):
+        if t.dtype != torch.float32 or t.numel() != batch * H * Lq or not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous float32 [batch*H*Lq]")
+    _check("rmm_attention_weights_kmajor_rowstats", lib.rmm_attention_weights_kmajor_rowstats(
+        S.data_ptr(), batch, H, Lq, Lk, S.stride(2), 1 if causal else 0, row_max.data_ptr(),
+        row_rinv.data_ptr(), Pt.data_ptr(), Pt.stride(2), energy.data_ptr(), workspace.data_ptr(),
+        ws_bytes, _stream(d, stream)))
     return Pt
 
 

@@ -285,6 +285,25 @@ rmm_status_t rmm_reduced_qk(const void *Q, const void *Kc, const int32_t *idx, r
                                        static_cast<float *>(S), stream));
 }
 
+rmm_status_t rmm_reduced_qk_rowstats(const void *Q, const void *Kc, const int32_t *idx, int64_t batch,
+                                     int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
+                                     int64_t k, float scale, int causal, void *S, float *row_max,
+                                     float *row_rinv, hipStream_t stream) {
+    if (!Q || !Kc || !idx || !S || !row_max || !row_rinv) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch < 1 || H < 1 || Hkv < 1 || Lq < 1 || Lk < 1 || D < 1) return RMM_ERR_INVALID_ARGUMENT;
+    if (H % Hkv != 0) return RMM_ERR_INVALID_ARGUMENT;
+    if (k < 1 || k > D) return RMM_ERR_INVALID_ARGUMENT;
+    if (Lq > kInt32Max || Lk > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
+    if (batch * H > kGridYZMax || Lq > kGridYZMax * 64) return RMM_ERR_UNSUPPORTED;
+    if (!rmm::qk_rows_ok(Lk, D, S) || reinterpret_cast<uintptr_t>(row_max) % 4 ||
+        reinterpret_cast<uintptr_t>(row_rinv) % 4)
+        return RMM_ERR_UNSUPPORTED;
+    const hipError_t e = rmm::launch_qk_rowstats_bf16(
+        static_cast<const uint16_t *>(Q), static_cast<const uint16_t *>(Kc), idx, batch, H, Hkv, Lq, Lk,
+        D, k, scale, causal != 0, static_cast<uint16_t *>(S), row_max, row_rinv, stream);
+    return e == hipErrorNotSupported ? RMM_ERR_UNSUPPORTED : from_hip(e);
+}
+
 rmm_status_t rmm_reduced_attention(const void *Q, const void *Kc, const void *V,
                                    const int32_t *idx, rmm_dtype_t dtype, int64_t batch,
                                    int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk, int64_t D,
@@ -456,10 +475,10 @@ size_t rmm_attention_weights_kmajor_workspace_size(int64_t batch, int64_t H, int
     return align256(rmm::weights_workspace_bytes(batch * H, Lq, Lk));
 }
 
-rmm_status_t rmm_attention_weights_kmajor(const void *S, int64_t batch, int64_t H, int64_t Lq,
-                                          int64_t Lk, int64_t lds, int causal, void *Pt,
-                                          int64_t ldpt, double *energy, void *workspace,
-                                          size_t workspace_bytes, hipStream_t stream) {
+static rmm_status_t attention_weights(const void *S, int64_t batch, int64_t H, int64_t Lq, int64_t Lk,
+                                      int64_t lds, int causal, const float *row_max,
+                                      const float *row_rinv, void *Pt, int64_t ldpt, double *energy,
+                                      void *workspace, size_t workspace_bytes, hipStream_t stream) {
     if (!S || !Pt || !energy) return RMM_ERR_INVALID_ARGUMENT;
     if (batch < 1 || H < 1 || Lq < 1 || Lk < 1 || lds < Lk || ldpt < Lq) return RMM_ERR_INVALID_ARGUMENT;
     if (Lq > kInt32Max || Lk > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
@@ -474,8 +493,29 @@ rmm_status_t rmm_attention_weights_kmajor(const void *S, int64_t batch, int64_t 
     if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
     return from_hip(rmm::launch_attention_weights_kmajor(
-        static_cast<const uint16_t *>(S), U, Lq, Lk, lds, causal != 0, static_cast<uint16_t *>(Pt), ldpt,
-        energy, workspace, stream));
+        static_cast<const uint16_t *>(S), U, Lq, Lk, lds, causal != 0, row_max, row_rinv,
+        static_cast<uint16_t *>(Pt), ldpt, energy, workspace, stream));
+}
+
+rmm_status_t rmm_attention_weights_kmajor(const void *S, int64_t batch, int64_t H, int64_t Lq,
+                                          int64_t Lk, int64_t lds, int causal, void *Pt,
+                                          int64_t ldpt, double *energy, void *workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+    return attention_weights(S, batch, H, Lq, Lk, lds, causal, nullptr, nullptr, Pt, ldpt, energy,
+                             workspace, workspace_bytes, stream);
+}
+
+rmm_status_t rmm_attention_weights_kmajor_rowstats(const void *S, int64_t batch, int64_t H, int64_t Lq,
+                                                   int64_t Lk, int64_t lds, int causal,
+                                                   const float *row_max, const float *row_rinv,
+                                                   void *Pt, int64_t ldpt, double *energy,
+                                                   void *workspace, size_t workspace_bytes,
+                                                   hipStream_t stream) {
+    if (!row_max || !row_rinv) return RMM_ERR_INVALID_ARGUMENT;
+    if (reinterpret_cast<uintptr_t>(row_max) % 4 || reinterpret_cast<uintptr_t>(row_rinv) % 4)
+        return RMM_ERR_UNSUPPORTED;
+    return attention_weights(S, batch, H, Lq, Lk, lds, causal, row_max, row_rinv, Pt, ldpt, energy,
+                             workspace, workspace_bytes, stream);
 }
 
 rmm_status_t rmm_reduced_pv_kmajor(const void *Pt, const void *V, const int32_t *idx, int64_t batch,

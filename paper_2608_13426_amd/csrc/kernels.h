@@ -85,10 +85,12 @@ hipError_t launch_score_softmax_kmajor(const uint16_t *S, int64_t B, int64_t M, 
 // softmax weights of attention scores written K-major with their token
 // energies (bf16 S rows 16-byte aligned; checked by the caller); the
 // workspace (weights_workspace_bytes, 256-byte aligned) holds the row
-// statistics and the scoring partials
+// statistics and the scoring partials; with rmax_in and rinv_in given the
+// row statistics are taken from them and not computed
 size_t weights_workspace_bytes(int64_t U, int64_t Lq, int64_t Lk);
 hipError_t launch_attention_weights_kmajor(const uint16_t *S, int64_t U, int64_t Lq, int64_t Lk,
-                                           int64_t lds, int causal, uint16_t *Pt, int64_t ldpt,
+                                           int64_t lds, int causal, const float *rmax_in,
+                                           const float *rinv_in, uint16_t *Pt, int64_t ldpt,
                                            double *energy, void *workspace, hipStream_t stream);
 // the gate|up product with the SwiGLU epilogue: W [K][ldw] holds 2F columns
 // in 128-column blocks (gate, then up, of the same 128 channels); writes the
@@ -161,6 +163,14 @@ hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *
                           int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
                           int64_t Lk, int64_t D, int64_t k, float scale, bool causal,
                           uint16_t *S, hipStream_t stream);
+// the row-major bf16 scores with each row's softmax statistics over its
+// stored kept scores (max, 1 / sum of exp(s - max); 0, 0 for an empty row);
+// hipErrorNotSupported (nothing launched) unless qk_rows_ok
+bool qk_rows_ok(int64_t Lk, int64_t D, const void *S);
+hipError_t launch_qk_rowstats_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *idx,
+                                   int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
+                                   int64_t D, int64_t k, float scale, bool causal, uint16_t *S,
+                                   float *rmax, float *rinv, hipStream_t stream);
 hipError_t launch_qk_f32(const float *Q, const float *Kc, const int32_t *idx,
                          int64_t batch, int64_t H, int64_t Hkv, int64_t Lq,
                          int64_t Lk, int64_t D, int64_t k, float scale, bool causal,

@@ -147,11 +147,19 @@ constexpr int BQ = 128;       // queries per block
 constexpr int kStoreAux = 16;
 }  // namespace rowk
 
-template <int D, int KSMAX, int WQ, int NTT, int BTT>
+// ST: also write each score row's softmax statistics over the stored bf16
+// scores of its kept keys: rmax[row] = their maximum, rinv[row] = 1 / sum of
+// exp(s - rmax) (0 and 0 for a row with nothing kept).  They are taken where
+// the staged tile is read back for its stores: each thread keeps, for each of
+// its rows, a running maximum over its 8-key chunks and a sum rescaled when
+// the maximum rises; a row's threads are consecutive lanes, merged at the end
+// in a fixed butterfly.
+template <int D, int KSMAX, int WQ, int NTT, int BTT, bool ST = false>
 __global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ Kc,
     const int32_t *__restrict__ idx, uint16_t *__restrict__ S, int H, int Hkv, int Lq, int Lk,
-    int k, float scale, int causal) {
+    int k, float scale, int causal, float *__restrict__ rmax = nullptr,
+    float *__restrict__ rinv = nullptr) {
     constexpr int BQ = rowk::BQ, BT = BTT, NT = NTT;
     constexpr int OS = BT + 8;             // staged output row (16-byte aligned)
     typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -190,6 +198,10 @@ __global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
     const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
         Sh + static_cast<int64_t>(q0) * Lk, 0, static_cast<uint32_t>(min(BQ, Lq - q0) * Lk * 2),
         0x00020000);
+    constexpr int SR = BQ / RPP;              // rows per thread in the store role
+    float st_m[SR], st_l[SR];                 // their running statistics (ST)
+#pragma unroll
+    for (int i = 0; i < SR; ++i) { st_m[i] = -__builtin_inff(); st_l[i] = 0.f; }
 
     if (n_compute > 0) {
         const int kp = (k + 15) & ~15;
@@ -253,13 +265,21 @@ __global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
 #pragma unroll
             for (int ks = 0; ks < KSMAX; ++ks)
                 if (ks < KS) qf[j][ks] = frag((wq * FJ + j) * 32 + lr, ks);
-        load_rows(key_rsrc(0));
+        // Each block walks its key tiles starting at a tile of its own and
+        // wrapping around, so that at any moment the blocks store to
+        // different column ranges of their rows (all starting at column 0
+        // measured about 1.5x slower without the causal mask: the row pieces
+        // of simultaneous tiles then share too few memory channels).
+        const int rot = (bh * 5 + qt) % n_compute;
+        auto tile_at = [&](int i) { const int t = i + rot; return t >= n_compute ? t - n_compute : t; };
+        load_rows(key_rsrc(tile_at(0)));
         __syncthreads();
         store_rows();
         __syncthreads();
 
-        for (int kt = 0; kt < n_compute; ++kt) {
-            if (kt + 1 < n_compute) load_rows(key_rsrc(kt + 1));
+        for (int it = 0; it < n_compute; ++it) {
+            const int kt = tile_at(it);
+            if (it + 1 < n_compute) load_rows(key_rsrc(tile_at(it + 1)));
             f32x16_t acc[FI][FJ];
 #pragma unroll
             for (int i = 0; i < FI; ++i)
@@ -314,9 +334,52 @@ __global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
                 const uint32_t off = col < Lk ? static_cast<uint32_t>((r * Lk + col) * 2) : 0x80000000u;
                 const uint4 v = *reinterpret_cast<const uint4 *>(&out_lds[r * OS + c16 * 8]);
                 __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{v.x, v.y, v.z, v.w}, sr, off, 0, kStoreAux);
+                if constexpr (ST) {
+                    // masked keys hold -inf already; a chunk past Lk is not scores
+                    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+                    float e[8];
+                    float cm = -__builtin_inff();
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        e[2 * q] = col < Lk ? __uint_as_float(w[q] << 16) : -__builtin_inff();
+                        e[2 * q + 1] = col < Lk ? __uint_as_float(w[q] & 0xffff0000u) : -__builtin_inff();
+                        cm = fmaxf(cm, fmaxf(e[2 * q], e[2 * q + 1]));
+                    }
+                    const float mm = fmaxf(st_m[i], cm);
+                    if (mm != -__builtin_inff()) {
+                        float l = st_m[i] == -__builtin_inff() ? 0.f : st_l[i] * __expf(st_m[i] - mm);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) l += __expf(e[q] - mm);   // exp(-inf) = 0
+                        st_m[i] = mm;
+                        st_l[i] = l;
+                    }
+                }
             }
-            if (kt + 1 < n_compute) store_rows();
+            if (it + 1 < n_compute) store_rows();
             lds_barrier();
+        }
+    }
+    if constexpr (ST) {
+#pragma unroll
+        for (int i = 0; i < SR; ++i) {
+#pragma unroll
+            for (int sh = 1; sh < CPR; sh <<= 1) {
+                const float m2 = __shfl_xor(st_m[i], sh), l2 = __shfl_xor(st_l[i], sh);
+                const float mm = fmaxf(st_m[i], m2);
+                if (mm != -__builtin_inff()) {
+                    const float a = st_m[i] == -__builtin_inff() ? 0.f : st_l[i] * __expf(st_m[i] - mm);
+                    const float c = m2 == -__builtin_inff() ? 0.f : l2 * __expf(m2 - mm);
+                    st_m[i] = mm;
+                    st_l[i] = a + c;
+                }
+            }
+            const int r = r16 + RPP * i;
+            if (c16 == 0 && q0 + r < Lq) {
+                const int64_t row = static_cast<int64_t>(bh) * Lq + q0 + r;
+                const bool empty = !(st_l[i] > 0.f);
+                rmax[row] = empty ? 0.f : st_m[i];
+                rinv[row] = empty ? 0.f : 1.0f / st_l[i];
+            }
         }
     }
     // key tiles wholly above the diagonal: one contiguous run per row, each
@@ -393,13 +456,34 @@ __global__ __launch_bounds__(256) void qk_f32_kernel(
 
 }  // namespace
 
+bool qk_rows_ok(int64_t Lk, int64_t D, const void *S) {
+    // Lk bound: a block's 128 rows of S are addressed with 32-bit byte offsets
+    return (D == 64 || D == 128) && Lk % 8 == 0 && Lk <= (1 << 22) &&
+           reinterpret_cast<uintptr_t>(S) % 16 == 0;
+}
+
+hipError_t launch_qk_rowstats_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *idx,
+                                   int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
+                                   int64_t D, int64_t k, float scale, bool causal, uint16_t *S,
+                                   float *rmax, float *rinv, hipStream_t stream) {
+    if (!qk_rows_ok(Lk, D, S)) return hipErrorNotSupported;
+    dim3 grid(static_cast<unsigned>((Lq + rowk::BQ - 1) / rowk::BQ), static_cast<unsigned>(batch * H));
+    const bool wide = D == 128 && k <= 96;
+    auto kern = D == 64 ? qk_bf16_rows_kernel<64, 4, 1, 256, 128, true>
+              : k <= 64 ? qk_bf16_rows_kernel<128, 4, 1, 512, 256, true>
+              : k <= 96 ? qk_bf16_rows_kernel<128, 8, 2, 512, 256, true>
+                        : qk_bf16_rows_kernel<128, 8, 2, 256, 128, true>;
+    hipLaunchKernelGGL(kern, grid, dim3(wide ? 512 : 256), 0, stream, Q, Kc, idx, S,
+                       static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
+                       static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0, rmax, rinv);
+    return hipGetLastError();
+}
+
 hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *idx,
                           int64_t batch, int64_t H, int64_t Hkv, int64_t Lq, int64_t Lk,
                           int64_t D, int64_t k, float scale, bool causal, uint16_t *S,
                           hipStream_t stream) {
-    // Lk bound: a block's 128 rows of S are addressed with 32-bit byte offsets
-    const bool rows_ok = (D == 64 || D == 128) && Lk % 8 == 0 && Lk <= (1 << 22) &&
-                         reinterpret_cast<uintptr_t>(S) % 16 == 0;
+    const bool rows_ok = qk_rows_ok(Lk, D, S);
     if (rows_ok) {
         dim3 grid(static_cast<unsigned>((Lq + rowk::BQ - 1) / rowk::BQ),
                   static_cast<unsigned>(batch * H));
@@ -414,7 +498,8 @@ hipError_t launch_qk_bf16(const uint16_t *Q, const uint16_t *Kc, const int32_t *
                             : qk_bf16_rows_kernel<128, 8, 2, 256, 128>;
         hipLaunchKernelGGL(kern, grid, dim3(wide ? 512 : 256), 0, stream, Q, Kc, idx, S,
                            static_cast<int>(H), static_cast<int>(Hkv), static_cast<int>(Lq),
-                           static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0);
+                           static_cast<int>(Lk), static_cast<int>(k), scale, causal ? 1 : 0,
+                           nullptr, nullptr);
         return hipGetLastError();
     }
     constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2;

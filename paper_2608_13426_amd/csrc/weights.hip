@@ -104,12 +104,16 @@ size_t weights_workspace_bytes(int64_t U, int64_t Lq, int64_t Lk) {
 }
 
 hipError_t launch_attention_weights_kmajor(const uint16_t *S, int64_t U, int64_t Lq, int64_t Lk,
-                                           int64_t lds, int causal, uint16_t *Pt, int64_t ldpt,
+                                           int64_t lds, int causal, const float *rmax_in,
+                                           const float *rinv_in, uint16_t *Pt, int64_t ldpt,
                                            double *energy, void *workspace, hipStream_t stream) {
     char *ws = static_cast<char *>(workspace);
     float *rmax = reinterpret_cast<float *>(ws);
     float *rinv = reinterpret_cast<float *>(ws + align256(static_cast<size_t>(U * Lq) * sizeof(float)));
     double *partials = reinterpret_cast<double *>(ws + 2 * align256(static_cast<size_t>(U * Lq) * sizeof(float)));
+    if (rmax_in && rinv_in)
+        return launch_score_softmax_kmajor(S, U, Lq, Lk, lds, rmax_in, rinv_in, Lk - Lq, causal, energy,
+                                           partials, Pt, ldpt, stream);
     const int64_t rows = U * Lq, per = kRowThreads / 64;
     hipLaunchKernelGGL(softmax_rowstats_kernel, dim3(static_cast<unsigned>((rows + per - 1) / per)),
                        dim3(kRowThreads), 0, stream, S, U, Lq, Lk, lds, causal, rmax, rinv);

@@ -507,6 +507,32 @@ def check_attention_weights(o):
     assert np.allclose(o.attention_weights(S).sum(axis=-1), 1.0, rtol=1e-14, atol=0)
 
 
+def check_softmax_row_stats(o):
+    # two keys 0 and ln 3: the maximum is ln 3 and the sum 1/3 + 1
+    m, rinv = o.softmax_row_stats(np.array([[0.0, math.log(3.0)]]))
+    assert m[0] == math.log(3.0) and abs(rinv[0] - 0.75) <= 1e-15
+    # n equal scores: 1/n; masked keys do not count; an empty row is (0, 0);
+    # the maximum is taken over the kept keys only
+    S = np.array([[2.5, 2.5, 2.5, 2.5], [1.0, -np.inf, 1.0, -np.inf], [-np.inf] * 4,
+                  [-7.0, -np.inf, -9.0, -np.inf]])
+    m, rinv = o.softmax_row_stats(S)
+    assert list(m) == [2.5, 1.0, 0.0, -7.0]
+    assert np.allclose(rinv, [0.25, 0.5, 0.0, 1.0 / (1.0 + math.exp(-2.0))], rtol=1e-15, atol=0)
+    # statistics over the last axis: a [2, 3, 5] input gives [2, 3] pairs; the
+    # maximum moves with a shift, the sum does not
+    rng = np.random.default_rng(8)
+    S = rng.standard_normal((2, 3, 5))
+    m, rinv = o.softmax_row_stats(S)
+    assert m.shape == (2, 3) and np.array_equal(m, S.max(axis=-1))
+    m2, rinv2 = o.softmax_row_stats(S + 4.0)
+    assert np.allclose(m2, m + 4.0, rtol=0, atol=1e-14) and np.allclose(rinv2, rinv, rtol=1e-14, atol=0)
+    # with a brute-force sum of exp(s - m) over the row
+    for i in range(2):
+        for j in range(3):
+            tot = sum(math.exp(float(v) - float(m[i, j])) for v in S[i, j])
+            assert abs(rinv[i, j] * tot - 1.0) <= 1e-14
+
+
 def check_margin(o):
     assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
     assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
@@ -516,4 +542,5 @@ def check_margin(o):
 
 ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
               check_bounds, check_worked_example, check_qk, check_attention, check_pv,
-              check_swiglu, check_rmsnorm, check_attention_weights, check_margin)
+              check_swiglu, check_rmsnorm, check_attention_weights, check_softmax_row_stats,
+              check_margin)

@@ -544,3 +544,46 @@ def test_decode_step_validation():
     assert need > 0                                    # one token: the list is split over slices
     assert f(arr(), 1, 1, NULL, 0, NULL) == WS_SMALL
     assert f(arr(), 1, 1, P, need - 1, NULL) == WS_SMALL
+
+
+def test_reduced_qk_rowstats_validation():
+    f = rmm.lib.rmm_reduced_qk_rowstats
+    # Q, Kc, idx, batch, H, Hkv, Lq, Lk, D, k, scale, causal, S, row_max, row_rinv, stream
+    base = [P, P, P, 1, 4, 2, 64, 96, 128, 64, 0.125, 1, P, P, P, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 1, 2, 12, 13, 14):
+        assert call(i, NULL) == INVALID
+    assert call(5, 3) == INVALID              # H % Hkv
+    assert call(9, 0) == INVALID              # k
+    assert call(9, 129) == INVALID
+    assert call(8, 96) == UNSUPPORTED         # D not 64 or 128
+    assert call(7, 100) == UNSUPPORTED        # Lk % 8
+    assert call(12, ctypes.c_void_p(0x100008)) == UNSUPPORTED   # S not 16-byte aligned
+    assert call(13, ctypes.c_void_p(0x100002)) == UNSUPPORTED   # misaligned statistics
+
+
+def test_attention_weights_kmajor_rowstats_validation():
+    f = rmm.lib.rmm_attention_weights_kmajor_rowstats
+    need = rmm.rmm_attention_weights_kmajor_workspace_size(1, 2, 64, 96)
+    # S, batch, H, Lq, Lk, lds, causal, row_max, row_rinv, Pt, ldpt, energy, ws, bytes, stream
+    base = [P, 1, 2, 64, 96, 96, 1, P, P, P, 64, P, P, need, NULL]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return f(*a)
+
+    for i in (0, 7, 8, 9, 11):
+        assert call(i, NULL) == INVALID
+    assert call(5, 90) == INVALID             # lds < Lk
+    assert call(10, 60) == INVALID            # ldpt < Lq
+    assert call(5, 100) == UNSUPPORTED        # lds % 8
+    assert call(8, ctypes.c_void_p(0x100002)) == UNSUPPORTED   # misaligned statistics
+    assert call(12, NULL) == WS_SMALL
+    assert call(13, need - 1) == WS_SMALL
+    assert call(12, ctypes.c_void_p(0x100008)) == INVALID

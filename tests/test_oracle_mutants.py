@@ -263,7 +263,27 @@ def _aw_no_max(S):                     # no shift by the row max and no empty-ro
         return E / E.sum(axis=-1, keepdims=True)
 
 
+def _rs_min(S):                        # the row minimum instead of the maximum
+    S = np.asarray(S, dtype=np.float64)
+    keep = np.isfinite(S)
+    m = np.where(keep.any(axis=-1), np.min(np.where(keep, S, np.inf), axis=-1), 0.0)
+    e = np.where(keep, np.exp(np.where(keep, S, 0.0) - m[..., None]), 0.0).sum(axis=-1)
+    return m, np.where(e > 0, 1.0 / np.where(e > 0, e, 1.0), 0.0)
+
+
+def _rs_sum_not_recip(S):              # the sum, not its reciprocal
+    m, rinv = ro_softmax_row_stats(S)
+    return m, np.where(rinv > 0, 1.0 / np.where(rinv > 0, rinv, 1.0), 0.0)
+
+
+def _rs_over_first_axis(S):            # statistics over the first axis
+    S = np.asarray(S, dtype=np.float64)
+    m, rinv = ro_softmax_row_stats(np.moveaxis(S, 0, -1))
+    return m.T if m.ndim == 2 else m, rinv.T if rinv.ndim == 2 else rinv
+
+
 ro_attention_weights = ro.attention_weights
+ro_softmax_row_stats = ro.softmax_row_stats
 
 MUTANTS = {
     "rmsnorm_sum_not_mean": ("rmsnorm", _rms_sum),
@@ -273,6 +293,9 @@ MUTANTS = {
     "weights_over_queries": ("attention_weights", _aw_over_queries),
     "weights_unnormalised": ("attention_weights", _aw_unnormalised),
     "weights_masked_row_nan": ("attention_weights", _aw_no_max),
+    "rowstats_min": ("softmax_row_stats", _rs_min),
+    "rowstats_sum_not_recip": ("softmax_row_stats", _rs_sum_not_recip),
+    "rowstats_over_first_axis": ("softmax_row_stats", _rs_over_first_axis),
     "silu_is_sigmoid": ("silu", _silu_sigmoid),
     "silu_sign": ("silu", _silu_sign),
     "swiglu_swapped": ("swiglu", _swiglu_swapped),
