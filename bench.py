@@ -86,21 +86,21 @@ def _sources(main):
 # file, the shared headers and the build script) is the one it was measured
 # with, and for the same launch mix; re-run the counters after any change.
 GEMM_TRAFFIC = {"sources": _sources("gemm.hip"),
-                "sha256": "46521fd8443677785dd42eeb429fb82a7e6f5cbf4a313acdb25c8f08134be0f6",
+                "sha256": "320468af771bcd41da7ab34a97e30d62b659662958eaeb48460ed0c7c62006f5",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
-                "bytes": round((399487.78 * 2.0 + 172205.10) * 1024)}
+                "bytes": round((399472.02 * 2.0 + 172236.73) * 1024)}
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"sources": _sources("attn.hip"),
-                "sha256": "79e5d1b3403e7f09ad5106e4faae95093d6e9e88e435f6c921e6da50f7e12dd3",
+                "sha256": "384857b27a513e02c7be105e3b17521ec02b241ab45dd2c72255443d1a15549a",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0",
-                "bytes": round((103417.58 * 2.0 + 65545.13 + 8249.04 * 2.0 + 40960.00) * 1024)}
+                "bytes": round((103749.28 * 2.0 + 65552.71 + 8249.04 * 2.0 + 40960.00) * 1024)}
 # per rmm_rmsnorm_kmajor call (8192 x 4096): rms_rowscale_kernel, the
 # normalising score_tile_kernel and its score_finalize_kernel
 NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip")],
-                "sha256": "5cc677544347de159e47c3c26c8f7e6530f3de50ea6b970e79e54b04ec79030f",
+                "sha256": "b052756bdffce5d525515347f00c82c66fddbc9c99c2f4938e11a30c2b39fe2f",
                 "mix": "layer_8b attn_in,mlp_in r=0.25,0.5,0.75,1.0",
-                "bytes": round((32784.54 * 2.0 + 64.06 + 32983.86 * 2.0 + 66560.00 +
+                "bytes": round((32784.52 * 2.0 + 64.07 + 32984.46 * 2.0 + 66560.00 +
                                 532.50 * 2.0 + 32.00) * 1024)}
 
 
