@@ -324,19 +324,26 @@ __global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
                     }
                 }
             lds_barrier();
+            const int col = kt * BT + c16 * 8;
+            uint4 staged[BQ / RPP];
 #pragma unroll
             for (int i = 0; i < BQ / RPP; ++i) {
                 const int r = r16 + RPP * i;
-                const int col = kt * BT + c16 * 8;
                 // unconditional (a column past Lk goes out of range): a branch
                 // here would make the compiler's wait for the next K rows also
                 // wait for these stores
                 const uint32_t off = col < Lk ? static_cast<uint32_t>((r * Lk + col) * 2) : 0x80000000u;
                 const uint4 v = *reinterpret_cast<const uint4 *>(&out_lds[r * OS + c16 * 8]);
                 __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{v.x, v.y, v.z, v.w}, sr, off, 0, kStoreAux);
-                if constexpr (ST) {
-                    // masked keys hold -inf already; a chunk past Lk is not scores
-                    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+                staged[i] = v;
+            }
+            if constexpr (ST) {
+                // After the stores are issued, so that this work overlaps their
+                // drain, and without branches, for the same reason as above.
+                // Masked keys hold -inf already; a chunk past Lk is not scores.
+#pragma unroll
+                for (int i = 0; i < BQ / RPP; ++i) {
+                    const uint32_t w[4] = {staged[i].x, staged[i].y, staged[i].z, staged[i].w};
                     float e[8];
                     float cm = -__builtin_inff();
 #pragma unroll
@@ -346,13 +353,13 @@ __global__ __launch_bounds__(NTT, NTT == 256 ? 2 : 1) void qk_bf16_rows_kernel(
                         cm = fmaxf(cm, fmaxf(e[2 * q], e[2 * q + 1]));
                     }
                     const float mm = fmaxf(st_m[i], cm);
-                    if (mm != -__builtin_inff()) {
-                        float l = st_m[i] == -__builtin_inff() ? 0.f : st_l[i] * __expf(st_m[i] - mm);
+                    // with nothing kept so far every term below is exp(-inf) = 0
+                    const float mref = mm == -__builtin_inff() ? 0.f : mm;
+                    float l = st_l[i] * __expf(st_m[i] - mref);
 #pragma unroll
-                        for (int q = 0; q < 8; ++q) l += __expf(e[q] - mm);   // exp(-inf) = 0
-                        st_m[i] = mm;
-                        st_l[i] = l;
-                    }
+                    for (int q = 0; q < 8; ++q) l += __expf(e[q] - mref);
+                    st_m[i] = mm;
+                    st_l[i] = l;
                 }
             }
             if (it + 1 < n_compute) store_rows();
