@@ -92,7 +92,7 @@ GEMM_TRAFFIC = {"sources": _sources("gemm.hip"),
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"sources": _sources("attn.hip"),
-                "sha256": "384857b27a513e02c7be105e3b17521ec02b241ab45dd2c72255443d1a15549a",
+                "sha256": "43d88ffe69ffba77bf469fb0f9867149c80882c050f19f3f9483cd791909b4d2",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0",
                 "bytes": round((103749.28 * 2.0 + 65552.71 + 8249.04 * 2.0 + 40960.00) * 1024)}
 # per rmm_rmsnorm_kmajor call (8192 x 4096): rms_rowscale_kernel, the

@@ -8,9 +8,9 @@
 //      past k (kp = 16 * KS >= k).  This is H*Lk*kp bf16 of workspace, read
 //      back once per query tile; it turns the per-tile key gather into plain
 //      16-byte rows.
-//   2. attn_fwd_kernel: one workgroup per (head, 256 queries), four waves of
-//      64 queries (two 32-query blocks sharing every K and V fragment), a
-//      three-slot LDS ring of 64-key tiles filled by LDS DMA two tiles ahead:
+//   2. attn_fwd_kernel: one workgroup per (head, 256 queries), eight waves
+//      of 32 queries (two per SIMD), a four-slot LDS ring of 64-key tiles
+//      filled by LDS DMA two tiles ahead:
 //        * S^T = Ki Q_I^T per tile (v_mfma_f32_32x32x16_bf16; Q's retained
 //          dims gathered once into registers), so a lane holds 16 keys of
 //          one query and the row max needs one exchange with the lane 32
@@ -22,7 +22,9 @@
 //          tile's max exceeds it by more than 8 (log2 units), so weights
 //          stay <= 256 and most tiles skip the rescale;
 //        * O^T += V^T P^T with the weights rounded to bf16 as the MFMA's
-//          second operand and V^T read with the gfx950 transposing LDS read.
+//          second operand and V^T read with the gfx950 transposing LDS read;
+//        * the two waves of a SIMD take the softmax at opposite ends of a
+//          step, so one's exponentials meet the other's MFMAs.
 //      A query with no unmasked key gets O = 0.
 #include <type_traits>
 
