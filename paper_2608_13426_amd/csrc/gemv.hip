@@ -161,51 +161,59 @@ __global__ __launch_bounds__(gv::NT) void gemv_partial_grouped_kernel(GemvGroups
                        chunk, s, b, q.S == 1);
 }
 
-// Y[b][m][n] = sum over slices s, in order, of P[b][s][m][n]
+// The slice reduction of one 64-column piece: the 256 threads are 64
+// columns (one per lane) x 4 waves; wave w adds slices [w*S/4, (w+1)*S/4)
+// in slice order (eight loads in flight), and the four quarter sums are
+// added in wave order.  p points at slice 0 of the lane's column; slice s
+// is st floats further.  Returns the sum in wave 0 (other waves: garbage).
+__device__ __forceinline__ float reduce_slices(const float *__restrict__ p, int64_t st, int S,
+                                               bool col_ok) {
+    __shared__ float quarter[3][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int s0 = w * S / 4, s1 = (w + 1) * S / 4;
+    float sum = 0.f;
+    if (col_ok) {
+        int s = s0;
+        for (; s + 8 <= s1; s += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[(s + u) * st];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) sum += v[u];
+        }
+        for (; s < s1; ++s) sum += p[s * st];
+    }
+    if (w > 0) quarter[w - 1][lane] = sum;
+    __syncthreads();
+    if (w == 0) sum = ((sum + quarter[0][lane]) + quarter[1][lane]) + quarter[2][lane];
+    return sum;
+}
+
+// Y[b][m][n] = the slices' partials P[b][s][m][n] added in the order of
+// reduce_slices; workgroup (x, m, b) covers columns 64x .. 64x+63
 __global__ __launch_bounds__(256) void gemv_reduce_kernel(const float *__restrict__ P,
                                                           uint16_t *__restrict__ Y, int M, int N,
                                                           int S, int64_t ldy) {
-    const int n = blockIdx.x * 256 + threadIdx.x;
+    const int n = blockIdx.x * 64 + (threadIdx.x & 63);
     const int m = blockIdx.y, b = blockIdx.z;
-    if (n >= N) return;
     const float *p = P + (static_cast<int64_t>(b) * S * M + m) * N + n;
-    const int64_t st = static_cast<int64_t>(M) * N;
-    float sum = 0.f;
-    int s = 0;
-    for (; s + 8 <= S; s += 8) {               // eight loads in flight, added in slice order
-        float v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = p[(s + u) * st];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) sum += v[u];
-    }
-    for (; s < S; ++s) sum += p[s * st];
-    Y[(static_cast<int64_t>(b) * M + m) * ldy + n] = f32_to_bf16(sum);
+    const float sum = reduce_slices(p, static_cast<int64_t>(M) * N, S, n < N);
+    if (threadIdx.x < 64 && n < N) Y[(static_cast<int64_t>(b) * M + m) * ldy + n] = f32_to_bf16(sum);
 }
 
 // the slice reduction of every group with more than one slice: workgroup
-// blockIdx.x of group g covers 256 columns of one unit, numbered from rfirst[g]
+// blockIdx.x of group g covers 64 columns of one unit, numbered from rfirst[g]
 __global__ __launch_bounds__(256) void gemv_reduce_grouped_kernel(GemvGroups G) {
     int g = -1;
     for (int i = 0; i < G.n; ++i)
         if (G.g[i].S > 1 && static_cast<int>(blockIdx.x) >= G.g[i].rfirst) g = i;
     const GemvGroup &q = G.g[g];
     const int local = static_cast<int>(blockIdx.x) - q.rfirst;
-    const int nb = (q.N + 255) / 256;
-    const int b = local / nb, n = (local % nb) * 256 + static_cast<int>(threadIdx.x);
-    if (n >= q.N) return;
+    const int nb = (q.N + 63) / 64;
+    const int b = local / nb, n = (local % nb) * 64 + static_cast<int>(threadIdx.x & 63);
     const float *p = q.P + static_cast<int64_t>(b) * q.S * q.N + n;
-    float sum = 0.f;
-    int s = 0;
-    for (; s + 8 <= q.S; s += 8) {
-        float v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = p[static_cast<int64_t>(s + u) * q.N];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) sum += v[u];
-    }
-    for (; s < q.S; ++s) sum += p[static_cast<int64_t>(s) * q.N];
-    q.Y[static_cast<int64_t>(b) * q.ldy + n] = f32_to_bf16(sum);
+    const float sum = reduce_slices(p, q.N, q.S, n < q.N);
+    if (threadIdx.x < 64 && n < q.N) q.Y[static_cast<int64_t>(b) * q.ldy + n] = f32_to_bf16(sum);
 }
 
 template <int MR, bool VEC>
@@ -225,7 +233,7 @@ hipError_t launch_mr(const uint16_t *X, const uint16_t *W, const int32_t *idx, i
                        static_cast<int>(k), ldx, ldw, ldy, SR, S);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    dim3 rgrid(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(M), static_cast<unsigned>(B));
+    dim3 rgrid(static_cast<unsigned>((N + 63) / 64), static_cast<unsigned>(M), static_cast<unsigned>(B));
     hipLaunchKernelGGL(gemv_reduce_kernel, rgrid, dim3(256), 0, stream, P, Y, static_cast<int>(M),
                        static_cast<int>(N), S, ldy);
     return hipGetLastError();
@@ -272,7 +280,7 @@ hipError_t launch_gemv_grouped_bf16(GemvGroups G, int64_t B, hipStream_t stream)
         q.first = blocks;
         blocks += q.chunks * q.S * static_cast<int>(B);
         q.rfirst = rblocks;
-        if (q.S > 1) rblocks += (q.N + 255) / 256 * static_cast<int>(B);
+        if (q.S > 1) rblocks += (q.N + 63) / 64 * static_cast<int>(B);
     }
     hipLaunchKernelGGL(gemv_partial_grouped_kernel, dim3(static_cast<unsigned>(blocks)), dim3(gv::NT), 0,
                        stream, G);

@@ -229,6 +229,13 @@ template <int NT, int C>
 __device__ __forceinline__ void select_token16(const uint16_t *__restrict__ x, int K, int k,
                                                int32_t *__restrict__ out) {
     static_assert(C % 8 == 0 && C <= 16 && NT >= 256 && NT <= 1024, "chunk");
+    // The keys of a token bunch up in a few digits (one per binary exponent),
+    // so one histogram would take most of a wave's 64 increments on one
+    // word.  Lanes count into HR copies (lane % HR), HR + 1 words apart so
+    // that one digit's copies sit in different banks, and the copies are
+    // summed before the scan.
+    constexpr int HR = 16, HS = 257;
+    __shared__ uint32_t hcopy[HR * HS];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t scan_buf[NT / kWave];
     __shared__ int s_thr, s_need;
@@ -254,16 +261,24 @@ __device__ __forceinline__ void select_token16(const uint16_t *__restrict__ x, i
     // pass 1 over bits 14..7, pass 2 over bits 6..0 of the keys in the chosen bucket
     int need = k, thr = -1, take_ties = 0;
     int prefix = -1;                    // pass-1 digit, once chosen
+    uint32_t *hmine = hcopy + (lane % HR) * HS;
 #pragma unroll
     for (int pass = 0; pass < 2; ++pass) {
-        if (tid < 256) hist[tid] = 0;
+        for (int j = tid; j < HR * HS; j += NT) hcopy[j] = 0;
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const uint32_t u = key[c];
             if (u & 0x8000u) continue;
-            if (pass == 0) atomicAdd(&hist[u >> 7], 1u);
-            else if (static_cast<int>(u >> 7) == prefix) atomicAdd(&hist[u & 0x7fu], 1u);
+            if (pass == 0) atomicAdd(&hmine[u >> 7], 1u);
+            else if (static_cast<int>(u >> 7) == prefix) atomicAdd(&hmine[u & 0x7fu], 1u);
+        }
+        __syncthreads();
+        if (tid < 256) {
+            uint32_t t = 0;
+#pragma unroll
+            for (int r = 0; r < HR; ++r) t += hcopy[r * HS + tid];
+            hist[tid] = t;
         }
         __syncthreads();
         if (tid < kWave) {
@@ -289,7 +304,7 @@ __device__ __forceinline__ void select_token16(const uint16_t *__restrict__ x, i
         }
         __syncthreads();
         const int d = s_thr, nb = s_need, size = static_cast<int>(hist[0]);
-        __syncthreads();                // hist is cleared by the next pass
+        __syncthreads();                // hist is rewritten by the next pass
         if (pass == 0) {
             if (size == nb) { thr = (d << 7) - 1; take_ties = 0; break; }   // the whole bucket
             prefix = d;
