@@ -83,6 +83,12 @@ template <int NT, int C, bool REG, int SRC>
 __global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src, int64_t ld,
                                                     int64_t K, int64_t k, int cpt,
                                                     int32_t *__restrict__ idx) {
+    // lanes count into HR copies of the histogram (lane % HR), HR + 1 words
+    // apart so that one digit's copies sit in different banks: the keys of a
+    // unit often share a digit, and one copy would take most of a wave's
+    // increments on one word
+    constexpr int HR = 16, HS = 257;
+    __shared__ uint32_t hcopy[HR * HS];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t scan_buf[NT / kWave];
     __shared__ uint32_t s_digit, s_above, s_count;
@@ -149,22 +155,30 @@ __global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src
         prefix = kmax & mask;
     }
     uint32_t need = static_cast<uint32_t>(k);
+    uint32_t *hmine = hcopy + (tid % HR) * HS;
     while (top >= 0) {
         // digit: bits top .. shift (up to 8 of them)
         const int shift = max(0, top - 7);
         const uint64_t dmask = (1ull << (top - shift + 1)) - 1;
-        for (int i = tid; i < 256; i += NT) hist[i] = 0;
+        for (int i = tid; i < HR * HS; i += NT) hcopy[i] = 0;
         __syncthreads();
         if constexpr (REG) {
 #pragma unroll
             for (int c = 0; c < C; ++c)
                 if (c < n_own && (keys[c] & mask) == prefix)
-                    atomicAdd(&hist[(keys[c] >> shift) & dmask], 1u);
+                    atomicAdd(&hmine[(keys[c] >> shift) & dmask], 1u);
         } else {
             for (int c = 0; c < n_own; ++c) {
                 const uint64_t u = key_at(c);
-                if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & dmask], 1u);
+                if ((u & mask) == prefix) atomicAdd(&hmine[(u >> shift) & dmask], 1u);
             }
+        }
+        __syncthreads();
+        for (int i = tid; i < 256; i += NT) {
+            uint32_t t = 0;
+#pragma unroll
+            for (int r = 0; r < HR; ++r) t += hcopy[r * HS + i];
+            hist[i] = t;
         }
         __syncthreads();
         if (tid < kWave) {
