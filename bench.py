@@ -536,7 +536,8 @@ def time_norm_chain(L, name, r, steps, warmup, eps=1e-5):
 
 def time_pv_chain(L, r, steps, warmup, bufs):
     """The value product fed by its producer, on the layer's causal scores S
-    (the sweep's last ratio: r = 1 in the default run) and values V:
+    (those of the headline ratio: per head the reduced QK^T over k = 64 of
+    the 128 dims) and values V:
       reduced : rmm_attention_weights_kmajor (softmax weights written K-major
                 with their token energies; the masked half of S is never
                 read) -> TopK of the token energies per head ->
@@ -627,9 +628,9 @@ def time_pv_chain(L, r, steps, warmup, bufs):
 
 def attention_weights(L):
     """P = softmax(S) per head, in place in L.S (bf16).  S holds the causal
-    scores of the sweep's last ratio (r = 1 in the default run: the full
-    QK^T/sqrt(D)), so P is the layer's attention weights (masked entries
-    -inf -> weight 0)."""
+    scores of the headline ratio (one untimed step at r = 0.5 leaves them
+    there: per head the reduced QK^T over 64 of the 128 dims, scaled), so P
+    is the layer's attention weights (masked entries -inf -> weight 0)."""
     import torch
     a = L.wk.attention
     for h in range(a.H):
@@ -1074,6 +1075,11 @@ def main():
                          "achieved": round(d_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(d_ach / PEAK_HBM_GBS, 4), "traffic": None},
         }
+    if not (args.no_pv_chain and args.no_pv):
+        # the value-product records take the layer's causal scores at the
+        # headline ratio (one untimed step leaves them in L.S, with the
+        # per-head selection in L.qidx), whatever ran before
+        run_step(L, HEADLINE_R)
     if not args.no_pv_chain:
         import torch
         import paper_2608_13426_amd as rmm
