@@ -95,13 +95,12 @@ ATTN_TRAFFIC = {"sources": _sources("attn.hip"),
                 "sha256": "43d88ffe69ffba77bf469fb0f9867149c80882c050f19f3f9483cd791909b4d2",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0",
                 "bytes": round((103749.28 * 2.0 + 65552.71 + 8249.04 * 2.0 + 40960.00) * 1024)}
-# per rmm_rmsnorm_kmajor call (8192 x 4096): rms_rowscale_kernel, the
-# normalising score_tile_kernel and its score_finalize_kernel
+# per rmm_rmsnorm_kmajor call (8192 x 4096, the same whatever r):
+# rms_block_kmajor_kernel and its score_finalize_grouped_kernel
 NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip")],
-                "sha256": "b052756bdffce5d525515347f00c82c66fddbc9c99c2f4938e11a30c2b39fe2f",
-                "mix": "layer_8b attn_in,mlp_in r=0.25,0.5,0.75,1.0",
-                "bytes": round((32784.52 * 2.0 + 64.07 + 32984.46 * 2.0 + 66560.00 +
-                                532.50 * 2.0 + 32.00) * 1024)}
+                "sha256": "58e8ff81198e8e72fe4030d63df52bfc93539c055743b1f6836cb37506f1e712",
+                "mix": "layer_8b attn_in,mlp_in",
+                "bytes": round((33033.23 * 2.0 + 74515.35 + 4115.00 * 2.0 + 32.00) * 1024)}
 
 
 def sources_sha256(paths):
@@ -1036,16 +1035,16 @@ def main():
                   "rmm_rmsnorm_kmajor writes the normalised rows K-major with their column "
                   "energies in one pass over X (no scoring pass), unfused = torch RMSNorm, "
                   "rmm_score_kmajor; both then TopK and the K-major GEMM (q|k|v or gate|up)",
-            "kernels": ["rms_rowscale_kernel", "score_tile_kernel (normalising variant)",
-                        "score_finalize_kernel", "select_kernel", "gemm_kmajor_tr_kernel"],
+            "kernels": ["rms_block_kmajor_kernel", "score_finalize_grouped_kernel",
+                        "select_kernel", "gemm_kmajor_tr_kernel"],
             "per_input_ratio": nc,
-            "roofline": {"bound": "hbm", "kernel": "rmm_rmsnorm_kmajor (all three kernels)",
+            "roofline": {"bound": "hbm", "kernel": "rmm_rmsnorm_kmajor (both kernels)",
                          "achieved": round(p_b / (p_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(p_b / (p_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
                          "bytes_basis": "one read of X + one write of Xt + the energies per call",
                          "traffic": recorded_traffic(
-                             NORM_TRAFFIC, f"{wk.name} attn_in,mlp_in r={','.join(str(r) for r in sorted(sweep))}"),
-                         "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, all three kernels)"},
+                             NORM_TRAFFIC, f"{wk.name} attn_in,mlp_in"),
+                         "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, both kernels)"},
         }
     if not args.no_decode:
         dec = {r: time_decode(L, r, args.steps, args.warmup) for r in sorted(sweep)}

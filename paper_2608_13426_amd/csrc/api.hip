@@ -143,8 +143,10 @@ rmm_status_t rmm_rmsnorm_kmajor(const void *X, const void *gamma, float eps, int
     if (!(eps >= 0.f) || std::isinf(eps)) return RMM_ERR_INVALID_ARGUMENT;   // also NaN
     if (M > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
     if (K % 8 || K > kInt32Max || B > kGridYZMax) return RMM_ERR_UNSUPPORTED;
-    // the tile kernel addresses one row split with 32-bit byte offsets
-    if (rmm::score_rows_per_split(B, M, K) * ldx * 2 >= (int64_t(1) << 31)) return RMM_ERR_UNSUPPORTED;
+    // the two-pass tile kernel addresses one row split with 32-bit byte offsets
+    if (!rmm::rmsnorm_single_pass(K, ldx) &&
+        rmm::score_rows_per_split(B, M, K) * ldx * 2 >= (int64_t(1) << 31))
+        return RMM_ERR_UNSUPPORTED;
     if (!aligned16(X) || !aligned16(gamma) || !aligned16(Xt) || ldx % 8 || ldxt % 8 ||
         reinterpret_cast<uintptr_t>(energy) % 8)
         return RMM_ERR_UNSUPPORTED;

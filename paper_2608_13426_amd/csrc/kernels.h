@@ -19,6 +19,10 @@ int64_t score_rows_per_split(int64_t B, int64_t M, int64_t K);
 // energy[b][j] = sum over s = 0..S-1, in order, of partials[b][s][j]
 hipError_t launch_score_finalize(const double *partials, int64_t B, int64_t S, int64_t K,
                                  double *energy, hipStream_t stream);
+// the same sum for many splits (a fixed order of its own: 16 consecutive
+// runs of splits, each in order, then the runs in order)
+hipError_t launch_score_finalize_grouped(const double *partials, int64_t B, int64_t S, int64_t K,
+                                         double *energy, hipStream_t stream);
 int64_t score_splits(int64_t B, int64_t M, int64_t K);
 size_t score_workspace_bytes(int64_t B, int64_t M, int64_t K);
 
@@ -36,8 +40,11 @@ hipError_t launch_score_norm_kmajor(const uint16_t *X, int64_t B, int64_t M, int
                                    double *partials, uint16_t *Xt, int64_t ldxt, hipStream_t stream);
 // RMSNorm writing the K-major normalised activations and their column
 // energies (bf16, K % 8 == 0, 16-byte aligned rows; checked by the caller);
-// the workspace (rmsnorm_workspace_bytes, 256-byte aligned) holds the row
-// scales and the scoring partials
+// the workspace (rmsnorm_workspace_bytes, 256-byte aligned, enough for
+// either path) holds the partial energies (and, for rows wider than one pass
+// takes, the row scales); rmsnorm_single_pass: whether rows of K channels at
+// stride ldx are normalised in one pass
+bool rmsnorm_single_pass(int64_t K, int64_t ldx);
 size_t rmsnorm_workspace_bytes(int64_t B, int64_t M, int64_t K);
 hipError_t launch_rmsnorm_kmajor(const uint16_t *X, const uint16_t *gamma, float eps, int64_t B,
                                  int64_t M, int64_t K, int64_t ldx, uint16_t *Xt, int64_t ldxt,

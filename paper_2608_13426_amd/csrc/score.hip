@@ -327,6 +327,41 @@ __global__ __launch_bounds__(64) void score_finalize_kernel(
     energy[t] = s;
 }
 
+// The same sum for many splits: 16 row groups of a column each add their
+// ceil(S / 16) consecutive splits in order (16 loads in flight per thread),
+// then the 16 group sums are added in group order.  64 columns per
+// workgroup of 1024 threads.
+constexpr int kFinGroups = 16;
+__global__ __launch_bounds__(64 * kFinGroups) void score_finalize_grouped_kernel(
+    const double *__restrict__ partials, int64_t S, int64_t K, double *__restrict__ energy) {
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * 64 + c, b = blockIdx.y;
+    const int64_t sg = (S + kFinGroups - 1) / kFinGroups;
+    const int64_t s0 = g * sg, s1 = min(S, s0 + sg);
+    double acc = 0.0;
+    if (j < K) {
+        const double *p = partials + b * S * K + j;
+        int64_t s = s0;
+        for (; s + 16 <= s1; s += 16) {
+            double v[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) v[i] = p[(s + i) * K];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc += v[i];
+        }
+        for (; s < s1; ++s) acc += p[s * K];
+    }
+    __shared__ double red[kFinGroups][64];
+    red[g][c] = acc;
+    __syncthreads();
+    if (g == 0 && j < K) {
+        double t = red[0][c];
+#pragma unroll
+        for (int q = 1; q < kFinGroups; ++q) t += red[q][c];
+        energy[b * K + j] = t;
+    }
+}
+
 template <bool XT>
 hipError_t launch_tiles(const uint16_t *X, int64_t B, int64_t M, int64_t K, int64_t ldx,
                         int64_t S, double *out, int64_t unit_stride, int64_t split_stride,
@@ -433,6 +468,14 @@ hipError_t launch_score_finalize(const double *partials, int64_t B, int64_t S, i
     const int64_t n = B * K;
     hipLaunchKernelGGL(score_finalize_kernel, dim3(static_cast<unsigned>((n + 63) / 64)), dim3(64), 0,
                        stream, partials, B, S, K, energy);
+    return hipGetLastError();
+}
+
+hipError_t launch_score_finalize_grouped(const double *partials, int64_t B, int64_t S, int64_t K,
+                                         double *energy, hipStream_t stream) {
+    const dim3 grid(static_cast<unsigned>((K + 63) / 64), static_cast<unsigned>(B));
+    hipLaunchKernelGGL(score_finalize_grouped_kernel, grid, dim3(64 * kFinGroups), 0, stream, partials,
+                       S, K, energy);
     return hipGetLastError();
 }
 
