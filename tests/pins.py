@@ -533,6 +533,40 @@ def check_softmax_row_stats(o):
             assert abs(rinv[i, j] * tot - 1.0) <= 1e-14
 
 
+def check_bound_values(o):
+    """The bound helpers on small integer cases whose values are worked out
+    by hand (not from the helpers' formulas), Sec. 3.5 / Appendix E.
+
+    Case 1: one discarded column, so the error is the rank-one term
+    A[:, 1] B[1, :] and both bounds are tight: ||(0, 4)|| * ||(0, 2)|| = 8.
+    eps_A = 16 / 25 (column 1 carries 16 of A's 25), eps_B = 4 / 31.
+
+    Case 2: columns 0 and 1 discarded, a0 = (1, 0), a1 = (0, 2) and rows
+    b0 = (1, 0), b1 = (0, 3): error ||a0 b0^T + a1 b1^T|| = ||diag(1, 6)|| =
+    sqrt(37); rank-one bound 1*1 + 2*3 = 7; factorized bound
+    sqrt(1 + 4) * sqrt(1 + 9) = sqrt(50); eps_A = 5 / 13, eps_B = 10 / 12."""
+    A1 = np.array([[3.0, 0.0, 0.0], [0.0, 4.0, 0.0]])
+    B1 = np.array([[1.0, 1.0], [0.0, 2.0], [5.0, 0.0]])
+    i1 = np.array([0, 2])
+    assert o.rank_one_bound(A1, B1, i1) == 8.0
+    assert o.factorized_bound(A1, B1, i1) == 8.0
+    assert abs(o.normalized_bound(A1, B1, i1) - math.sqrt(16 / 25 * 4 / 31)) <= 1e-15
+    Y1, e1 = o.reduced_matmul(A1, B1, i1), o.column_energies(A1)
+    assert float(np.linalg.norm(exact_matmul(A1, B1) - Y1)) == 8.0
+    assert o.residual_energy(e1, i1) == 16.0
+    assert o.retained_energy_fraction(e1, i1) == 9.0 / 25.0
+
+    A2 = np.array([[1.0, 0.0, 2.0], [0.0, 2.0, 2.0]])
+    B2 = np.array([[1.0, 0.0], [0.0, 3.0], [1.0, 1.0]])
+    i2 = np.array([2])
+    assert o.rank_one_bound(A2, B2, i2) == 7.0
+    assert abs(o.factorized_bound(A2, B2, i2) - math.sqrt(50.0)) <= 1e-14
+    assert abs(o.normalized_bound(A2, B2, i2) - math.sqrt(5 / 13 * 10 / 12)) <= 1e-15
+    Y2 = o.reduced_matmul(A2, B2, i2)
+    assert abs(float(np.linalg.norm(exact_matmul(A2, B2) - Y2)) - math.sqrt(37.0)) <= 1e-14
+    assert o.residual_energy(o.column_energies(A2), i2) == 5.0
+
+
 def check_margin(o):
     assert o.selection_margin(np.array([4.0, 2.0, 1.0]), 1) == 0.5
     assert o.selection_margin(np.array([4.0, 4.0, 1.0]), 1) == 0.0
@@ -543,4 +577,4 @@ def check_margin(o):
 ALL_CHECKS = (check_retained_count, check_energies, check_selection, check_product,
               check_bounds, check_worked_example, check_qk, check_attention, check_pv,
               check_swiglu, check_rmsnorm, check_attention_weights, check_softmax_row_stats,
-              check_margin)
+              check_bound_values, check_margin)

@@ -285,7 +285,29 @@ def _rs_over_first_axis(S):            # statistics over the first axis
 ro_attention_weights = ro.attention_weights
 ro_softmax_row_stats = ro.softmax_row_stats
 
+def _b1_kept(A, B, idx):
+    # sums over the kept indices instead of the discarded ones
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    return math.fsum(float(np.linalg.norm(A[:, j]) * np.linalg.norm(B[j, :]))
+                     for j in np.asarray(idx, dtype=np.int64))
+
+
+def _b2_whole_b(A, B, idx):
+    # the factorized bound with all of B's rows
+    A = np.asarray(A, dtype=np.float64)
+    comp = ro._complement(idx, A.shape[1])
+    return float(np.linalg.norm(A[:, comp]) * np.linalg.norm(np.asarray(B, dtype=np.float64)))
+
+
+def _bn_no_sqrt(A, B, idx):
+    return ro.discarded_energy_ratio(A, idx, 1) * ro.discarded_energy_ratio(B, idx, 0)
+
+
 MUTANTS = {
+    "bound_rank_one_kept": ("rank_one_bound", _b1_kept),
+    "bound_factorized_whole_b": ("factorized_bound", _b2_whole_b),
+    "bound_normalized_no_sqrt": ("normalized_bound", _bn_no_sqrt),
     "rmsnorm_sum_not_mean": ("rmsnorm", _rms_sum),
     "rmsnorm_eps_outside_sqrt": ("rmsnorm", _rms_eps_outside),
     "rmsnorm_gamma_on_rows": ("rmsnorm", _rms_gamma_rows),
