@@ -146,6 +146,9 @@ def parse():
                    help="skip the timing of the scores -> weights -> token-axis value product chain")
     p.add_argument("--no-pv", action="store_true",
                    help="skip the separate timing of the token-axis reduced value product")
+    p.add_argument("--no-paper-kernels", action="store_true",
+                   help="skip the paper's kernel-level benchmark (reduced QK^T and AV at "
+                        "L = 1024, 2048, 4096, rho = 0.8)")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="copy this many MiB device to device once before timing (a "
                         "counter-calibration probe for rocprofv3 runs; not timed)")
@@ -810,6 +813,99 @@ def time_decode(L, r, steps, warmup, B=1):
             "gemv_gbs": g_bytes / (g_us * 1e-6) / 1e9}
 
 
+# The paper's kernel-level latency table (Sec. 6, "GEMM kernel latency"):
+# LLaMA-3.1-8B attention, batch 1, rho = 0.8, each RMM operation timed with
+# its scoring and TopK; dense and RMM milliseconds on an A100 (context only).
+PAPER_A100_MS = {
+    ("qk", 1024): (0.120, 0.089), ("qk", 2048): (0.433, 0.336), ("qk", 4096): (1.675, 1.071),
+    ("av", 1024): (0.065, 0.039), ("av", 2048): (0.207, 0.114), ("av", 4096): (0.753, 0.399),
+}
+
+
+def time_paper_kernels(wk, dev, steps, warmup, rho=0.8, lengths=(1024, 2048, 4096)):
+    """The paper's kernel-level benchmark on this GPU: per sequence length L
+    (32 query / 8 kv heads, d = 128, causal, batch 1, the 8B layer's Q, K and
+    V recipe cut to L tokens), at retention rho and at 1:
+      qk       : rmm_score of Q per head -> rmm_select -> rmm_reduced_qk (S
+                 written, masked), against torch's dense bf16 Q @ K^T (K
+                 repeated over each kv head's query heads, transposed once
+                 outside the timed region);
+      av       : rmm_reduced_pv on the row-major weights P (column norms of P
+                 -> TopK -> gathered product), against torch's dense P @ V;
+      av_chain : from the scores S, rmm_attention_weights_kmajor (weights
+                 K-major with their token energies) -> rmm_select ->
+                 rmm_reduced_pv_kmajor, against torch softmax + P @ V.
+    S holds the full causal scores (the qk pipeline at r = 1) and P their
+    softmax (untimed).  Every call is bracketed by HIP events."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    import workloads as wl
+    a = wk.attention
+    H, Hkv, D, G = a.H, a.Hkv, a.D, a.H // a.Hkv
+    out = {}
+    for Ln in lengths:
+        qf, kf = wl.workload_qk(wk, Ln)
+        vf = wl.workload_v(wk, Ln)
+        bf = lambda x: torch.from_numpy(wl.f32_to_bf16_bits(x).view(np.int16)).to(dev).view(torch.bfloat16)
+        Q, Kc, V = bf(qf)[None], bf(kf)[None], bf(vf)[None]
+        S = torch.empty((1, H, Ln, Ln), dtype=torch.bfloat16, device=dev)
+        P = torch.empty_like(S)
+        O = torch.empty((1, H, Ln, D), dtype=torch.bfloat16, device=dev)
+        e = torch.empty(H * max(D, Ln), dtype=torch.float64, device=dev)
+        ws = torch.empty(max(rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, H, Ln, D, D), 1),
+                         dtype=torch.uint8, device=dev)
+        rec = {"L": Ln}
+        for r in (rho, 1.0):           # S ends as the full causal scores
+            k = rmm.rmm_retained_count(r, D)
+            idx = torch.empty(H * k, dtype=torch.int32, device=dev)
+
+            def qk():
+                rmm.rmm_score(Q.reshape(H, Ln, D), e[:H * D], ws)
+                rmm.rmm_select(e[:H * D], k, idx)
+                rmm.rmm_reduced_qk(Q, Kc, idx.view(1, H, k), S, causal=True)
+            rec[f"qk_rmm_us@{r}"] = time_calls(qk, steps, warmup)
+        Kt = Kc.repeat_interleave(G, dim=1).transpose(-1, -2).contiguous()
+        rec["qk_dense_torch_us"] = time_calls(lambda: torch.matmul(Q, Kt, out=P), steps, warmup)
+        del Kt
+        Vr = V.repeat_interleave(G, dim=1).contiguous()
+        Pt = torch.empty_like(S)
+        wsw = torch.empty(rmm.rmm_attention_weights_kmajor_workspace_size(1, H, Ln, Ln),
+                          dtype=torch.uint8, device=dev)
+        for r in (rho, 1.0):
+            kt = rmm.rmm_retained_count(r, Ln)
+            idt = torch.empty(H * kt, dtype=torch.int32, device=dev)
+
+            def chain():
+                rmm.rmm_attention_weights_kmajor(S, Pt, e[:H * Ln], causal=True, workspace=wsw)
+                rmm.rmm_select(e[:H * Ln], kt, idt)
+                rmm.rmm_reduced_pv_kmajor(Pt, V, idt.view(H, kt), O, causal=True)
+            rec[f"av_chain_rmm_us@{r}"] = time_calls(chain, steps, warmup)
+
+        def dense_chain():
+            torch.softmax(S[0], dim=-1, out=P[0])
+            torch.matmul(P, Vr, out=O)
+        rec["av_chain_dense_torch_us"] = time_calls(dense_chain, steps, warmup)
+        del Pt, wsw
+        # P = the softmax weights, row-major (left by the dense chain)
+        wpv = torch.empty(max(rmm.rmm_workspace_size(rmm.RMM_OP_PV, H, Ln, Ln, Ln), 1),
+                          dtype=torch.uint8, device=dev)
+        for r in (rho, 1.0):
+            kt = rmm.rmm_retained_count(r, Ln)
+            rec[f"av_rmm_us@{r}"] = time_calls(lambda: rmm.rmm_reduced_pv(P, V, kt, O, workspace=wpv),
+                                               steps, warmup)
+        rec["av_dense_torch_us"] = time_calls(lambda: torch.matmul(P, Vr, out=O), steps, warmup)
+        for op in ("qk", "av", "av_chain"):
+            rec[f"{op}_speedup_vs_dense_torch"] = rec[f"{op}_dense_torch_us"] / rec[f"{op}_rmm_us@{rho}"]
+            rec[f"{op}_speedup_vs_r1"] = rec[f"{op}_rmm_us@1.0"] / rec[f"{op}_rmm_us@{rho}"]
+        for op in ("qk", "av"):
+            d_ms, r_ms = PAPER_A100_MS[(op, Ln)]
+            rec[f"{op}_paper_a100_ms"] = {"dense": d_ms, "rmm": r_ms, "speedup": round(d_ms / r_ms, 2)}
+        out[Ln] = {kk: (round(v, 3) if isinstance(v, float) else v) for kk, v in rec.items()}
+        del Q, Kc, V, S, P, O, Vr, wpv
+        torch.cuda.empty_cache()
+    return out
+
+
 # ---------------------------------------------------------- CPU baseline
 
 def cpu_baseline(wk, tokens, r):
@@ -1169,6 +1265,28 @@ def main():
                          "achieved": round(p_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(p_ach / PEAK_HBM_GBS, 4), "traffic": None,
                          "bytes_basis": "one read of P + kept V rows + O per call"},
+        }
+    if not args.no_paper_kernels:
+        pk = time_paper_kernels(wk, L.dev, args.steps, args.warmup)
+        for Ln, rec in pk.items():
+            print(f"# paper kernels L={Ln}: QK^T rmm {rec['qk_rmm_us@0.8']:.1f} us (r=1 "
+                  f"{rec['qk_rmm_us@1.0']:.1f}, dense torch {rec['qk_dense_torch_us']:.1f}); "
+                  f"AV rmm {rec['av_rmm_us@0.8']:.1f} us (r=1 {rec['av_rmm_us@1.0']:.1f}, dense "
+                  f"torch {rec['av_dense_torch_us']:.1f}); AV from S rmm {rec['av_chain_rmm_us@0.8']:.1f} "
+                  f"us (r=1 {rec['av_chain_rmm_us@1.0']:.1f}, dense torch softmax + P@V "
+                  f"{rec['av_chain_dense_torch_us']:.1f})", file=sys.stderr, flush=True)
+        out["paper_kernels"] = {
+            "op": "the paper's kernel-level latency benchmark (Sec. 6): per sequence length, "
+                  "reduced QK^T (per-head scoring + TopK + rmm_reduced_qk writing the masked S) "
+                  "and reduced AV (rmm_reduced_pv on row-major P: column norms + TopK + gathered "
+                  "product; av_chain: from the scores, the weights written K-major with their "
+                  "token energies + TopK + product) at rho = 0.8 and 1, against torch's dense bf16 "
+                  "products (av_chain: torch softmax + P @ V); "
+                  f"{wk.attention.H} q / {wk.attention.Hkv} kv heads, d={wk.attention.D}, causal, "
+                  "batch 1; paper_a100_ms: the paper's own dense and RMM times on an A100 "
+                  "(context, other hardware)",
+            "rho": 0.8,
+            "per_length": {str(Ln): rec for Ln, rec in pk.items()},
         }
     if not args.no_cpu_baseline:
         tokens = args.cpu_tokens or wk.M
