@@ -643,6 +643,24 @@ size_t rmm_decode_step_workspace_size(const rmm_decode_group_t *groups, int ngro
 rmm_status_t rmm_decode_step(const rmm_decode_group_t *groups, int ngroups, int64_t B,
                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The reduced products of a decode step over caller-made sets, several at
+ * once   (Sec. 3.2 reduced product; the boundary accepts any ascending list,
+ * e.g. sets computed for an earlier token or by another call).
+ *
+ * For each group g and sequence b: Y_g[b][n] = sum over t of
+ * X_g[b][idx_g[b][t]] * W_g[idx_g[b][t]][n], exactly what rmm_reduced_gemv
+ * (M = 1) computes, in two launches for all groups together (the products,
+ * then the fixed-order reduction of split lists): rmm_decode_step without
+ * its selection.  idx_g is read, not written: int32 [B][k], each list
+ * strictly ascending within [0, K) (not checked on the device; an index
+ * outside it reads outside W).
+ *
+ * groups, workspace, errors: as rmm_decode_step (the same workspace size).
+ */
+rmm_status_t rmm_decode_products(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);
 

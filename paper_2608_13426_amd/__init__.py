@@ -24,7 +24,7 @@ __all__ = [
     "rmm_linear_noalloc", "rmm_noalloc_scratch_bytes", "rmm_rmsnorm_kmajor",
     "rmm_rmsnorm_kmajor_workspace_size", "rmm_attention_weights_kmajor",
     "rmm_attention_weights_kmajor_workspace_size", "rmm_reduced_pv_kmajor", "rmm_decode_step",
-    "rmm_decode_step_workspace_size", "DecodeGroup", "rmm_reduced_qk_rowstats",
+    "rmm_decode_step_workspace_size", "rmm_decode_products", "DecodeGroup", "rmm_reduced_qk_rowstats",
     "rmm_attention_weights_kmajor_rowstats", "EXPORTED_SYMBOLS",
 ]
 
@@ -71,6 +71,8 @@ _SIGS = {
     "rmm_decode_step_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(DecodeGroup), ctypes.c_int,
                                                          _i64]),
     "rmm_decode_step": (ctypes.c_int, [ctypes.POINTER(DecodeGroup), ctypes.c_int, _i64, _p,
+                                       ctypes.c_size_t, _p]),
+    "rmm_decode_products": (ctypes.c_int, [ctypes.POINTER(DecodeGroup), ctypes.c_int, _i64, _p,
                                        ctypes.c_size_t, _p]),
     "rmm_reduced_pv_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
                                              _i64, ctypes.c_int, _p, _p]),
@@ -785,6 +787,20 @@ def _decode_groups(groups):
 def rmm_decode_step_workspace_size(groups) -> int:
     arr, B = _decode_groups(groups)
     return int(lib.rmm_decode_step_workspace_size(arr, len(groups), B))
+
+
+def rmm_decode_products(groups, workspace: torch.Tensor | None = None, stream=None):
+    """For each group (X [B, K], W [K, N], k, idx [B*k], Y [B, N]) with idx
+    holding caller-made ascending sets: Y = the reduced product; all groups
+    in two launches (rmm_decode_step without its selection)."""
+    arr, B = _decode_groups(groups)
+    d = groups[0][0].device
+    need = int(lib.rmm_decode_step_workspace_size(arr, len(groups), B))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=d)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("rmm_decode_products", lib.rmm_decode_products(arr, len(groups), B, _ptr(workspace),
+                                                          ws_bytes, _stream(d, stream)))
 
 
 def rmm_decode_step(groups, workspace: torch.Tensor | None = None, stream=None):

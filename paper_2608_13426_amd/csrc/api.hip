@@ -606,6 +606,20 @@ rmm_status_t rmm_decode_step(const rmm_decode_group_t *groups, int ngroups, int6
     return from_hip(rmm::launch_gemv_grouped_bf16(G, B, stream));
 }
 
+rmm_status_t rmm_decode_products(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                                 void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    rmm_status_t st = check_decode_groups(groups, ngroups, B);
+    if (st != RMM_OK) return st;
+    rmm::GemvGroups G;
+    const size_t need = decode_groups(groups, ngroups, B, nullptr, &G);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+        if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
+    }
+    decode_groups(groups, ngroups, B, workspace, &G);
+    return from_hip(rmm::launch_gemv_grouped_bf16(G, B, stream));
+}
+
 const char *rmm_status_string(rmm_status_t status) {
     switch (status) {
     case RMM_OK: return "success";

@@ -519,9 +519,12 @@ def test_reduced_pv_kmajor_validation():
     assert call(10, 68) == UNSUPPORTED        # ldpt % 8
 
 
-def test_decode_step_validation():
+@pytest.mark.parametrize("entry", ["rmm_decode_step", "rmm_decode_products"])
+def test_decode_step_validation(entry):
+    """Both grouped decode entry points validate the same way (the products
+    alone take the same groups and workspace)."""
     G = rmm.DecodeGroup
-    f = rmm.lib.rmm_decode_step
+    f = getattr(rmm.lib, entry)
 
     def arr(**kw):
         d = dict(X=0x100000, W=0x100000, idx=0x100000, Y=0x100000, K=4096, N=1024, k=2048,

@@ -245,9 +245,13 @@ def _decode_case(dev, groups_np, B, r):
         rmm.rmm_reduced_gemv(Xd.view(B, 1, K), Wd, i2.view(B, k), Y2.view(B, 1, N))
         sep.append((i2, Y2))
     rmm.rmm_decode_step(groups)
-    for (Xd, Wd, k, idx, Y), (i2, Y2), (Xb, Wb) in zip(groups, sep, groups_np):
+    # the products alone over the step's sets, into fresh outputs
+    prod = [(Xd, Wd, k, idx, torch.full_like(Y, 7.0)) for Xd, Wd, k, idx, Y in groups]
+    rmm.rmm_decode_products(prod)
+    for (Xd, Wd, k, idx, Y), (i2, Y2), (Xb, Wb), p in zip(groups, sep, groups_np, prod):
         assert torch.equal(idx, i2), "sets differ from rmm_select_tokens"
         assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16)), "products differ from rmm_reduced_gemv"
+        assert torch.equal(p[4].view(torch.int16), Y.view(torch.int16)), "rmm_decode_products differs"
         X = wl.decode(Xb, "bf16").astype(np.float64)
         W = wl.decode(Wb, "bf16").astype(np.float64)
         e_ref = X * X                                   # one row: the exact energies

@@ -96,6 +96,7 @@ def _run(dev, Xbits, gbits, eps, pad=0, rows=None, project=None):
     (1, 130, 520, 10.0, 0, 4),       # K not a multiple of 64 (partial column strip); a large eps
     (4, 2000, 1024, 1e-5, 0, 5),     # four units, several row splits each
     (1, 9000, 256, 1e-5, 0, 6),      # many row splits of a narrow input
+    (2, 512, 3072, 1e-5, 0, 7),      # 16 row blocks per unit (paired blocks), 3 column tiles per wave
 ])
 def test_rmsnorm_kmajor(B, M, K, eps, pad, seed):
     dev = require_gpu()
