@@ -149,6 +149,9 @@ def parse():
     p.add_argument("--no-paper-kernels", action="store_true",
                    help="skip the paper's kernel-level benchmark (reduced QK^T and AV at "
                         "L = 1024, 2048, 4096, rho = 0.8)")
+    p.add_argument("--no-layer-forward", action="store_true",
+                   help="skip the prefill pass of the whole layer (RMM producers and "
+                        "products against torch's dense layer)")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="copy this many MiB device to device once before timing (a "
                         "counter-calibration probe for rocprofv3 runs; not timed)")
@@ -814,6 +817,129 @@ def time_decode(L, r, steps, warmup, B=1):
             "gemv_gbs": g_bytes / (g_us * 1e-6) / 1e9}
 
 
+def time_layer_forward(L, steps, warmup, ratios=(0.5, 0.8, 1.0), eps=1e-5):
+    """One prefill pass of the whole decoder layer (batch 1, the layer's
+    attention input standing in for its hidden state x; rotary position
+    embedding left out on both sides), every product reduced at ratio r and
+    every reduced input produced K-major with its energies by its producer:
+      h1 = x + o-proj(attention(q|k|v-proj(rmsnorm(x))))
+      h2 = h1 + down(swiglu(gate|up(rmsnorm(h1))))
+    as rmm_rmsnorm_kmajor -> TopK -> q|k|v GEMM -> heads laid out (torch
+    copies) -> per-head scoring + TopK -> rmm_reduced_attention_kmajor -> TopK
+    -> o GEMM -> residual (torch) -> rmm_rmsnorm_kmajor -> TopK ->
+    rmm_reduced_gemm_swiglu_kmajor -> TopK -> down GEMM -> residual (torch);
+    against torch's dense layer (RMSNorm in fp32, x @ W products, SDPA with
+    its fused flash or memory-efficient kernels only, silu(g) * u).  Every
+    pass is bracketed by HIP events.  rel_diff_vs_torch: ||h2 - h2_torch|| /
+    ||h2_torch|| for the pass at that ratio (at r = 1 only rounding differs)."""
+    import torch
+    import torch.nn.functional as F_
+    import paper_2608_13426_amd as rmm
+    import workloads as wl
+    wk, M, dev = L.wk, L.M, L.dev
+    a = wk.attention
+    HD, KVD = a.H * a.D, a.Hkv * a.D
+    Dm = wk.inputs["attn_in"][0]
+    Fh = wk.inputs["down_in"][0]
+    bf = lambda t: t.to(torch.bfloat16)
+    gam = [bf(torch.from_numpy(1.0 + 0.3 * wl.normal_blocks((wk.seed, 77 + i), (1, Dm))[0]).to(dev))
+           for i in range(2)]
+    x = L.X["attn_in"]
+    Wqkv, Wo, Wd = L.Wcat["attn_in"], L.Wcat["o_in"], L.Wcat["down_in"]
+    Wgu_cat = L.Wcat["mlp_in"]
+    Wgu = rmm.swiglu_weight_layout(L.W["gate"], L.W["up"])
+    # RMM path buffers
+    Xt_a = torch.empty((Dm, M), dtype=torch.bfloat16, device=dev)
+    Xt_m = torch.empty_like(Xt_a)
+    e_n = torch.empty(Dm, dtype=torch.float64, device=dev)
+    ws_n = torch.empty(rmm.rmm_rmsnorm_kmajor_workspace_size(1, M, Dm), dtype=torch.uint8, device=dev)
+    Yqkv = torch.empty((M, Wqkv.shape[1]), dtype=torch.bfloat16, device=dev)
+    Q = torch.empty((1, a.H, M, a.D), dtype=torch.bfloat16, device=dev)
+    Kh = torch.empty((1, a.Hkv, M, a.D), dtype=torch.bfloat16, device=dev)
+    Vh = torch.empty_like(Kh)
+    e_q = torch.empty(a.H * a.D, dtype=torch.float64, device=dev)
+    ws_q = torch.empty(max(rmm.rmm_workspace_size(rmm.RMM_OP_SCORE, a.H, M, a.D), 1), dtype=torch.uint8,
+                       device=dev)
+    Ot = torch.empty((HD, M), dtype=torch.bfloat16, device=dev)
+    e_o = torch.empty(HD, dtype=torch.float64, device=dev)
+    Yo = torch.empty((M, Wo.shape[1]), dtype=torch.bfloat16, device=dev)
+    h1 = torch.empty_like(x)
+    Ht = torch.empty((Fh, M), dtype=torch.bfloat16, device=dev)
+    e_h = torch.empty(Fh, dtype=torch.float64, device=dev)
+    ws_s = torch.empty(rmm.rmm_gemm_swiglu_workspace_size(1, M, Fh), dtype=torch.uint8, device=dev)
+    Yd = torch.empty((M, Wd.shape[1]), dtype=torch.bfloat16, device=dev)
+    h2 = torch.empty_like(x)
+    rec = {}
+    outs = {}
+    for r in ratios:
+        k_in = rmm.rmm_retained_count(r, Dm)
+        k_q = rmm.rmm_retained_count(r, a.D)
+        k_o = rmm.rmm_retained_count(r, HD)
+        k_d = rmm.rmm_retained_count(r, Fh)
+        i_a = torch.empty(k_in, dtype=torch.int32, device=dev)
+        i_m = torch.empty_like(i_a)
+        i_q = torch.empty(a.H * k_q, dtype=torch.int32, device=dev)
+        i_o = torch.empty(k_o, dtype=torch.int32, device=dev)
+        i_d = torch.empty(k_d, dtype=torch.int32, device=dev)
+        ws_k = torch.empty(rmm.rmm_attention_kmajor_workspace_size(1, a.H, M, M, a.D, k_q),
+                           dtype=torch.uint8, device=dev)
+
+        def layer():
+            rmm.rmm_rmsnorm_kmajor(x, gam[0], eps, Xt_a, e_n, ws_n)
+            rmm.rmm_select(e_n, k_in, i_a)
+            rmm.rmm_reduced_gemm_kmajor(Xt_a, Wqkv, i_a.view(1, k_in), Yqkv)
+            Q[0].copy_(Yqkv[:, :HD].view(M, a.H, a.D).transpose(0, 1))
+            Kh[0].copy_(Yqkv[:, HD:HD + KVD].view(M, a.Hkv, a.D).transpose(0, 1))
+            Vh[0].copy_(Yqkv[:, HD + KVD:].view(M, a.Hkv, a.D).transpose(0, 1))
+            rmm.rmm_score(Q.reshape(a.H, M, a.D), e_q, ws_q)
+            rmm.rmm_select(e_q, k_q, i_q)
+            rmm.rmm_reduced_attention_kmajor(Q, Kh, Vh, i_q.view(1, a.H, k_q), Ot, e_o, causal=True,
+                                             workspace=ws_k)
+            rmm.rmm_select(e_o, k_o, i_o)
+            rmm.rmm_reduced_gemm_kmajor(Ot, Wo, i_o.view(1, k_o), Yo)
+            torch.add(x, Yo, out=h1)
+            rmm.rmm_rmsnorm_kmajor(h1, gam[1], eps, Xt_m, e_n, ws_n)
+            rmm.rmm_select(e_n, k_in, i_m)
+            rmm.rmm_reduced_gemm_swiglu_kmajor(Xt_m, Wgu, i_m.view(1, k_in), Ht, e_h, workspace=ws_s)
+            rmm.rmm_select(e_h, k_d, i_d)
+            rmm.rmm_reduced_gemm_kmajor(Ht, Wd, i_d.view(1, k_d), Yd)
+            torch.add(h1, Yd, out=h2)
+        rec[f"rmm_ms@{r}"] = time_calls(layer, steps, warmup) / 1e3
+        layer()
+        outs[r] = h2.float().clone()
+        del ws_k
+
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    def rmsnorm(t, g):
+        tf = t.float()
+        return bf(bf(tf * torch.rsqrt(tf.pow(2).mean(-1, keepdim=True) + eps)).float() * g.float())
+
+    def dense():
+        qkv = rmsnorm(x, gam[0]) @ Wqkv
+        q = qkv[:, :HD].view(M, a.H, a.D).transpose(0, 1)[None]
+        kk = qkv[:, HD:HD + KVD].view(M, a.Hkv, a.D).transpose(0, 1)[None]
+        vv = qkv[:, HD + KVD:].view(M, a.Hkv, a.D).transpose(0, 1)[None]
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+            att = F_.scaled_dot_product_attention(q, kk, vv, is_causal=True, enable_gqa=True)
+        d1 = x + att[0].transpose(0, 1).reshape(M, HD) @ Wo
+        gu = rmsnorm(d1, gam[1]) @ Wgu_cat
+        hh = F_.silu(gu[:, :Fh]) * gu[:, Fh:]
+        return d1 + hh @ Wd
+    try:
+        rec["torch_dense_ms"] = time_calls(dense, steps, warmup) / 1e3
+        ref = dense().float()
+        for r in ratios:
+            rec[f"rel_diff_vs_torch@{r}"] = float((outs[r] - ref).norm() / ref.norm())
+            rec[f"speedup_vs_torch@{r}"] = rec["torch_dense_ms"] / rec[f"rmm_ms@{r}"]
+    except RuntimeError as err:              # no fused SDPA kernel for these inputs
+        rec["torch_dense_ms"] = None
+        rec["torch_dense_error"] = str(err)[:200]
+    for r in ratios:
+        rec[f"speedup_vs_r1@{r}"] = rec["rmm_ms@1.0"] / rec[f"rmm_ms@{r}"] if "rmm_ms@1.0" in rec else None
+    return {kk: (round(v, 4) if isinstance(v, float) else v) for kk, v in rec.items()}
+
+
 # The paper's kernel-level latency table (Sec. 6, "GEMM kernel latency"):
 # LLaMA-3.1-8B attention, batch 1, rho = 0.8, each RMM operation timed with
 # its scoring and TopK; dense and RMM milliseconds on an A100 (context only).
@@ -1266,6 +1392,20 @@ def main():
                          "achieved": round(p_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(p_ach / PEAK_HBM_GBS, 4), "traffic": None,
                          "bytes_basis": "one read of P + kept V rows + O per call"},
+        }
+    if not args.no_layer_forward:
+        lf = time_layer_forward(L, args.steps, args.warmup)
+        print(f"# layer forward: rmm " + ", ".join(f"r={r} {lf[f'rmm_ms@{r}']:.3f} ms"
+                                                   for r in (0.5, 0.8, 1.0))
+              + f"; torch dense {lf.get('torch_dense_ms')} ms", file=sys.stderr, flush=True)
+        out["layer_forward"] = {
+            "op": "one prefill pass of the whole decoder layer (batch 1, seq "
+                  f"{wk.M}, no rotary embedding): RMSNorm producers, reduced q|k|v, per-head "
+                  "reduced attention writing the o-projection's K-major input, reduced o, "
+                  "residual, RMSNorm producer, reduced gate|up with the SwiGLU producer, reduced "
+                  "down, residual; every product at ratio r; against torch's dense layer "
+                  "(fp32 RMSNorm, x @ W, fused SDPA, silu(g) * u)",
+            "per_ratio": lf,
         }
     if not args.no_paper_kernels:
         pk = time_paper_kernels(wk, L.dev, args.steps, args.warmup)
