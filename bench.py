@@ -347,6 +347,23 @@ def time_attention(L, r, steps, warmup):
             "retained_tflops": flop / (ms * 1e-3) / 1e12, "calls": steps}
 
 
+def time_sdpa(L, steps, warmup):
+    """torch's fused causal attention (SDPA limited to its flash and
+    memory-efficient kernels, GQA) on the layer's Q, K and V, for context;
+    None when neither kernel takes these inputs."""
+    import torch
+    import torch.nn.functional as F_
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    def call():
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+            return F_.scaled_dot_product_attention(L.Q, L.Kc, L.V, is_causal=True, enable_gqa=True)
+    try:
+        return time_calls(call, steps, warmup)
+    except RuntimeError:
+        return None
+
+
 def time_calls(fn, steps, warmup):
     """Average microseconds of `fn` (launches on the current stream): `warmup`
     untimed calls, then `steps` calls each bracketed by HIP events."""
@@ -1184,6 +1201,8 @@ def main():
         }
     if not args.no_fused_attention:
         att = {r: time_attention(L, r, args.steps, args.warmup) for r in sorted(sweep)}
+        sdpa_us = time_sdpa(L, args.steps, args.warmup)
+        print(f"# torch SDPA (dense, causal): {sdpa_us} us/call", file=sys.stderr, flush=True)
         for r, rec in att.items():
             print(f"# fused attention r={r}: {rec['avg_call_us']:.1f} us/call, "
                   f"{rec['retained_tflops']:.1f} TFLOP/s", file=sys.stderr, flush=True)
@@ -1200,6 +1219,7 @@ def main():
                                    for k, v in rec.items()} for r, rec in att.items()},
             "speedup_vs_r1": round(a_1["avg_call_us"] / a_h["avg_call_us"], 3) if a_1 else None,
             "speedup_bound": round(2.0 / (1.0 + HEADLINE_R), 3),
+            "torch_sdpa_us": (round(sdpa_us, 1) if sdpa_us else None),
             "roofline": {"bound": "mfma", "kernel": "attn_fwd_kernel (+ attn_compact_k_kernel)",
                          "achieved": round(a_ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(a_ach / PEAK_BF16_TFLOPS, 4),
