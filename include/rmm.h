@@ -615,20 +615,21 @@ rmm_status_t rmm_reduced_pv_kmajor(const void *Pt, const void *V, const int32_t 
  *              lower index, NaN above +inf above every finite value)
  *   Y_g[b][n] = sum over t of X_g[b][idx_g[b][t]] * W_g[idx_g[b][t]][n]
  * in three launches for all groups together (selection, products, the
- * fixed-order reduction of split lists) instead of three per group.  The
+ * fixed-order reduction of split lists) instead of three per group (a group
+ * of more than 32768 channels takes one more selection launch of its own).  The
  * groups must be independent of each other (no group reads another's Y);
  * within a model's layer step those are products whose inputs are ready
  * together.
  *
  * groups   : host array of ngroups (1..8) descriptions; per group X bf16
- *            [B][ldx] (16-byte aligned, ldx % 8 == 0, ldx >= K, K <= 16384),
+ *            [B][ldx] (16-byte aligned, ldx % 8 == 0, ldx >= K),
  *            W bf16 [K][ldw] (16-byte aligned, ldw % 8 == 0, ldw >= N),
  *            idx int32 [B][k] written, Y bf16 [B][ldy] written, 1 <= k <= K.
  * workspace: rmm_decode_step_workspace_size(groups, ngroups, B) bytes,
  *            256-byte aligned, or NULL when that is 0 (fp32 partial sums).
  * Errors   : INVALID_ARGUMENT for null pointers, sizes < 1, k outside
  *            [1, K], ld too small, a misaligned workspace; UNSUPPORTED for
- *            more than 8 groups, B > 65535, K > 16384, misaligned X or W,
+ *            more than 8 groups, B > 65535, misaligned X or W,
  *            ldx or ldw not multiples of 8, K*ldw*2 >= 2^31;
  *            WORKSPACE_TOO_SMALL.
  */

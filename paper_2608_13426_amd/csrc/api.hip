@@ -577,7 +577,7 @@ static rmm_status_t check_decode_groups(const rmm_decode_group_t *groups, int n,
         if (d.K < 1 || d.N < 1 || d.k < 1 || d.k > d.K) return RMM_ERR_INVALID_ARGUMENT;
         if (d.ldx < d.K || d.ldw < d.N || d.ldy < d.N) return RMM_ERR_INVALID_ARGUMENT;
         if (d.N > kInt32Max) return RMM_ERR_INVALID_ARGUMENT;
-        if (d.K > 16384 || !aligned16(d.X) || d.ldx % 8 || !aligned16(d.W) || d.ldw % 8)
+        if (!aligned16(d.X) || d.ldx % 8 || !aligned16(d.W) || d.ldw % 8)
             return RMM_ERR_UNSUPPORTED;
         if (d.K * d.ldw * 2 >= (int64_t(1) << 31)) return RMM_ERR_UNSUPPORTED;
     }

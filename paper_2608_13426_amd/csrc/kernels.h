@@ -133,8 +133,10 @@ struct GemvGroups {
     GemvGroup g[kMaxGemvGroups];
     int n;
 };
-// TopK of x^2 for every unit of every group (bf16 tokens, K <= 16384, 16-byte
-// aligned rows; checked by the caller)
+// TopK of x^2 for every unit of every group (bf16 tokens, 16-byte aligned
+// rows; checked by the caller): one launch for the groups of up to
+// kToken16MaxK channels, one launch of the generic selection per wider group
+constexpr int64_t kToken16MaxK = 32 * 1024;
 hipError_t launch_select_tokens_grouped(const GemvGroups &G, int64_t B, hipStream_t stream);
 // the groups' reduced products (one launch) and slice reductions (one launch)
 hipError_t launch_gemv_grouped_bf16(GemvGroups G, int64_t B, hipStream_t stream);

@@ -231,7 +231,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src
     }
 }
 
-// One bf16 token per workgroup (a decode step), K <= 16 * 1024: the keys are
+// One bf16 token per workgroup (a decode step), K <= 32 * 1024 (at most
+// 32768 keys, so both 16-bit halves of the packed scan below hold): the keys are
 // the 15 magnitude bits, so the k-th largest key is found in at most two
 // histogram passes (bits 14..7, then 6..0), each of the NT threads owning C
 // consecutive keys loaded as 16-byte vectors.  The kept set is then
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const void *__restrict__ src
 template <int NT, int C>
 __device__ __forceinline__ void select_token16(const uint16_t *__restrict__ x, int K, int k,
                                                int32_t *__restrict__ out) {
-    static_assert(C % 8 == 0 && C <= 16 && NT >= 256 && NT <= 1024, "chunk");
+    static_assert(C % 8 == 0 && C <= 32 && NT >= 256 && NT <= 1024, "chunk");
     // The keys of a token bunch up in a few digits (one per binary exponent),
     // so one histogram would take most of a wave's 64 increments on one
     // word.  Lanes count into HR copies (lane % HR), HR + 1 words apart so
@@ -363,8 +364,11 @@ __global__ __launch_bounds__(NT) void select_token16_kernel(const uint16_t *__re
 // takes unit b of group g
 __global__ __launch_bounds__(1024) void select_token16_grouped_kernel(GemvGroups G) {
     const GemvGroup &q = G.g[blockIdx.y];
-    select_token16<1024, 16>(q.X + static_cast<int64_t>(blockIdx.x) * q.ldx, q.K, q.k,
-                             q.idx_out + static_cast<int64_t>(blockIdx.x) * q.k);
+    if (q.K > kToken16MaxK) return;              // selected by a launch of its own
+    const uint16_t *x = q.X + static_cast<int64_t>(blockIdx.x) * q.ldx;
+    int32_t *out = q.idx_out + static_cast<int64_t>(blockIdx.x) * q.k;
+    if (q.K <= 16 * 1024) select_token16<1024, 16>(x, q.K, q.k, out);   // uniform per workgroup
+    else select_token16<1024, 32>(x, q.K, q.k, out);
 }
 
 template <int NT, int C>
@@ -437,16 +441,24 @@ hipError_t launch_select(const double *energy, int64_t B, int64_t K, int64_t k,
 hipError_t launch_select_tokens_grouped(const GemvGroups &G, int64_t B, hipStream_t stream) {
     hipLaunchKernelGGL(select_token16_grouped_kernel, dim3(static_cast<unsigned>(B), static_cast<unsigned>(G.n)),
                        dim3(1024), 0, stream, G);
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    // groups too wide for the one-pass token kernel: the generic selection
+    for (int i = 0; i < G.n && e == hipSuccess; ++i) {
+        const GemvGroup &q = G.g[i];
+        if (q.K > kToken16MaxK)
+            e = launch_select_tokens(q.X, true, B, q.K, q.ldx, q.k, q.idx_out, stream);
+    }
+    return e;
 }
 
 hipError_t launch_select_tokens(const void *X, bool bf16, int64_t B, int64_t K, int64_t ldx,
                                 int64_t k, int32_t *idx, hipStream_t stream) {
-    if (bf16 && K <= 16 * 1024 && reinterpret_cast<uintptr_t>(X) % 16 == 0 && ldx % 8 == 0) {
+    if (bf16 && K <= kToken16MaxK && reinterpret_cast<uintptr_t>(X) % 16 == 0 && ldx % 8 == 0) {
         if (K <= 8 * 256) return launch_token16<256, 8>(X, ldx, B, K, k, idx, stream);
         if (K <= 16 * 256) return launch_token16<256, 16>(X, ldx, B, K, k, idx, stream);
         if (K <= 16 * 512) return launch_token16<512, 16>(X, ldx, B, K, k, idx, stream);
-        return launch_token16<1024, 16>(X, ldx, B, K, k, idx, stream);
+        if (K <= 16 * 1024) return launch_token16<1024, 16>(X, ldx, B, K, k, idx, stream);
+        return launch_token16<1024, 32>(X, ldx, B, K, k, idx, stream);
     }
     return bf16 ? launch_src<kTokenBf16>(X, ldx, B, K, k, idx, stream)
                 : launch_src<kTokenF32>(X, ldx, B, K, k, idx, stream);

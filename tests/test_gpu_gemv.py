@@ -159,6 +159,8 @@ def _tokens_case(seed, dtype, B, K, special=False, integers=False):
     ("f32", 3, 777, 0.5, True, False, 8),
     ("bf16", 1, 1, 1.0, False, False, 9),
     ("bf16", 5, 64, 0.001, False, False, 10),     # k = 1
+    ("bf16", 2, 32768, 0.5, False, True, 11),     # 32 keys per thread, many exact ties
+    ("bf16", 2, 20000, 0.3, True, False, 12),     # 32 keys per thread, NaN, +-inf, +-0
 ])
 def test_select_tokens(dtype, B, K, r, special, integers, seed):
     """Equals the oracle's TopK of x^2 and, bit for bit, rmm_score +
@@ -268,7 +270,9 @@ def _decode_case(dev, groups_np, B, r):
 def test_decode_step_groups(B, r, seed):
     """Ragged groups (K, N not multiples of the chunk; a single-slice group)."""
     dev = require_gpu()
-    shapes = [(1000, 1536), (4096, 520), (264, 72), (2048, 3000)]
+    # one group wider than 16384 channels (two chunks of 16 keys per thread),
+    # one wider than 32768 (a selection launch of its own)
+    shapes = [(1000, 1536), (4096, 520), (264, 72), (2048, 3000), (20000, 136), (33000, 72)]
     groups = [(wl.random_case(seed + 10 * i, (B, K), "bf16", n_outlier=max(1, K // 100)),
                wl.random_case(seed + 10 * i + 1, (K, N), "bf16", std=0.02)) for i, (K, N) in enumerate(shapes)]
     _decode_case(dev, groups, B, r)
