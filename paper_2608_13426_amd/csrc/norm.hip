@@ -19,9 +19,9 @@
 // registers, writes the block's K-major columns as 64-byte pieces (32
 // tokens) and one float64 partial energy per (block, column), which a
 // second kernel adds over the blocks in a fixed order (16 runs of
-// consecutive blocks, each in order, then the runs in order).  The two blocks that
-// share each 128-byte line of an Xt row run on the same XCD, so its L2 joins
-// the halves.
+// consecutive blocks, each in order, then the runs in order).  The two
+// blocks that share each 128-byte line of an Xt row run on the same XCD, so
+// its L2 joins the halves.
 //
 // Wider rows: two launches.  rms_rowscale_kernel: one wave per row reads
 // the row once (16-byte loads, fp32 sums of the exact squares in a fixed
@@ -260,11 +260,15 @@ hipError_t launch_rmsnorm_kmajor(const uint16_t *X, const uint16_t *gamma, float
         const int tpw = (tiles + kBlkWaves - 1) / kBlkWaves;
         const dim3 grid(static_cast<unsigned>(nblk), static_cast<unsigned>(B));
         const int Ki = static_cast<int>(K);
-        switch (tpw) {
-        case 1: hipLaunchKernelGGL(rms_block_kmajor_kernel<1>, grid, dim3(kBlkThreads), 0, stream, X, M, Ki, ldx, eps, gamma, Xt, ldxt, out); break;
-        case 2: hipLaunchKernelGGL(rms_block_kmajor_kernel<2>, grid, dim3(kBlkThreads), 0, stream, X, M, Ki, ldx, eps, gamma, Xt, ldxt, out); break;
-        case 3: hipLaunchKernelGGL(rms_block_kmajor_kernel<3>, grid, dim3(kBlkThreads), 0, stream, X, M, Ki, ldx, eps, gamma, Xt, ldxt, out); break;
-        default: hipLaunchKernelGGL(rms_block_kmajor_kernel<4>, grid, dim3(kBlkThreads), 0, stream, X, M, Ki, ldx, eps, gamma, Xt, ldxt, out); break;
+        auto launch = [&](auto kernel) {
+            hipLaunchKernelGGL(kernel, grid, dim3(kBlkThreads), 0, stream, X, M, Ki, ldx, eps, gamma,
+                               Xt, ldxt, out);
+        };
+        switch (tpw) {          // column tiles per wave
+        case 1: launch(rms_block_kmajor_kernel<1>); break;
+        case 2: launch(rms_block_kmajor_kernel<2>); break;
+        case 3: launch(rms_block_kmajor_kernel<3>); break;
+        default: launch(rms_block_kmajor_kernel<4>); break;
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess || nblk == 1) return e;
