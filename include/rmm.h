@@ -662,6 +662,41 @@ rmm_status_t rmm_decode_step(const rmm_decode_group_t *groups, int ngroups, int6
 rmm_status_t rmm_decode_products(const rmm_decode_group_t *groups, int ngroups, int64_t B,
                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The reduced products of a decode step for a batch of sequences, each
+ * weight row read once for the whole batch   (Sec. 3.2 reduced product; App.
+ * A: each sequence's set follows its own current token).
+ *
+ * For each group g and sequence b < B: Y_g[b][n] = sum over t of
+ * X_g[b][idx_g[b][t]] * W_g[idx_g[b][t]][n] -- what rmm_decode_products
+ * computes -- but instead of reading k rows of W for every sequence
+ * (B*k*N*2 bytes), the rows of the union of the B sets are streamed once and
+ * multiplied by all sequences together on the matrix cores, each sequence
+ * taking exact zeros for the rows it does not keep.  Worth it once B*r
+ * exceeds about 1 (the per-sequence reads then exceed the whole of W).
+ * Results equal rmm_decode_products' within rounding (another order of the
+ * additions), not bit for bit.  W must be finite in the union's rows: a
+ * sequence's zero times an infinite or NaN weight of a row that only other
+ * sequences keep would make its output NaN.
+ *
+ * groups   : as rmm_decode_products (idx_g read: int32 [B][k], each list
+ *            strictly ascending within [0, K); a list that is not gives
+ *            undefined values but no access outside the buffers).
+ * B        : 1..32 sequences.
+ * workspace: rmm_decode_products_shared_workspace_size(groups, ngroups, B)
+ *            bytes (never 0), 256-byte aligned.
+ * Four launches for all groups together: the range boundaries of each list,
+ * the union of every 512-index range with the activations over it, the
+ * products (fp32 partials per range), the fixed-order reduction of the
+ * ranges.
+ * Errors   : as rmm_decode_products; UNSUPPORTED also for B > 32.
+ */
+size_t rmm_decode_products_shared_workspace_size(const rmm_decode_group_t *groups, int ngroups,
+                                                 int64_t B);
+rmm_status_t rmm_decode_products_shared(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                                        void *workspace, size_t workspace_bytes,
+                                        hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);
 

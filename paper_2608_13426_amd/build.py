@@ -18,8 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "librmm.so")
 
-SOURCES = ("api.hip", "score.hip", "select.hip", "gemm.hip", "gemv.hip", "qk.hip", "attn.hip",
-           "noalloc.hip", "norm.hip", "weights.hip")
+SOURCES = ("api.hip", "score.hip", "select.hip", "gemm.hip", "gemv.hip", "gemv_shared.hip", "qk.hip",
+           "attn.hip", "noalloc.hip", "norm.hip", "weights.hip")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -620,6 +620,57 @@ rmm_status_t rmm_decode_products(const rmm_decode_group_t *groups, int ngroups, 
     return from_hip(rmm::launch_gemv_grouped_bf16(G, B, stream));
 }
 
+// The shared-rows decode products' kernel arguments (shapes validated), each
+// group's workspace carved from ws; returns the workspace bytes needed.
+static size_t share_groups(const rmm_decode_group_t *groups, int n, int64_t B, void *ws,
+                           rmm::ShareGroups *G) {
+    size_t off = 0;
+    G->n = n;
+    for (int i = 0; i < n; ++i) {
+        const rmm_decode_group_t &d = groups[i];
+        rmm::ShareGroup &q = G->g[i];
+        q = rmm::ShareGroup{};
+        q.X = static_cast<const uint16_t *>(d.X);
+        q.W = static_cast<const uint16_t *>(d.W);
+        q.idx = d.idx;
+        q.Y = static_cast<uint16_t *>(d.Y);
+        q.N = static_cast<int>(d.N);
+        q.K = static_cast<int>(d.K);
+        q.k = static_cast<int>(d.k);
+        q.ldx = d.ldx;
+        q.ldw = d.ldw;
+        q.ldy = d.ldy;
+        void *base = ws ? static_cast<void *>(static_cast<char *>(ws) + off) : nullptr;
+        off += align256(rmm::share_group_layout(B, d.N, d.K, base, &q));
+    }
+    return off;
+}
+
+static rmm_status_t check_share_groups(const rmm_decode_group_t *groups, int n, int64_t B) {
+    const rmm_status_t st = check_decode_groups(groups, n, B);
+    if (st != RMM_OK) return st;
+    return B > rmm::kShareMaxB ? RMM_ERR_UNSUPPORTED : RMM_OK;
+}
+
+size_t rmm_decode_products_shared_workspace_size(const rmm_decode_group_t *groups, int ngroups,
+                                                 int64_t B) {
+    if (check_share_groups(groups, ngroups, B) != RMM_OK) return 0;
+    rmm::ShareGroups G;
+    return share_groups(groups, ngroups, B, nullptr, &G);
+}
+
+rmm_status_t rmm_decode_products_shared(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                                        void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const rmm_status_t st = check_share_groups(groups, ngroups, B);
+    if (st != RMM_OK) return st;
+    rmm::ShareGroups G;
+    const size_t need = share_groups(groups, ngroups, B, nullptr, &G);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
+    share_groups(groups, ngroups, B, workspace, &G);
+    return from_hip(rmm::launch_share_products(G, B, stream));
+}
+
 const char *rmm_status_string(rmm_status_t status) {
     switch (status) {
     case RMM_OK: return "success";

@@ -1,0 +1,344 @@
+// Decode products of B sequences over the union of their retained sets
+// (Sec. 3.2 definition of RMM; App. A: during decoding each sequence's set
+// follows its own current token).
+//
+//   Y[b][n] = sum_{t < k} X[b][I_b[t]] * W[I_b[t]][n],   b < B <= 32
+//
+// The per-sequence product reads k rows of W for every sequence (B*k*N*2
+// bytes), more than the whole of W once B*r > 1.  Here every row that some
+// sequence keeps is read once: over the union U of the B sets,
+//
+//   Y[b][n] = sum_{j in U} xs[b][j] * W[j][n],   xs[b][j] = X[b][j] if j in
+//                                                 I_b, else 0,
+//
+// a product of a B x |U| matrix with |U| rows of W, done on the MFMA units
+// (32 sequences x 32 columns per v_mfma_f32_32x32x16_bf16).  For finite W
+// each sequence's sum has exactly the terms of its own set (the others are
+// exact zeros); the order of the additions differs from the per-sequence
+// kernel, so results agree within rounding, not bit for bit.
+//
+// The contraction axis is cut into ranges of kShareRange indices.  Four
+// launches:
+//   1. share_offsets_kernel: for every sequence and range boundary, the first
+//      position of the sequence's (ascending) list at or past it -- each list
+//      position writes the boundaries between its predecessor and itself, so
+//      every entry has one writer and no memory needs clearing;
+//   2. share_union_kernel, one workgroup per range: the members of each
+//      sequence's sub-list set bits of a per-index sequence mask in LDS
+//      (atomic OR: order-free), the indices with a nonzero mask are compacted
+//      in ascending order (a block scan), and the range's union rows and
+//      xs[b][row] (bf16, zeros past the union and for sequences that do not
+//      keep the row) go to the workspace;
+//   3. share_product_kernel, one workgroup per (range, 128-column chunk):
+//      the union rows of W stream through a four-slot LDS ring by LDS DMA
+//      (three stages of 32 rows in flight), W fragments come back with the
+//      transposing LDS read, xs fragments with 16-byte LDS reads; each range
+//      writes fp32 partials (or Y when there is one range);
+//   4. the decode step's fixed-order slice reduction adds the ranges in order.
+#include <type_traits>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace rmm {
+
+namespace {
+
+namespace sh {
+constexpr int RG = kShareRange;    // contraction indices per range
+constexpr int NT = 256;            // threads of every kernel here
+constexpr int NW = NT / 64;
+constexpr int CW = 128;            // columns per product workgroup (32 per wave)
+constexpr int RS = 32;             // union rows per stage
+constexpr int NS = 4;              // ring slots
+constexpr int DA = NS - 1;         // stages in flight ahead of the MFMAs
+constexpr int ROWB = CW * 2;       // bytes per staged W row
+constexpr int SLOT = RS * ROWB;    // bytes per ring slot
+constexpr int PER = RS / 4 / NW;   // DMA instructions per wave per stage (4 rows each)
+constexpr int XROW = RG + 8;       // bf16 per LDS row of xs (16-byte aligned, banks offset)
+static_assert(RG == 2 * NT && PER * 4 * NW == RS && (DA - 1) * PER < 16, "layout");
+}  // namespace sh
+
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt unconstrained
+template <int N>
+__device__ __forceinline__ void share_wait_vmcnt() {
+    static_assert(N >= 0 && N < 16, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+// group of workgroup `bid` in a launch whose groups start at first(g)
+template <typename F>
+__device__ __forceinline__ int share_group(const ShareGroups &G, int bid, F first) {
+    int g = 0;
+    while (g + 1 < G.n && bid >= first(G.g[g + 1])) ++g;
+    return g;
+}
+
+// 1. list positions of the range boundaries: pos[b][r] = first t with
+// I_b[t] >= r * RG (pos[b][R] = k)
+__global__ __launch_bounds__(sh::NT) void share_offsets_kernel(ShareGroups G, int B) {
+    const int bid = static_cast<int>(blockIdx.x);
+    const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_o; });
+    const ShareGroup &q = G.g[gi];
+    const int per = (q.k + sh::NT - 1) / sh::NT;     // workgroups per sequence
+    const int local = bid - q.first_o;
+    const int b = local / per;
+    const int t = (local % per) * sh::NT + static_cast<int>(threadIdx.x);
+    if (b >= B || t >= q.k) return;
+    const int32_t *I = q.idx + static_cast<int64_t>(b) * q.k;
+    int32_t *pos = q.pos + static_cast<int64_t>(b) * (q.R + 1);
+    // indices outside [0, K) are clamped (lists are required to lie within it)
+    auto range_of = [&](int32_t j) { return min(max(j, 0), q.K - 1) / sh::RG; };
+    const int hi = range_of(I[t]);
+    const int lo = t == 0 ? -1 : range_of(I[t - 1]);
+    for (int r = lo + 1; r <= hi; ++r) pos[r] = t;
+    if (t == q.k - 1)
+        for (int r = hi + 1; r <= q.R; ++r) pos[r] = q.k;
+}
+
+// 2. the union of the B sub-lists of one range, and xs over it
+__global__ __launch_bounds__(sh::NT) void share_union_kernel(ShareGroups G, int B) {
+    using namespace sh;
+    __shared__ uint32_t mask[RG];
+    __shared__ int32_t lrow[RG];
+    __shared__ uint32_t lmask[RG];
+    __shared__ int32_t wsum[NW];
+    const int bid = static_cast<int>(blockIdx.x);
+    const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_u; });
+    const ShareGroup &q = G.g[gi];
+    const int r = bid - q.first_u;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j0 = r * RG, nj = min(RG, q.K - j0);
+    for (int i = tid; i < RG; i += NT) mask[i] = 0u;
+    __syncthreads();
+    for (int b = 0; b < B; ++b) {
+        const int32_t *pos = q.pos + static_cast<int64_t>(b) * (q.R + 1);
+        // clamped, so that a list that breaks the ascending precondition
+        // still reads inside itself
+        const int t0 = min(max(pos[r], 0), q.k);
+        const int t1 = min(max(pos[r + 1], t0), q.k);
+        const int32_t *I = q.idx + static_cast<int64_t>(b) * q.k;
+        for (int t = t0 + tid; t < t1; t += NT) {
+            const int j = I[t] - j0;
+            if (j >= 0 && j < nj) atomicOr(&mask[j], 1u << b);
+        }
+    }
+    __syncthreads();
+    // ascending compaction: thread tid owns indices 2*tid and 2*tid + 1
+    const uint32_t m0 = mask[2 * tid], m1 = mask[2 * tid + 1];
+    const int c = (m0 != 0u) + (m1 != 0u);
+    int incl = c;                                  // inclusive scan within the wave
+#pragma unroll
+    for (int sft = 1; sft < 64; sft <<= 1) {
+        const int v = __shfl_up(incl, sft);
+        if (lane >= sft) incl += v;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < wave; ++w) base += wsum[w];
+    int off = base + incl - c;
+    if (m0 != 0u) { lrow[off] = j0 + 2 * tid; lmask[off] = m0; ++off; }
+    if (m1 != 0u) { lrow[off] = j0 + 2 * tid + 1; lmask[off] = m1; }
+    int u = 0;
+    for (int w = 0; w < NW; ++w) u += wsum[w];
+    __syncthreads();
+    const int up = (u + RS - 1) / RS * RS;
+    int32_t *rows = q.rows + static_cast<int64_t>(r) * RG;
+    for (int p = tid; p < u; p += NT) rows[p] = lrow[p];
+    if (tid == 0) q.cnt[r] = u;
+    // xs[r][b][p], p < up: the sequence's value where it keeps the row
+    uint16_t *xs = q.xs + static_cast<int64_t>(r) * 32 * RG;
+    for (int i = tid; i < B * up; i += NT) {
+        const int b = i / up, p = i % up;
+        uint16_t v = 0;
+        if (p < u && ((lmask[p] >> b) & 1u)) v = q.X[static_cast<int64_t>(b) * q.ldx + lrow[p]];
+        xs[b * RG + p] = v;
+    }
+}
+
+// 3. the range's product for 128 columns: Y^T tile (columns x sequences)
+__global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G, int B) {
+    using namespace sh;
+    __shared__ __attribute__((aligned(16))) uint16_t xl[32 * XROW];
+    __shared__ int32_t rl[RG];
+    // one LDS object per ring slot: the compiler then sees that reading one
+    // slot cannot alias the loads still landing in the others
+    __shared__ __attribute__((aligned(1024))) char sl0[SLOT], sl1[SLOT], sl2[SLOT], sl3[SLOT];
+    static_assert(NS == 4, "four slots");
+    auto slot_at = [&](auto I) -> char * {
+        constexpr int i = decltype(I)::value;
+        if constexpr (i == 0) return sl0;
+        else if constexpr (i == 1) return sl1;
+        else if constexpr (i == 2) return sl2;
+        else return sl3;
+    };
+    const int bid = static_cast<int>(blockIdx.x);
+    const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_p; });
+    const ShareGroup &q = G.g[gi];
+    const int local = bid - q.first_p;
+    const int r = local / q.chunks, chunk = local % q.chunks;
+    const int n0 = chunk * CW;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int u = min(max(q.cnt[r], 0), RG);      // written by the union kernel
+    const int up = (u + RS - 1) / RS * RS;
+    const int nst = up / RS;
+
+    // the range's union rows and xs (sequences past B: zeros)
+    for (int p = tid; p < up; p += NT) rl[p] = p < u ? q.rows[static_cast<int64_t>(r) * RG + p] : 0;
+    const uint16_t *xs = q.xs + static_cast<int64_t>(r) * 32 * RG;
+    const int cpr = up / 8;                        // 16-byte chunks per xs row
+    for (int i = tid; i < 32 * cpr; i += NT) {
+        const int b = i / cpr, ch = i % cpr;
+        const uint4 v = b < B ? *reinterpret_cast<const uint4 *>(xs + b * RG + 8 * ch) : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4 *>(&xl[b * XROW + 8 * ch]) = v;
+    }
+    __syncthreads();
+
+    // W rows from column n0 on; columns past N read padding or the next row
+    // (never stored), rows past the matrix's end read zeros
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(q.W + n0), 0,
+        static_cast<uint32_t>((static_cast<int64_t>(q.K) * q.ldw - n0) * 2), 0x00020000);
+    const uint32_t wrow = static_cast<uint32_t>(q.ldw) * 2u;
+    constexpr uint32_t kOut = 0x80000000u;
+    // DMA role: instruction e of the wave stages rows 8*wave + 4*e + lane/16
+    // of a stage; lane fills chunk position lane % 16 of its row with source
+    // chunk (lane % 16) ^ 4*(row % 4)  (row % 4 = lane / 16)
+    const int drow = lane >> 4;
+    const uint32_t dcol = static_cast<uint32_t>((lane & 15) ^ (4 * drow)) * 16u;
+    auto dma = [&](char *slot, int st) {
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            const int row = 8 * wave + 4 * e;
+            const int p = st * RS + row + drow;
+            const uint32_t off = p < u ? static_cast<uint32_t>(rl[p]) * wrow + dcol : kOut;
+            lds_load16(wr, slot + row * ROWB, off);
+        }
+    };
+    // Fragment role (transposing read): 16-lane group g reads rows
+    // 8*(g/2) + s/4 (+4) of a 16-row step, columns 16*(g%2) + 4*(s%4) .. +3 of
+    // the wave's 32-column block, whose chunks sit at position ^ 4*(row % 4)
+    const int g16 = lane >> 4, s16 = lane & 15;
+    const int f4 = (s16 >> 2) & 3;
+    const int col_off = (2 * (g16 & 1) + ((s16 & 3) >> 1)) * 16 + 8 * (s16 & 1);
+    const int woff = (8 * (g16 >> 1) + (s16 >> 2)) * ROWB + col_off + 64 * (wave ^ f4);
+    // xs fragment: sequence lane % 32, rows 8*(lane/32) .. +7 of the step
+    const int xoff = (lane & 31) * XROW + 8 * (lane >> 5);
+
+    f32x16_t acc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    // every step issues one stage of loads (past the last stage: out of
+    // range, zeros into a slot nobody reads), so the wait is a fixed count
+    dma(sl0, 0);
+    dma(sl1, 1);
+    dma(sl2, 2);
+    share_wait_vmcnt<(DA - 1) * PER>();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_barrier" ::: "memory");
+    // stage st lives in slot st % 4; step st refills the slot read in step st - 1
+    auto step = [&](auto I, int st) {
+        constexpr int sl = decltype(I)::value;
+        dma(slot_at(std::integral_constant<int, (sl + DA) % NS>{}), st + DA);
+        const char *slot = slot_at(I);
+#pragma unroll
+        for (int ks = 0; ks < RS / 16; ++ks) {
+            const char *wb = slot + woff + ks * 16 * ROWB;
+            const s16x4_t lo = lds_read_tr16(wb);
+            const s16x4_t hi = lds_read_tr16(wb + 4 * ROWB);
+            const bf16x8_t wf = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t *>(&xl[xoff + st * RS + ks * 16]);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xf, acc, 0, 0, 0);
+        }
+        share_wait_vmcnt<(DA - 1) * PER>();        // stage st + 1 landed
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_barrier" ::: "memory");
+    };
+    int st = 0;
+    for (; st + NS <= nst; st += NS) {
+        step(I0{}, st);
+        step(I1{}, st + 1);
+        step(I2{}, st + 2);
+        step(I3{}, st + 3);
+    }
+    if (st < nst) step(I0{}, st);
+    if (st + 1 < nst) step(I1{}, st + 1);
+    if (st + 2 < nst) step(I2{}, st + 2);
+    share_wait_vmcnt<0>();                          // the trailing out-of-range loads
+
+    // acc[4*gq + i]: column n0 + 32*wave + 8*gq + 4*(lane/32) + i, sequence lane % 32
+    const int b = lane & 31;
+    if (b >= B) return;
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int n = n0 + 32 * wave + 8 * gq + 4 * (lane >> 5) + i;
+            if (n >= q.N) continue;
+            if (q.R == 1)
+                q.Y[static_cast<int64_t>(b) * q.ldy + n] = f32_to_bf16(acc[4 * gq + i]);
+            else
+                q.P[(static_cast<int64_t>(b) * q.R + r) * q.N + n] = acc[4 * gq + i];
+        }
+}
+
+}  // namespace
+
+size_t share_group_layout(int64_t B, int64_t N, int64_t K, void *ws, ShareGroup *q) {
+    auto a256 = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+    const int64_t R = (K + kShareRange - 1) / kShareRange;
+    const size_t pos = a256(static_cast<size_t>(B * (R + 1)) * 4);
+    const size_t rows = a256(static_cast<size_t>(R * kShareRange) * 4);
+    const size_t cnt = a256(static_cast<size_t>(R) * 4);
+    const size_t xs = a256(static_cast<size_t>(R * 32 * kShareRange) * 2);
+    const size_t part = R > 1 ? a256(static_cast<size_t>(B * R * N) * 4) : 0;
+    // addresses formed as integers: ws may be null when only the size is asked
+    const uintptr_t p = reinterpret_cast<uintptr_t>(ws);
+    q->pos = reinterpret_cast<int32_t *>(p);
+    q->rows = reinterpret_cast<int32_t *>(p + pos);
+    q->cnt = reinterpret_cast<int32_t *>(p + pos + rows);
+    q->xs = reinterpret_cast<uint16_t *>(p + pos + rows + cnt);
+    q->P = R > 1 ? reinterpret_cast<float *>(p + pos + rows + cnt + xs) : nullptr;
+    q->R = static_cast<int>(R);
+    q->chunks = static_cast<int>((N + sh::CW - 1) / sh::CW);
+    return pos + rows + cnt + xs + part;
+}
+
+hipError_t launch_share_products(ShareGroups G, int64_t B, hipStream_t stream) {
+    int o = 0, un = 0, pr = 0;
+    GemvGroups Gr;
+    Gr.n = G.n;
+    for (int i = 0; i < G.n; ++i) {
+        ShareGroup &q = G.g[i];
+        q.first_o = o;
+        o += static_cast<int>(B) * ((q.k + sh::NT - 1) / sh::NT);
+        q.first_u = un;
+        un += q.R;
+        q.first_p = pr;
+        pr += q.R * q.chunks;
+        GemvGroup &s = Gr.g[i];
+        s = GemvGroup{};
+        s.P = q.P;
+        s.Y = q.Y;
+        s.N = q.N;
+        s.S = q.R;
+        s.ldy = q.ldy;
+    }
+    const int Bi = static_cast<int>(B);
+    hipLaunchKernelGGL(share_offsets_kernel, dim3(static_cast<unsigned>(o)), dim3(sh::NT), 0, stream, G, Bi);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(share_union_kernel, dim3(static_cast<unsigned>(un)), dim3(sh::NT), 0, stream, G, Bi);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(share_product_kernel, dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0, stream, G, Bi);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_gemv_reduce_grouped(Gr, B, stream);
+}
+
+}  // namespace rmm

@@ -551,6 +551,45 @@ def test_decode_step_validation(entry):
     assert f(arr(), 1, 1, P, need - 1, NULL) == WS_SMALL
 
 
+def test_decode_products_shared_validation():
+    """The shared-rows products validate their groups as the other decode
+    entry points do, take at most 32 sequences, and always need workspace."""
+    G = rmm.DecodeGroup
+    f = rmm.lib.rmm_decode_products_shared
+    size = rmm.lib.rmm_decode_products_shared_workspace_size
+
+    def arr(**kw):
+        d = dict(X=0x100000, W=0x100000, idx=0x100000, Y=0x100000, K=4096, N=1024, k=2048,
+                 ldx=4096, ldw=1024, ldy=1024)
+        d.update(kw)
+        return (G * 1)(G(**d))
+
+    assert f(None, 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(), 0, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(), 1, 0, NULL, 0, NULL) == INVALID
+    assert f(arr(Y=None), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(k=4097), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(ldy=1000), 1, 1, NULL, 0, NULL) == INVALID
+    assert f(arr(W=0x100008), 1, 1, NULL, 0, NULL) == UNSUPPORTED
+    assert f(arr(ldw=1028, N=1028, ldy=1028), 1, 1, NULL, 0, NULL) == UNSUPPORTED
+    assert f(arr(), 1, 33, NULL, 0, NULL) == UNSUPPORTED
+    assert size(arr(), 1, 33) == 0
+    nine = (G * 9)(*[arr()[0]] * 9)
+    assert f(nine, 9, 1, NULL, 0, NULL) == UNSUPPORTED
+    # 8 ranges of 512 indices: boundaries, union rows, counts, activations
+    # and the fp32 partials of every range, each 256-byte aligned
+    B, R, N = 16, 8, 1024
+    a256 = lambda x: (x + 255) // 256 * 256
+    want = (a256(B * (R + 1) * 4) + a256(R * 512 * 4) + a256(R * 4) + a256(R * 32 * 512 * 2)
+            + a256(B * R * N * 4))
+    need = size(arr(), 1, B)
+    assert need == want
+    assert size(arr(K=512, ldx=512, k=100), 1, B) > 0      # one range: no partials, still lists
+    assert f(arr(), 1, B, NULL, 0, NULL) == WS_SMALL
+    assert f(arr(), 1, B, P, need - 1, NULL) == WS_SMALL
+    assert f(arr(), 1, B, ctypes.c_void_p(0x100010), need, NULL) == INVALID   # misaligned
+
+
 def test_reduced_qk_rowstats_validation():
     f = rmm.lib.rmm_reduced_qk_rowstats
     # Q, Kc, idx, batch, H, Hkv, Lq, Lk, D, k, scale, causal, S, row_max, row_rinv, stream
