@@ -23,18 +23,20 @@
 //      position of the sequence's (ascending) list at or past it -- each list
 //      position writes the boundaries between its predecessor and itself, so
 //      every entry has one writer and no memory needs clearing;
-//   2. share_union_kernel, one workgroup per range: the members of each
+//   2. share_union_kernel, one workgroup per range: the sequences'
+//      activations over the range are staged in LDS, the members of each
 //      sequence's sub-list set bits of a per-index sequence mask in LDS
 //      (atomic OR: order-free), the indices with a nonzero mask are compacted
 //      in ascending order (a block scan), and the range's union rows and
 //      xs[b][row] (bf16, zeros past the union and for sequences that do not
 //      keep the row) go to the workspace;
 //   3. share_product_kernel, one workgroup per (range, 128-column chunk):
-//      the union rows of W stream through a four-slot LDS ring by LDS DMA
-//      (three stages of 32 rows in flight), W fragments come back with the
-//      transposing LDS read, xs fragments with 16-byte LDS reads; each range
-//      writes fp32 partials (or Y when there is one range);
-//   4. the decode step's fixed-order slice reduction adds the ranges in order.
+//      the union rows of W stream through a six-slot LDS ring by LDS DMA
+//      (five stages of 32 rows in flight), W fragments come back with the
+//      transposing LDS read, xs fragments are loaded into registers with
+//      their stage; each range writes fp32 partials (or Y when there is one
+//      range);
+//   4. share_reduce_kernel adds the ranges' partials in range order.
 #include <type_traits>
 
 #include "device_common.h"
@@ -50,20 +52,20 @@ constexpr int NT = 256;            // threads of every kernel here
 constexpr int NW = NT / 64;
 constexpr int CW = 128;            // columns per product workgroup (32 per wave)
 constexpr int RS = 32;             // union rows per stage
-constexpr int NS = 4;              // ring slots
+constexpr int NS = 6;              // ring slots
 constexpr int DA = NS - 1;         // stages in flight ahead of the MFMAs
 constexpr int ROWB = CW * 2;       // bytes per staged W row
 constexpr int SLOT = RS * ROWB;    // bytes per ring slot
 constexpr int PER = RS / 4 / NW;   // DMA instructions per wave per stage (4 rows each)
-constexpr int XROW = RG + 8;       // bf16 per LDS row of xs (16-byte aligned, banks offset)
-static_assert(RG == 2 * NT && PER * 4 * NW == RS && (DA - 1) * PER < 16, "layout");
+constexpr int LPS = PER + RS / 16; // vector loads per wave per stage (DMA + xs fragments)
+static_assert(RG <= 1024 && PER * 4 * NW == RS && (DA - 1) * LPS < 64, "layout");
 }  // namespace sh
 
 // s_waitcnt vmcnt(N) with expcnt and lgkmcnt unconstrained
 template <int N>
 __device__ __forceinline__ void share_wait_vmcnt() {
-    static_assert(N >= 0 && N < 16, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
 // group of workgroup `bid` in a launch whose groups start at first(g)
@@ -96,37 +98,91 @@ __global__ __launch_bounds__(sh::NT) void share_offsets_kernel(ShareGroups G, in
         for (int r = hi + 1; r <= q.R; ++r) pos[r] = q.k;
 }
 
-// 2. the union of the B sub-lists of one range, and xs over it
-__global__ __launch_bounds__(sh::NT) void share_union_kernel(ShareGroups G, int B) {
+// 2. the union of the B sub-lists of one range, and xs over it (1024
+// threads: the work of one range is a few dependent LDS passes)
+constexpr int kUnionThreads = 1024;
+__global__ __launch_bounds__(kUnionThreads) void share_union_kernel(ShareGroups G, int B) {
     using namespace sh;
+    constexpr int UT = kUnionThreads, UW = UT / 64;
     __shared__ uint32_t mask[RG];
     __shared__ int32_t lrow[RG];
     __shared__ uint32_t lmask[RG];
-    __shared__ int32_t wsum[NW];
+    __shared__ int32_t wsum[UW];
+    __shared__ int32_t seg[kShareMaxB + 1];       // prefix sums of the sub-list lengths
+    __shared__ int32_t beg[kShareMaxB];           // first list position of each sub-list
+    __shared__ __attribute__((aligned(16))) uint16_t xr[kShareMaxB * RG];   // X over the range
     const int bid = static_cast<int>(blockIdx.x);
     const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_u; });
     const ShareGroup &q = G.g[gi];
     const int r = bid - q.first_u;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j0 = r * RG, nj = min(RG, q.K - j0);
-    for (int i = tid; i < RG; i += NT) mask[i] = 0u;
-    __syncthreads();
-    for (int b = 0; b < B; ++b) {
-        const int32_t *pos = q.pos + static_cast<int64_t>(b) * (q.R + 1);
-        // clamped, so that a list that breaks the ascending precondition
-        // still reads inside itself
-        const int t0 = min(max(pos[r], 0), q.k);
-        const int t1 = min(max(pos[r + 1], t0), q.k);
-        const int32_t *I = q.idx + static_cast<int64_t>(b) * q.k;
-        for (int t = t0 + tid; t < t1; t += NT) {
-            const int j = I[t] - j0;
-            if (j >= 0 && j < nj) atomicOr(&mask[j], 1u << b);
+    for (int i = tid; i < RG; i += UT) mask[i] = 0u;
+    // the sub-lists of the range (clamped, so that a list that breaks the
+    // ascending precondition still reads inside itself) and their offsets
+    if (wave == 0) {
+        int len = 0;
+        if (lane < B) {
+            const int32_t *pos = q.pos + static_cast<int64_t>(lane) * (q.R + 1);
+            const int t0 = min(max(pos[r], 0), q.k);
+            const int t1 = min(max(pos[r + 1], t0), q.k);
+            beg[lane] = t0;
+            len = t1 - t0;
+        }
+        int incl = len;
+#pragma unroll
+        for (int sft = 1; sft < 32; sft <<= 1) {
+            const int v = __shfl_up(incl, sft);
+            if (lane >= sft) incl += v;
+        }
+        if (lane < B) seg[lane + 1] = incl;
+        if (lane == 0) seg[0] = 0;
+    }
+    // each sequence's activations over the range, 16 bytes at a time (X rows
+    // are 16-byte aligned and j0 is a multiple of 8); past K: zeros, never kept
+    const int cpr = RG / 8;
+    for (int i = tid; i < B * cpr; i += UT) {
+        const int b = i / cpr, c = i % cpr;
+        const uint16_t *x = q.X + static_cast<int64_t>(b) * q.ldx + j0 + 8 * c;
+        uint16_t *d = &xr[b * RG + 8 * c];
+        if (8 * c + 8 <= nj) {
+            *reinterpret_cast<uint4 *>(d) = *reinterpret_cast<const uint4 *>(x);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) d[e] = 8 * c + e < nj ? x[e] : 0;
         }
     }
     __syncthreads();
-    // ascending compaction: thread tid owns indices 2*tid and 2*tid + 1
-    const uint32_t m0 = mask[2 * tid], m1 = mask[2 * tid + 1];
-    const int c = (m0 != 0u) + (m1 != 0u);
+    // every entry of every sub-list sets its sequence's bit (atomic OR:
+    // order-free); entries are numbered across the sub-lists, four loads in
+    // flight per thread
+    const int E = seg[B];
+    for (int e0 = tid; e0 < E; e0 += 4 * UT) {
+        int jj[4];
+        uint32_t bit[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * UT;
+            jj[u] = -1;
+            bit[u] = 0u;
+            if (e < E) {
+                int lo = 0, hi = B - 1;                // the sub-list holding entry e
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (seg[mid] <= e) lo = mid; else hi = mid - 1;
+                }
+                jj[u] = q.idx[static_cast<int64_t>(lo) * q.k + beg[lo] + (e - seg[lo])] - j0;
+                bit[u] = 1u << lo;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (jj[u] >= 0 && jj[u] < nj) atomicOr(&mask[jj[u]], bit[u]);
+    }
+    __syncthreads();
+    // ascending compaction: thread tid < RG owns index tid
+    const uint32_t m = tid < RG ? mask[tid] : 0u;
+    const int c = m != 0u;
     int incl = c;                                  // inclusive scan within the wave
 #pragma unroll
     for (int sft = 1; sft < 64; sft <<= 1) {
@@ -137,41 +193,48 @@ __global__ __launch_bounds__(sh::NT) void share_union_kernel(ShareGroups G, int 
     __syncthreads();
     int base = 0;
     for (int w = 0; w < wave; ++w) base += wsum[w];
-    int off = base + incl - c;
-    if (m0 != 0u) { lrow[off] = j0 + 2 * tid; lmask[off] = m0; ++off; }
-    if (m1 != 0u) { lrow[off] = j0 + 2 * tid + 1; lmask[off] = m1; }
+    if (c) {
+        lrow[base + incl - 1] = j0 + tid;
+        lmask[base + incl - 1] = m;
+    }
     int u = 0;
-    for (int w = 0; w < NW; ++w) u += wsum[w];
+    for (int w = 0; w < UW; ++w) u += wsum[w];
     __syncthreads();
     const int up = (u + RS - 1) / RS * RS;
     int32_t *rows = q.rows + static_cast<int64_t>(r) * RG;
-    for (int p = tid; p < u; p += NT) rows[p] = lrow[p];
+    for (int p = tid; p < u; p += UT) rows[p] = lrow[p];
     if (tid == 0) q.cnt[r] = u;
-    // xs[r][b][p], p < up: the sequence's value where it keeps the row
+    // xs[r][b][p], p < up: the sequence's value where it keeps the row, two
+    // rows per thread and store
     uint16_t *xs = q.xs + static_cast<int64_t>(r) * 32 * RG;
-    for (int i = tid; i < B * up; i += NT) {
-        const int b = i / up, p = i % up;
-        uint16_t v = 0;
-        if (p < u && ((lmask[p] >> b) & 1u)) v = q.X[static_cast<int64_t>(b) * q.ldx + lrow[p]];
-        xs[b * RG + p] = v;
+    const int hp = up / 2;
+    for (int i = tid; i < B * hp; i += UT) {
+        const int b = i / hp, p = 2 * (i % hp);
+        uint32_t v = 0;
+        if (p < u && ((lmask[p] >> b) & 1u)) v = xr[b * RG + lrow[p] - j0];
+        if (p + 1 < u && ((lmask[p + 1] >> b) & 1u))
+            v |= static_cast<uint32_t>(xr[b * RG + lrow[p + 1] - j0]) << 16;
+        *reinterpret_cast<uint32_t *>(&xs[b * RG + p]) = v;
     }
 }
 
 // 3. the range's product for 128 columns: Y^T tile (columns x sequences)
-__global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G, int B) {
+__global__ __launch_bounds__(sh::NT, 3) void share_product_kernel(ShareGroups G, int B) {
     using namespace sh;
-    __shared__ __attribute__((aligned(16))) uint16_t xl[32 * XROW];
     __shared__ int32_t rl[RG];
     // one LDS object per ring slot: the compiler then sees that reading one
     // slot cannot alias the loads still landing in the others
-    __shared__ __attribute__((aligned(1024))) char sl0[SLOT], sl1[SLOT], sl2[SLOT], sl3[SLOT];
-    static_assert(NS == 4, "four slots");
+    __shared__ __attribute__((aligned(1024))) char sl0[SLOT], sl1[SLOT], sl2[SLOT], sl3[SLOT], sl4[SLOT],
+        sl5[SLOT];
+    static_assert(NS == 6, "six slots");
     auto slot_at = [&](auto I) -> char * {
         constexpr int i = decltype(I)::value;
         if constexpr (i == 0) return sl0;
         else if constexpr (i == 1) return sl1;
         else if constexpr (i == 2) return sl2;
-        else return sl3;
+        else if constexpr (i == 3) return sl3;
+        else if constexpr (i == 4) return sl4;
+        else return sl5;
     };
     const int bid = static_cast<int>(blockIdx.x);
     const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_p; });
@@ -184,16 +247,7 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
     const int u = min(max(q.cnt[r], 0), RG);      // written by the union kernel
     const int up = (u + RS - 1) / RS * RS;
     const int nst = up / RS;
-
-    // the range's union rows and xs (sequences past B: zeros)
     for (int p = tid; p < up; p += NT) rl[p] = p < u ? q.rows[static_cast<int64_t>(r) * RG + p] : 0;
-    const uint16_t *xs = q.xs + static_cast<int64_t>(r) * 32 * RG;
-    const int cpr = up / 8;                        // 16-byte chunks per xs row
-    for (int i = tid; i < 32 * cpr; i += NT) {
-        const int b = i / cpr, ch = i % cpr;
-        const uint4 v = b < B ? *reinterpret_cast<const uint4 *>(xs + b * RG + 8 * ch) : make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4 *>(&xl[b * XROW + 8 * ch]) = v;
-    }
     __syncthreads();
 
     // W rows from column n0 on; columns past N read padding or the next row
@@ -201,6 +255,10 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
     const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t *>(q.W + n0), 0,
         static_cast<uint32_t>((static_cast<int64_t>(q.K) * q.ldw - n0) * 2), 0x00020000);
+    // the range's xs rows (sequences past B are never read)
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(q.xs + static_cast<int64_t>(r) * 32 * RG), 0,
+        static_cast<uint32_t>(32 * RG * 2), 0x00020000);
     const uint32_t wrow = static_cast<uint32_t>(q.ldw) * 2u;
     constexpr uint32_t kOut = 0x80000000u;
     // DMA role: instruction e of the wave stages rows 8*wave + 4*e + lane/16
@@ -217,6 +275,18 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
             lds_load16(wr, slot + row * ROWB, off);
         }
     };
+    // xs fragment of a 16-row step (the MFMA's second operand): sequence
+    // lane % 32, rows 8*(lane/32) .. +7, loaded into registers with the stage
+    const int xb = lane & 31;
+    const uint32_t xoff = static_cast<uint32_t>(xb * RG + 8 * (lane >> 5)) * 2u;
+    bf16x8_t xq[NS][RS / 16];
+    auto xload = [&](bf16x8_t (&d)[RS / 16], int st) {
+#pragma unroll
+        for (int ks = 0; ks < RS / 16; ++ks) {
+            const uint32_t off = xb < B && st < nst ? xoff + static_cast<uint32_t>(st * RS + ks * 16) * 2u : kOut;
+            d[ks] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+        }
+    };
     // Fragment role (transposing read): 16-lane group g reads rows
     // 8*(g/2) + s/4 (+4) of a 16-row step, columns 16*(g%2) + 4*(s%4) .. +3 of
     // the wave's 32-column block, whose chunks sit at position ^ 4*(row % 4)
@@ -224,8 +294,6 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
     const int f4 = (s16 >> 2) & 3;
     const int col_off = (2 * (g16 & 1) + ((s16 & 3) >> 1)) * 16 + 8 * (s16 & 1);
     const int woff = (8 * (g16 >> 1) + (s16 >> 2)) * ROWB + col_off + 64 * (wave ^ f4);
-    // xs fragment: sequence lane % 32, rows 8*(lane/32) .. +7 of the step
-    const int xoff = (lane & 31) * XROW + 8 * (lane >> 5);
 
     f32x16_t acc;
 #pragma unroll
@@ -234,18 +302,24 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
     using I3 = std::integral_constant<int, 3>;
+    using I4 = std::integral_constant<int, 4>;
+    using I5 = std::integral_constant<int, 5>;
     // every step issues one stage of loads (past the last stage: out of
-    // range, zeros into a slot nobody reads), so the wait is a fixed count
-    dma(sl0, 0);
-    dma(sl1, 1);
-    dma(sl2, 2);
-    share_wait_vmcnt<(DA - 1) * PER>();
+    // range, zeros into a slot or registers nobody reads), so the wait is a
+    // fixed count
+    dma(sl0, 0); xload(xq[0], 0);
+    dma(sl1, 1); xload(xq[1], 1);
+    dma(sl2, 2); xload(xq[2], 2);
+    dma(sl3, 3); xload(xq[3], 3);
+    dma(sl4, 4); xload(xq[4], 4);
+    share_wait_vmcnt<(DA - 1) * LPS>();
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_barrier" ::: "memory");
-    // stage st lives in slot st % 4; step st refills the slot read in step st - 1
+    // stage st lives in slot st % NS; step st refills the slot read in step st - 1
     auto step = [&](auto I, int st) {
-        constexpr int sl = decltype(I)::value;
-        dma(slot_at(std::integral_constant<int, (sl + DA) % NS>{}), st + DA);
+        constexpr int sl = decltype(I)::value, nx = (sl + DA) % NS;
+        dma(slot_at(std::integral_constant<int, nx>{}), st + DA);
+        xload(xq[nx], st + DA);
         const char *slot = slot_at(I);
 #pragma unroll
         for (int ks = 0; ks < RS / 16; ++ks) {
@@ -253,10 +327,9 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
             const s16x4_t lo = lds_read_tr16(wb);
             const s16x4_t hi = lds_read_tr16(wb + 4 * ROWB);
             const bf16x8_t wf = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t *>(&xl[xoff + st * RS + ks * 16]);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xf, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xq[sl][ks], acc, 0, 0, 0);
         }
-        share_wait_vmcnt<(DA - 1) * PER>();        // stage st + 1 landed
+        share_wait_vmcnt<(DA - 1) * LPS>();       // stage st + 1 landed
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_barrier" ::: "memory");
     };
@@ -266,10 +339,14 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
         step(I1{}, st + 1);
         step(I2{}, st + 2);
         step(I3{}, st + 3);
+        step(I4{}, st + 4);
+        step(I5{}, st + 5);
     }
     if (st < nst) step(I0{}, st);
     if (st + 1 < nst) step(I1{}, st + 1);
     if (st + 2 < nst) step(I2{}, st + 2);
+    if (st + 3 < nst) step(I3{}, st + 3);
+    if (st + 4 < nst) step(I4{}, st + 4);
     share_wait_vmcnt<0>();                          // the trailing out-of-range loads
 
     // acc[4*gq + i]: column n0 + 32*wave + 8*gq + 4*(lane/32) + i, sequence lane % 32
@@ -286,6 +363,42 @@ __global__ __launch_bounds__(sh::NT, 2) void share_product_kernel(ShareGroups G,
             else
                 q.P[(static_cast<int64_t>(b) * q.R + r) * q.N + n] = acc[4 * gq + i];
         }
+}
+
+// 4. Y[b][n] = the ranges' partials P[b][r][n] added in range order; a
+// thread takes four consecutive columns of one sequence
+__global__ __launch_bounds__(sh::NT) void share_reduce_kernel(ShareGroups G, int B) {
+    const int bid = static_cast<int>(blockIdx.x);
+    const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_r; });
+    const ShareGroup &q = G.g[gi];
+    const int n4 = (q.N + 3) / 4;
+    const int i = (bid - q.first_r) * sh::NT + static_cast<int>(threadIdx.x);
+    if (q.R < 2 || i >= B * n4) return;
+    const int b = i / n4, n = 4 * (i % n4);
+    const float *p = q.P + static_cast<int64_t>(b) * q.R * q.N + n;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    if (q.N % 4 == 0) {
+        int r = 0;
+        for (; r + 8 <= q.R; r += 8) {
+            float4 v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = *reinterpret_cast<const float4 *>(p + static_cast<int64_t>(r + e) * q.N);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { s[0] += v[e].x; s[1] += v[e].y; s[2] += v[e].z; s[3] += v[e].w; }
+        }
+        for (; r < q.R; ++r) {
+            const float4 v = *reinterpret_cast<const float4 *>(p + static_cast<int64_t>(r) * q.N);
+            s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+        }
+    } else {
+        for (int r = 0; r < q.R; ++r)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (n + e < q.N) s[e] += p[static_cast<int64_t>(r) * q.N + e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (n + e < q.N) q.Y[static_cast<int64_t>(b) * q.ldy + n + e] = f32_to_bf16(s[e]);
 }
 
 }  // namespace
@@ -311,9 +424,7 @@ size_t share_group_layout(int64_t B, int64_t N, int64_t K, void *ws, ShareGroup 
 }
 
 hipError_t launch_share_products(ShareGroups G, int64_t B, hipStream_t stream) {
-    int o = 0, un = 0, pr = 0;
-    GemvGroups Gr;
-    Gr.n = G.n;
+    int o = 0, un = 0, pr = 0, rd = 0;
     for (int i = 0; i < G.n; ++i) {
         ShareGroup &q = G.g[i];
         q.first_o = o;
@@ -322,23 +433,20 @@ hipError_t launch_share_products(ShareGroups G, int64_t B, hipStream_t stream) {
         un += q.R;
         q.first_p = pr;
         pr += q.R * q.chunks;
-        GemvGroup &s = Gr.g[i];
-        s = GemvGroup{};
-        s.P = q.P;
-        s.Y = q.Y;
-        s.N = q.N;
-        s.S = q.R;
-        s.ldy = q.ldy;
+        q.first_r = rd;
+        if (q.R > 1) rd += (static_cast<int>(B) * ((q.N + 3) / 4) + sh::NT - 1) / sh::NT;
     }
     const int Bi = static_cast<int>(B);
     hipLaunchKernelGGL(share_offsets_kernel, dim3(static_cast<unsigned>(o)), dim3(sh::NT), 0, stream, G, Bi);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(share_union_kernel, dim3(static_cast<unsigned>(un)), dim3(sh::NT), 0, stream, G, Bi);
+    hipLaunchKernelGGL(share_union_kernel, dim3(static_cast<unsigned>(un)), dim3(kUnionThreads), 0, stream,
+                       G, Bi);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(share_product_kernel, dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0, stream, G, Bi);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    return launch_gemv_reduce_grouped(Gr, B, stream);
+    if ((e = hipGetLastError()) != hipSuccess || rd == 0) return e;
+    hipLaunchKernelGGL(share_reduce_kernel, dim3(static_cast<unsigned>(rd)), dim3(sh::NT), 0, stream, G, Bi);
+    return hipGetLastError();
 }
 
 }  // namespace rmm

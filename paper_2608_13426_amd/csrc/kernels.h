@@ -163,7 +163,7 @@ struct ShareGroup {
     float *P;               // [B][R][N] fp32 partials when R > 1
     int N, K, k, R, chunks;
     int64_t ldx, ldw, ldy;
-    int first_o, first_u, first_p;
+    int first_o, first_u, first_p, first_r;
 };
 struct ShareGroups {
     ShareGroup g[kMaxGemvGroups];
