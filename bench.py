@@ -134,6 +134,9 @@ def parse():
                    help="skip the separate timing of the fused attention block")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the separate timing of the decode step")
+    p.add_argument("--no-decode-batched", action="store_true",
+                   help="skip the decode products for batches of sequences (per-sequence, "
+                        "shared rows, dense)")
     p.add_argument("--no-attention-chain", action="store_true",
                    help="skip the timing of the attention -> o-projection chain")
     p.add_argument("--no-mlp-chain", action="store_true",
@@ -159,6 +162,72 @@ def parse():
 
 
 # ---------------------------------------------------------------- inputs
+
+def time_decode_batched(L, r, B, steps, warmup):
+    """The products of one decode step for B sequences (the first B tokens of
+    each input stand in for their current tokens; each sequence's own TopK
+    set, made once outside the timed region): rmm_decode_products (each
+    sequence reads its own k rows) against rmm_decode_products_shared (each
+    row of the union of the B sets read once), and torch's dense product of
+    the same B tokens, each as a replayed graph of R back-to-back calls.
+    Algorithmic bytes of the shared products: the union rows of every W,
+    the tokens and the outputs."""
+    import torch
+    import paper_2608_13426_amd as rmm
+    wk = L.wk
+    groups, dense = [], []
+    union_bytes = 0
+    for name in L.groups:
+        K = wk.inputs[name][0]
+        k = rmm.rmm_retained_count(ratio_of(r, name), K)
+        X = L.X[name][:B].contiguous()
+        W = L.Wcat[name]
+        N = W.shape[1]
+        idx = torch.empty(B * k, dtype=torch.int32, device=L.dev)
+        rmm.rmm_select_tokens(X.view(B, 1, K), k, idx)
+        groups.append((X, W, k, idx, torch.empty((B, N), dtype=torch.bfloat16, device=L.dev)))
+        dense.append((X, W, torch.empty((B, N), dtype=torch.bfloat16, device=L.dev)))
+        u = int(np.unique(idx.cpu().numpy()).size)
+        union_bytes += u * N * 2 + B * (K + N) * 2 + 4 * B * k
+    ws_seq = torch.empty(max(rmm.rmm_decode_step_workspace_size(groups), 1), dtype=torch.uint8,
+                         device=L.dev)
+    ws_sh = torch.empty(rmm.rmm_decode_products_shared_workspace_size(groups), dtype=torch.uint8,
+                        device=L.dev)
+
+    def graph_us(fn, R=10):
+        def many():
+            for _ in range(R):
+                fn()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            many()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            many()
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(steps):
+            g.replay()
+        end.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) * 1e3 / (steps * R)
+
+    def dense_fn():
+        for X, W, Y in dense:
+            torch.matmul(X, W, out=Y)
+    seq_us = graph_us(lambda: rmm.rmm_decode_products(groups, workspace=ws_seq))
+    sh_us = graph_us(lambda: rmm.rmm_decode_products_shared(groups, workspace=ws_sh))
+    d_us = graph_us(dense_fn)
+    return {"r": r, "batch": B, "per_sequence_us": seq_us, "shared_us": sh_us, "dense_torch_us": d_us,
+            "shared_speedup_vs_per_sequence": seq_us / sh_us, "shared_speedup_vs_dense_torch": d_us / sh_us,
+            "union_bytes": union_bytes, "shared_gbs": union_bytes / (sh_us * 1e-6) / 1e9}
+
 
 class Layer:
     """Device-resident inputs, weights and outputs of one decoder layer."""
@@ -1316,6 +1385,31 @@ def main():
             "roofline": {"bound": "hbm", "kernel": "gemv_partial_grouped_kernel (+ gemv_reduce_grouped_kernel)",
                          "achieved": round(d_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(d_ach / PEAK_HBM_GBS, 4), "traffic": None},
+        }
+    if not args.no_decode_batched:
+        recs = [time_decode_batched(L, r, B, args.steps, args.warmup)
+                for B in (4, 16, 32) for r in (0.25, 0.5, 1.0)]
+        for rec in recs:
+            print(f"# decode products B={rec['batch']} r={rec['r']}: shared {rec['shared_us']:.1f} us "
+                  f"({rec['shared_gbs']:.0f} GB/s), per sequence {rec['per_sequence_us']:.1f} us, "
+                  f"dense torch {rec['dense_torch_us']:.1f} us", file=sys.stderr, flush=True)
+        head = next(x for x in recs if x["batch"] == 16 and x["r"] == HEADLINE_R)
+        out["decode_batched"] = {
+            "op": "the products of one decode step for B sequences (q|k|v, o, gate|up, down; each "
+                  "sequence its own TopK set): rmm_decode_products reads k rows per sequence, "
+                  "rmm_decode_products_shared reads each row of the union of the B sets once and "
+                  "multiplies all sequences on the matrix cores; torch's dense product of the same "
+                  "tokens; each a replayed graph of 10 back-to-back calls",
+            "kernels": ["share_offsets_kernel", "share_union_kernel",
+                        "share_product_kernel<128, 6>", "share_reduce_kernel"],
+            "per_batch_ratio": {f"B{x['batch']}@{x['r']}": {k: (round(v, 3) if isinstance(v, float) else v)
+                                                           for k, v in x.items()} for x in recs},
+            "roofline": {"bound": "hbm", "kernel": "rmm_decode_products_shared (all four kernels), B=16 "
+                                                   f"r={HEADLINE_R}",
+                         "achieved": round(head["shared_gbs"], 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(head["shared_gbs"] / PEAK_HBM_GBS, 4),
+                         "bytes_basis": "the union rows of every W once + the tokens and outputs",
+                         "traffic": None},
         }
     if not (args.no_pv_chain and args.no_pv):
         # the value-product records take the layer's causal scores at the

@@ -38,6 +38,7 @@
 //      range);
 //   4. share_reduce_kernel adds the ranges' partials in range order.
 #include <type_traits>
+#include <utility>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -50,15 +51,9 @@ namespace sh {
 constexpr int RG = kShareRange;    // contraction indices per range
 constexpr int NT = 256;            // threads of every kernel here
 constexpr int NW = NT / 64;
-constexpr int CW = 128;            // columns per product workgroup (32 per wave)
 constexpr int RS = 32;             // union rows per stage
-constexpr int NS = 6;              // ring slots
-constexpr int DA = NS - 1;         // stages in flight ahead of the MFMAs
-constexpr int ROWB = CW * 2;       // bytes per staged W row
-constexpr int SLOT = RS * ROWB;    // bytes per ring slot
-constexpr int PER = RS / 4 / NW;   // DMA instructions per wave per stage (4 rows each)
-constexpr int LPS = PER + RS / 16; // vector loads per wave per stage (DMA + xs fragments)
-static_assert(RG <= 1024 && PER * 4 * NW == RS && (DA - 1) * LPS < 64, "layout");
+constexpr int CW = 128;            // columns per product workgroup
+constexpr int NS = 6;              // ring slots of the product kernel
 }  // namespace sh
 
 // s_waitcnt vmcnt(N) with expcnt and lgkmcnt unconstrained
@@ -218,15 +213,34 @@ __global__ __launch_bounds__(kUnionThreads) void share_union_kernel(ShareGroups 
     }
 }
 
-// 3. the range's product for 128 columns: Y^T tile (columns x sequences)
-__global__ __launch_bounds__(sh::NT, 3) void share_product_kernel(ShareGroups G, int B) {
+// 3. the range's product for CW_ columns: Y^T tile (columns x sequences).
+// The four waves take CW_/128 blocks of 32 columns each; the ring has NS_
+// slots of 32 staged rows (NS_ - 1 stages in flight).
+template <int N, typename F, int... I>
+__device__ __forceinline__ void share_steps(F &&f, int st, int nst, std::integer_sequence<int, I...>) {
+    static_assert(sizeof...(I) == N, "steps");
+    ((st + I < nst ? f(std::integral_constant<int, I>{}, st + I) : void()), ...);
+}
+
+template <int CW_, int NS_>
+__global__ __launch_bounds__(sh::NT, (160 * 1024) / (NS_ * sh::RS * CW_ * 2 + 4 * sh::RG + 1024))
+void share_product_kernel(ShareGroups G, int B) {
     using namespace sh;
+    constexpr int ROWB = CW_ * 2;              // bytes per staged W row
+    constexpr int SLOT = RS * ROWB;            // bytes per ring slot
+    constexpr int RPI = 1024 / ROWB;           // rows one wave instruction stages
+    constexpr int LPR = ROWB / 16;             // lanes per staged row
+    constexpr int PER = RS / RPI / NW;         // DMA instructions per wave per stage
+    constexpr int NB = CW_ / 32 / NW;          // 32-column blocks per wave
+    constexpr int DA = NS_ - 1;                // stages in flight ahead of the MFMAs
+    constexpr int LPS = PER + RS / 16;         // vector loads per wave per stage (DMA + xs)
+    static_assert(NB >= 1 && PER >= 1 && NS_ >= 3 && NS_ <= 8 && (DA - 1) * LPS < 64, "layout");
     __shared__ int32_t rl[RG];
     // one LDS object per ring slot: the compiler then sees that reading one
     // slot cannot alias the loads still landing in the others
-    __shared__ __attribute__((aligned(1024))) char sl0[SLOT], sl1[SLOT], sl2[SLOT], sl3[SLOT], sl4[SLOT],
-        sl5[SLOT];
-    static_assert(NS == 6, "six slots");
+    __shared__ __attribute__((aligned(1024))) char sl0[SLOT], sl1[SLOT], sl2[SLOT];
+    __shared__ __attribute__((aligned(1024))) char sl3[NS_ > 3 ? SLOT : 16], sl4[NS_ > 4 ? SLOT : 16],
+        sl5[NS_ > 5 ? SLOT : 16], sl6[NS_ > 6 ? SLOT : 16], sl7[NS_ > 7 ? SLOT : 16];
     auto slot_at = [&](auto I) -> char * {
         constexpr int i = decltype(I)::value;
         if constexpr (i == 0) return sl0;
@@ -234,14 +248,16 @@ __global__ __launch_bounds__(sh::NT, 3) void share_product_kernel(ShareGroups G,
         else if constexpr (i == 2) return sl2;
         else if constexpr (i == 3) return sl3;
         else if constexpr (i == 4) return sl4;
-        else return sl5;
+        else if constexpr (i == 5) return sl5;
+        else if constexpr (i == 6) return sl6;
+        else return sl7;
     };
     const int bid = static_cast<int>(blockIdx.x);
     const int gi = share_group(G, bid, [](const ShareGroup &q) { return q.first_p; });
     const ShareGroup &q = G.g[gi];
     const int local = bid - q.first_p;
     const int r = local / q.chunks, chunk = local % q.chunks;
-    const int n0 = chunk * CW;
+    const int n0 = chunk * CW_;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int u = min(max(q.cnt[r], 0), RG);      // written by the union kernel
@@ -261,17 +277,18 @@ __global__ __launch_bounds__(sh::NT, 3) void share_product_kernel(ShareGroups G,
         static_cast<uint32_t>(32 * RG * 2), 0x00020000);
     const uint32_t wrow = static_cast<uint32_t>(q.ldw) * 2u;
     constexpr uint32_t kOut = 0x80000000u;
-    // DMA role: instruction e of the wave stages rows 8*wave + 4*e + lane/16
-    // of a stage; lane fills chunk position lane % 16 of its row with source
-    // chunk (lane % 16) ^ 4*(row % 4)  (row % 4 = lane / 16)
-    const int drow = lane >> 4;
-    const uint32_t dcol = static_cast<uint32_t>((lane & 15) ^ (4 * drow)) * 16u;
+    // DMA role: instruction e of the wave stages rows RPI*(PER*wave + e) +
+    // lane/LPR of a stage; the lane fills chunk position lane % LPR of its row
+    // with source chunk (lane % LPR) ^ 4*(row % 4)
+    const int drow = lane / LPR, dpos = lane % LPR;
     auto dma = [&](char *slot, int st) {
 #pragma unroll
         for (int e = 0; e < PER; ++e) {
-            const int row = 8 * wave + 4 * e;
-            const int p = st * RS + row + drow;
-            const uint32_t off = p < u ? static_cast<uint32_t>(rl[p]) * wrow + dcol : kOut;
+            const int row = RPI * (PER * wave + e);
+            const int rr = row + drow;
+            const int p = st * RS + rr;
+            const uint32_t col = static_cast<uint32_t>(dpos ^ (4 * (rr & 3))) * 16u;
+            const uint32_t off = p < u ? static_cast<uint32_t>(rl[p]) * wrow + col : kOut;
             lds_load16(wr, slot + row * ROWB, off);
         }
     };
@@ -279,7 +296,7 @@ __global__ __launch_bounds__(sh::NT, 3) void share_product_kernel(ShareGroups G,
     // lane % 32, rows 8*(lane/32) .. +7, loaded into registers with the stage
     const int xb = lane & 31;
     const uint32_t xoff = static_cast<uint32_t>(xb * RG + 8 * (lane >> 5)) * 2u;
-    bf16x8_t xq[NS][RS / 16];
+    bf16x8_t xq[NS_][RS / 16];
     auto xload = [&](bf16x8_t (&d)[RS / 16], int st) {
 #pragma unroll
         for (int ks = 0; ks < RS / 16; ++ks) {
@@ -289,80 +306,77 @@ __global__ __launch_bounds__(sh::NT, 3) void share_product_kernel(ShareGroups G,
     };
     // Fragment role (transposing read): 16-lane group g reads rows
     // 8*(g/2) + s/4 (+4) of a 16-row step, columns 16*(g%2) + 4*(s%4) .. +3 of
-    // the wave's 32-column block, whose chunks sit at position ^ 4*(row % 4)
+    // a 32-column block, whose 16-byte chunks sit at position ^ 4*(row % 4)
     const int g16 = lane >> 4, s16 = lane & 15;
     const int f4 = (s16 >> 2) & 3;
     const int col_off = (2 * (g16 & 1) + ((s16 & 3) >> 1)) * 16 + 8 * (s16 & 1);
-    const int woff = (8 * (g16 >> 1) + (s16 >> 2)) * ROWB + col_off + 64 * (wave ^ f4);
-
-    f32x16_t acc;
+    const int lane_off = (8 * (g16 >> 1) + (s16 >> 2)) * ROWB + col_off;
+    int woff[NB];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using I3 = std::integral_constant<int, 3>;
-    using I4 = std::integral_constant<int, 4>;
-    using I5 = std::integral_constant<int, 5>;
+    for (int j = 0; j < NB; ++j) {
+        const int qb = wave * NB + j;
+        woff[j] = lane_off + 64 * ((qb & ~3) + ((qb & 3) ^ f4));
+    }
+
+    f32x16_t acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
     // every step issues one stage of loads (past the last stage: out of
     // range, zeros into a slot or registers nobody reads), so the wait is a
     // fixed count
-    dma(sl0, 0); xload(xq[0], 0);
-    dma(sl1, 1); xload(xq[1], 1);
-    dma(sl2, 2); xload(xq[2], 2);
-    dma(sl3, 3); xload(xq[3], 3);
-    dma(sl4, 4); xload(xq[4], 4);
+    auto issue = [&](auto I, int st) {
+        dma(slot_at(I), st);
+        xload(xq[decltype(I)::value], st);
+    };
+    share_steps<DA>([&](auto I, int st) { issue(I, st); }, 0, DA, std::make_integer_sequence<int, DA>{});
     share_wait_vmcnt<(DA - 1) * LPS>();
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_barrier" ::: "memory");
-    // stage st lives in slot st % NS; step st refills the slot read in step st - 1
+    // stage st lives in slot st % NS_; step st refills the slot read in step st - 1
     auto step = [&](auto I, int st) {
-        constexpr int sl = decltype(I)::value, nx = (sl + DA) % NS;
-        dma(slot_at(std::integral_constant<int, nx>{}), st + DA);
-        xload(xq[nx], st + DA);
+        constexpr int sl = decltype(I)::value, nx = (sl + DA) % NS_;
+        issue(std::integral_constant<int, nx>{}, st + DA);
         const char *slot = slot_at(I);
 #pragma unroll
         for (int ks = 0; ks < RS / 16; ++ks) {
-            const char *wb = slot + woff + ks * 16 * ROWB;
-            const s16x4_t lo = lds_read_tr16(wb);
-            const s16x4_t hi = lds_read_tr16(wb + 4 * ROWB);
-            const bf16x8_t wf = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xq[sl][ks], acc, 0, 0, 0);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const char *wb = slot + woff[j] + ks * 16 * ROWB;
+                const s16x4_t lo = lds_read_tr16(wb);
+                const s16x4_t hi = lds_read_tr16(wb + 4 * ROWB);
+                const bf16x8_t wf =
+                    __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xq[sl][ks], acc[j], 0, 0, 0);
+            }
         }
         share_wait_vmcnt<(DA - 1) * LPS>();       // stage st + 1 landed
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_barrier" ::: "memory");
     };
     int st = 0;
-    for (; st + NS <= nst; st += NS) {
-        step(I0{}, st);
-        step(I1{}, st + 1);
-        step(I2{}, st + 2);
-        step(I3{}, st + 3);
-        step(I4{}, st + 4);
-        step(I5{}, st + 5);
-    }
-    if (st < nst) step(I0{}, st);
-    if (st + 1 < nst) step(I1{}, st + 1);
-    if (st + 2 < nst) step(I2{}, st + 2);
-    if (st + 3 < nst) step(I3{}, st + 3);
-    if (st + 4 < nst) step(I4{}, st + 4);
+    for (; st + NS_ <= nst; st += NS_) share_steps<NS_>(step, st, nst, std::make_integer_sequence<int, NS_>{});
+    share_steps<NS_ - 1>(step, st, nst, std::make_integer_sequence<int, NS_ - 1>{});
     share_wait_vmcnt<0>();                          // the trailing out-of-range loads
 
-    // acc[4*gq + i]: column n0 + 32*wave + 8*gq + 4*(lane/32) + i, sequence lane % 32
+    // acc[j][4*gq + i]: column n0 + 32*(wave*NB + j) + 8*gq + 4*(lane/32) + i,
+    // sequence lane % 32
     const int b = lane & 31;
     if (b >= B) return;
 #pragma unroll
-    for (int gq = 0; gq < 4; ++gq)
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int n = n0 + 32 * wave + 8 * gq + 4 * (lane >> 5) + i;
-            if (n >= q.N) continue;
-            if (q.R == 1)
-                q.Y[static_cast<int64_t>(b) * q.ldy + n] = f32_to_bf16(acc[4 * gq + i]);
-            else
-                q.P[(static_cast<int64_t>(b) * q.R + r) * q.N + n] = acc[4 * gq + i];
-        }
+        for (int gq = 0; gq < 4; ++gq)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = n0 + 32 * (wave * NB + j) + 8 * gq + 4 * (lane >> 5) + i;
+                if (n >= q.N) continue;
+                if (q.R == 1)
+                    q.Y[static_cast<int64_t>(b) * q.ldy + n] = f32_to_bf16(acc[j][4 * gq + i]);
+                else
+                    q.P[(static_cast<int64_t>(b) * q.R + r) * q.N + n] = acc[j][4 * gq + i];
+            }
 }
 
 // 4. Y[b][n] = the ranges' partials P[b][r][n] added in range order; a
@@ -443,7 +457,8 @@ hipError_t launch_share_products(ShareGroups G, int64_t B, hipStream_t stream) {
     hipLaunchKernelGGL(share_union_kernel, dim3(static_cast<unsigned>(un)), dim3(kUnionThreads), 0, stream,
                        G, Bi);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(share_product_kernel, dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0, stream, G, Bi);
+    hipLaunchKernelGGL((share_product_kernel<sh::CW, sh::NS>), dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0,
+                       stream, G, Bi);
     if ((e = hipGetLastError()) != hipSuccess || rd == 0) return e;
     hipLaunchKernelGGL(share_reduce_kernel, dim3(static_cast<unsigned>(rd)), dim3(sh::NT), 0, stream, G, Bi);
     return hipGetLastError();

@@ -18,7 +18,8 @@ def test_help_lists_the_options():
     assert p.returncode == 0
     for opt in ("--gpus", "--steps", "--warmup", "--ratios", "--no-cpu-baseline",
                 "--no-fused-attention", "--no-decode", "--copy-probe-mib", "--no-policies",
-                "--no-attention-chain", "--no-mlp-chain", "--no-pv", "--no-paper-kernels", "--no-layer-forward", "--workload"):
+                "--no-attention-chain", "--no-mlp-chain", "--no-pv", "--no-paper-kernels",
+                "--no-layer-forward", "--no-decode-batched", "--workload"):
         assert opt in p.stdout
 
 
