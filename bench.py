@@ -1401,7 +1401,7 @@ def main():
                   "multiplies all sequences on the matrix cores; torch's dense product of the same "
                   "tokens; each a replayed graph of 10 back-to-back calls",
             "kernels": ["share_offsets_kernel", "share_union_kernel",
-                        "share_product_kernel<128, 6>", "share_reduce_kernel"],
+                        "share_product_kernel<128, 6> (B < 8), <256, 4> (B >= 8)", "share_reduce_kernel"],
             "per_batch_ratio": {f"B{x['batch']}@{x['r']}": {k: (round(v, 3) if isinstance(v, float) else v)
                                                            for k, v in x.items()} for x in recs},
             "roofline": {"bound": "hbm", "kernel": "rmm_decode_products_shared (all four kernels), B=16 "

@@ -30,9 +30,10 @@
 //      in ascending order (a block scan), and the range's union rows and
 //      xs[b][row] (bf16, zeros past the union and for sequences that do not
 //      keep the row) go to the workspace;
-//   3. share_product_kernel, one workgroup per (range, 128-column chunk):
-//      the union rows of W stream through a six-slot LDS ring by LDS DMA
-//      (five stages of 32 rows in flight), W fragments come back with the
+//   3. share_product_kernel, one workgroup per (range, column chunk: 128
+//      columns below eight sequences, 256 from eight on): the union rows of
+//      W stream through an LDS ring by LDS DMA (six slots of 32 rows, or
+//      four of the wider rows), W fragments come back with the
 //      transposing LDS read, xs fragments are loaded into registers with
 //      their stage; each range writes fp32 partials (or Y when there is one
 //      range);
@@ -52,9 +53,13 @@ constexpr int RG = kShareRange;    // contraction indices per range
 constexpr int NT = 256;            // threads of every kernel here
 constexpr int NW = NT / 64;
 constexpr int RS = 32;             // union rows per stage
-constexpr int CW = 128;            // columns per product workgroup
-constexpr int NS = 6;              // ring slots of the product kernel
 }  // namespace sh
+
+// Product tile by batch size: 128 columns and six ring slots for fewer than
+// eight sequences (small unions: more, shorter workgroups), 256 columns
+// (512-byte staged rows) and four slots from eight on.
+constexpr int kShareWideB = 8;
+inline int share_cols(int64_t B) { return B >= kShareWideB ? 256 : 128; }
 
 // s_waitcnt vmcnt(N) with expcnt and lgkmcnt unconstrained
 template <int N>
@@ -433,7 +438,7 @@ size_t share_group_layout(int64_t B, int64_t N, int64_t K, void *ws, ShareGroup 
     q->xs = reinterpret_cast<uint16_t *>(p + pos + rows + cnt);
     q->P = R > 1 ? reinterpret_cast<float *>(p + pos + rows + cnt + xs) : nullptr;
     q->R = static_cast<int>(R);
-    q->chunks = static_cast<int>((N + sh::CW - 1) / sh::CW);
+    q->chunks = static_cast<int>((N + share_cols(B) - 1) / share_cols(B));
     return pos + rows + cnt + xs + part;
 }
 
@@ -457,8 +462,12 @@ hipError_t launch_share_products(ShareGroups G, int64_t B, hipStream_t stream) {
     hipLaunchKernelGGL(share_union_kernel, dim3(static_cast<unsigned>(un)), dim3(kUnionThreads), 0, stream,
                        G, Bi);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((share_product_kernel<sh::CW, sh::NS>), dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0,
-                       stream, G, Bi);
+    if (share_cols(B) == 256)
+        hipLaunchKernelGGL((share_product_kernel<256, 4>), dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0,
+                           stream, G, Bi);
+    else
+        hipLaunchKernelGGL((share_product_kernel<128, 6>), dim3(static_cast<unsigned>(pr)), dim3(sh::NT), 0,
+                           stream, G, Bi);
     if ((e = hipGetLastError()) != hipSuccess || rd == 0) return e;
     hipLaunchKernelGGL(share_reduce_kernel, dim3(static_cast<unsigned>(rd)), dim3(sh::NT), 0, stream, G, Bi);
     return hipGetLastError();

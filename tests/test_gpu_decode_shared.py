@@ -47,9 +47,8 @@ def _shared_case(dev, groups_np, sets, cols=None):
     rmm.rmm_decode_products(per)
     for i, ((Xb, Wb), I, g, p) in enumerate(zip(groups_np, sets, groups, per)):
         X = wl.decode(Xb, "bf16").astype(np.float64)
-        W = wl.decode(Wb, "bf16").astype(np.float64)
-        c = np.arange(W.shape[1]) if cols is None else cols[i]
-        Wc = W[:, c]
+        c = np.arange(Wb.shape[1]) if cols is None else cols[i]
+        Wc = wl.decode(np.ascontiguousarray(Wb[:, c]), "bf16").astype(np.float64)
         Ys, Yp = from_device(g[4])[:, c], from_device(p[4])[:, c]
         for b in range(I.shape[0]):
             S = I[b]
@@ -137,13 +136,15 @@ def test_shared_products_deterministic_and_graph_replay():
             assert torch.equal(a.view(torch.int16), g[4].view(torch.int16)), rep
 
 
-@pytest.mark.parametrize("B,r", [(16, 0.5), (32, 0.25), (8, 1.0)])
-def test_layer_8b_shared_products(B, r):
-    """The 8B layer's four projection groups (q|k|v, o, gate|up, down) for B
-    sequences at full size, each sequence's own TopK set; 512 sampled output
-    columns of every group checked."""
+@pytest.mark.parametrize("name,B,r", [("layer_8b", 16, 0.5), ("layer_8b", 32, 0.25), ("layer_8b", 8, 1.0),
+                                      ("layer_8b", 4, 0.5), ("layer_70b", 8, 0.5)])
+def test_layer_shared_products(name, B, r):
+    """A layer's four projection groups (q|k|v, o, gate|up, down) for B
+    sequences at full size (8B: 4096 / 14336 channels; 70B: 8192 / 28672),
+    each sequence's own TopK set; 512 sampled output columns of every group
+    checked."""
     dev = require_gpu()
-    wk = wl.WORKLOADS["layer_8b"]
+    wk = wl.WORKLOADS[name]
     by = {}
     for p in wk.projections:
         by.setdefault(p.input_name, []).append(p)
@@ -153,7 +154,7 @@ def test_layer_8b_shared_products(B, r):
         Wb = np.concatenate([wl.f32_to_bf16_bits(wl.workload_weight(wk, p)) for p in projs], axis=1)
         groups.append((Xb, Wb))
         sets.append(_topk_sets(Xb, ro.retained_count(r, Xb.shape[1])))
-    print(f"layer_8b shared decode products B={B} r={r}", flush=True)
+    print(f"{name} shared decode products B={B} r={r}", flush=True)
     rng = np.random.default_rng(5)
     cols = [np.unique(np.concatenate([[0, 127, 128, Wb.shape[1] - 1],
                                       rng.choice(Wb.shape[1], 508, replace=False)]))
