@@ -697,6 +697,20 @@ rmm_status_t rmm_decode_products_shared(const rmm_decode_group_t *groups, int ng
                                         void *workspace, size_t workspace_bytes,
                                         hipStream_t stream);
 
+/*
+ * A decode step for a batch of sequences   (App. A: each sequence's set
+ * follows its own current token; Sec. 3.2 reduced product): for each group,
+ * idx_g[b] = the TopK of X_g[b]^2 as rmm_decode_step selects it (the same
+ * lists, bit for bit), then Y_g = rmm_decode_products_shared's products over
+ * them -- one selection launch for all groups (plus one per group wider than
+ * 32768 channels) and the four launches of the shared products.
+ *
+ * groups, B, workspace, errors: as rmm_decode_products_shared (the same
+ * workspace size); idx_g is written.
+ */
+rmm_status_t rmm_decode_step_shared(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *rmm_status_string(rmm_status_t status);
 

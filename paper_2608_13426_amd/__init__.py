@@ -25,7 +25,8 @@ __all__ = [
     "rmm_rmsnorm_kmajor_workspace_size", "rmm_attention_weights_kmajor",
     "rmm_attention_weights_kmajor_workspace_size", "rmm_reduced_pv_kmajor", "rmm_decode_step",
     "rmm_decode_step_workspace_size", "rmm_decode_products", "rmm_decode_products_shared",
-    "rmm_decode_products_shared_workspace_size", "DecodeGroup", "rmm_reduced_qk_rowstats",
+    "rmm_decode_products_shared_workspace_size", "rmm_decode_step_shared", "DecodeGroup",
+    "rmm_reduced_qk_rowstats",
     "rmm_attention_weights_kmajor_rowstats", "EXPORTED_SYMBOLS",
 ]
 
@@ -79,6 +80,8 @@ _SIGS = {
                                                                     ctypes.c_int, _i64]),
     "rmm_decode_products_shared": (ctypes.c_int, [ctypes.POINTER(DecodeGroup), ctypes.c_int, _i64,
                                                   _p, ctypes.c_size_t, _p]),
+    "rmm_decode_step_shared": (ctypes.c_int, [ctypes.POINTER(DecodeGroup), ctypes.c_int, _i64, _p,
+                                              ctypes.c_size_t, _p]),
     "rmm_reduced_pv_kmajor": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
                                              _i64, ctypes.c_int, _p, _p]),
     "rmm_rmsnorm_kmajor": (ctypes.c_int, [_p, _p, ctypes.c_float, _i64, _i64, _i64, _i64, _p, _i64,
@@ -826,6 +829,20 @@ def rmm_decode_products_shared(groups, workspace: torch.Tensor | None = None, st
     _check("rmm_decode_products_shared",
            lib.rmm_decode_products_shared(arr, len(groups), B, _ptr(workspace), ws_bytes,
                                           _stream(d, stream)))
+
+
+def rmm_decode_step_shared(groups, workspace: torch.Tensor | None = None, stream=None):
+    """For each group (X [B, K], W [K, N], k, idx [B*k], Y [B, N]), B <= 32:
+    idx = each token's TopK (as rmm_decode_step), Y = the shared-rows
+    products over those sets (rmm_decode_products_shared)."""
+    arr, B = _decode_groups(groups)
+    d = groups[0][0].device
+    if workspace is None:
+        need = int(lib.rmm_decode_products_shared_workspace_size(arr, len(groups), B))
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=d)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("rmm_decode_step_shared",
+           lib.rmm_decode_step_shared(arr, len(groups), B, _ptr(workspace), ws_bytes, _stream(d, stream)))
 
 
 def rmm_decode_step(groups, workspace: torch.Tensor | None = None, stream=None):

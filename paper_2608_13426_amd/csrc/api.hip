@@ -671,6 +671,22 @@ rmm_status_t rmm_decode_products_shared(const rmm_decode_group_t *groups, int ng
     return from_hip(rmm::launch_share_products(G, B, stream));
 }
 
+rmm_status_t rmm_decode_step_shared(const rmm_decode_group_t *groups, int ngroups, int64_t B,
+                                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const rmm_status_t st = check_share_groups(groups, ngroups, B);
+    if (st != RMM_OK) return st;
+    rmm::ShareGroups G;
+    const size_t need = share_groups(groups, ngroups, B, nullptr, &G);
+    if (!workspace || workspace_bytes < need) return RMM_ERR_WORKSPACE_TOO_SMALL;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return RMM_ERR_INVALID_ARGUMENT;
+    // the selection reads the tokens and writes the lists (no workspace)
+    rmm::GemvGroups S;
+    decode_groups(groups, ngroups, B, nullptr, &S);
+    if (rmm::launch_select_tokens_grouped(S, B, stream) != hipSuccess) return RMM_ERR_HIP;
+    share_groups(groups, ngroups, B, workspace, &G);
+    return from_hip(rmm::launch_share_products(G, B, stream));
+}
+
 const char *rmm_status_string(rmm_status_t status) {
     switch (status) {
     case RMM_OK: return "success";

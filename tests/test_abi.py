@@ -551,11 +551,13 @@ def test_decode_step_validation(entry):
     assert f(arr(), 1, 1, P, need - 1, NULL) == WS_SMALL
 
 
-def test_decode_products_shared_validation():
-    """The shared-rows products validate their groups as the other decode
-    entry points do, take at most 32 sequences, and always need workspace."""
+@pytest.mark.parametrize("entry", ["rmm_decode_products_shared", "rmm_decode_step_shared"])
+def test_decode_products_shared_validation(entry):
+    """The shared-rows products (alone, or after the step's selection)
+    validate their groups as the other decode entry points do, take at most
+    32 sequences, and always need workspace."""
     G = rmm.DecodeGroup
-    f = rmm.lib.rmm_decode_products_shared
+    f = getattr(rmm.lib, entry)
     size = rmm.lib.rmm_decode_products_shared_workspace_size
 
     def arr(**kw):

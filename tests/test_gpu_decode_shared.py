@@ -93,6 +93,40 @@ def test_shared_products_set_structure():
         _shared_case(dev, [(Xb, Wb)], [I])
 
 
+@pytest.mark.parametrize("B,r,seed", [(4, 0.5, 90), (16, 0.25, 91), (32, 1.0, 92)])
+def test_decode_step_shared(B, r, seed):
+    """The batched step: its sets equal rmm_select_tokens' bit for bit, its
+    outputs rmm_decode_products_shared's over those sets bit for bit (and so
+    the oracle within the product bound); a group of more than 32768
+    channels takes the generic selection."""
+    dev = require_gpu()
+    shapes = [(4096, 1024), (2048, 520), (33000, 72)]
+    groups, ref = [], []
+    for i, (K, N) in enumerate(shapes):
+        Xb = wl.random_case(seed + 10 * i, (B, K), "bf16", n_outlier=max(1, K // 100))
+        Wb = wl.random_case(seed + 10 * i + 1, (K, N), "bf16", std=0.02)
+        Xd, Wd = _dev_bits(Xb, dev), _dev_bits(Wb, dev)
+        k = ro.retained_count(r, K)
+        idx = torch.full((B * k,), -1, dtype=torch.int32, device=dev)
+        groups.append((Xd, Wd, k, idx, torch.full((B, N), 9.0, dtype=torch.bfloat16, device=dev)))
+        i2 = torch.empty_like(idx)
+        rmm.rmm_select_tokens(Xd.view(B, 1, K), k, i2)
+        ref.append((Xd, Wd, k, i2, torch.full((B, N), 7.0, dtype=torch.bfloat16, device=dev)))
+    rmm.rmm_decode_step_shared(groups)
+    rmm.rmm_decode_products_shared(ref)
+    for g, q in zip(groups, ref):
+        assert torch.equal(g[3], q[3]), "sets differ from rmm_select_tokens"
+        assert torch.equal(g[4].view(torch.int16), q[4].view(torch.int16)), "outputs differ"
+    # the sets are the oracle's TopK of the exact squares; the products its
+    # reduced products within the bound
+    sets = [q[3].cpu().numpy().reshape(B, q[2]) for q in ref]
+    groups_np = [(g[0].view(torch.int16).cpu().numpy().view(np.uint16),
+                  g[1].view(torch.int16).cpu().numpy().view(np.uint16)) for g in groups]
+    for (Xb, _), I in zip(groups_np, sets):
+        assert np.array_equal(I, _topk_sets(Xb, I.shape[1]))
+    _shared_case(dev, groups_np, sets)
+
+
 def test_shared_products_deterministic_and_graph_replay():
     """Two calls give the same bits, and so does every replay of the call
     captured as a HIP graph (outputs clobbered, eager work in between)."""
