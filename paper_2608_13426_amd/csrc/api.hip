@@ -6,6 +6,7 @@
 
 #include "../../include/rmm.h"
 #include "kernels.h"
+#include "gemv_shared.h"
 
 namespace {
 

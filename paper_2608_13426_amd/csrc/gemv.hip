@@ -291,19 +291,6 @@ hipError_t launch_gemv_grouped_bf16(GemvGroups G, int64_t B, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_gemv_reduce_grouped(GemvGroups G, int64_t B, hipStream_t stream) {
-    int rblocks = 0;
-    for (int i = 0; i < G.n; ++i) {
-        GemvGroup &q = G.g[i];
-        q.rfirst = rblocks;
-        if (q.S > 1) rblocks += (q.N + 63) / 64 * static_cast<int>(B);
-    }
-    if (rblocks == 0) return hipSuccess;
-    hipLaunchKernelGGL(gemv_reduce_grouped_kernel, dim3(static_cast<unsigned>(rblocks)), dim3(256), 0,
-                       stream, G);
-    return hipGetLastError();
-}
-
 hipError_t launch_gemv_bf16(const uint16_t *X, const uint16_t *W, const int32_t *idx, int64_t B,
                             int64_t M, int64_t N, int64_t K, int64_t k, int64_t ldx, int64_t ldw,
                             uint16_t *Y, int64_t ldy, void *workspace, hipStream_t stream) {

@@ -43,6 +43,7 @@
 
 #include "device_common.h"
 #include "kernels.h"
+#include "gemv_shared.h"
 
 namespace rmm {
 

@@ -141,37 +141,6 @@ hipError_t launch_select_tokens_grouped(const GemvGroups &G, int64_t B, hipStrea
 // the groups' reduced products (one launch) and slice reductions (one launch)
 hipError_t launch_gemv_grouped_bf16(GemvGroups G, int64_t B, hipStream_t stream);
 
-// the slice reductions alone (groups with S > 1: P [B][S][N] -> Y)
-hipError_t launch_gemv_reduce_grouped(GemvGroups G, int64_t B, hipStream_t stream);
-
-// Decode products of B <= kShareMaxB sequences over the union of their sets
-// (each kept weight row read once for all of them).  The contraction axis is
-// cut into ranges of kShareRange indices; the layout function carves a
-// group's workspace (pos, rows, cnt, xs, P) from ws (which may be null when
-// only the size is wanted), sets R and chunks, and returns its bytes.
-constexpr int kShareRange = 512;
-constexpr int kShareMaxB = 32;
-struct ShareGroup {
-    const uint16_t *X;      // [B][ldx] bf16, one token per sequence
-    const uint16_t *W;      // [K][ldw] bf16, 16-byte aligned, ldw % 8 == 0
-    const int32_t *idx;     // [B][k] ascending lists
-    uint16_t *Y;            // [B][ldy] bf16
-    int32_t *pos;           // [B][R+1] list position of each range boundary
-    int32_t *rows;          // [R][kShareRange] union rows of each range
-    int32_t *cnt;           // [R] union size of each range
-    uint16_t *xs;           // [R][32][kShareRange] activations over the union rows
-    float *P;               // [B][R][N] fp32 partials when R > 1
-    int N, K, k, R, chunks;
-    int64_t ldx, ldw, ldy;
-    int first_o, first_u, first_p, first_r;
-};
-struct ShareGroups {
-    ShareGroup g[kMaxGemvGroups];
-    int n;
-};
-size_t share_group_layout(int64_t B, int64_t N, int64_t K, void *ws, ShareGroup *q);
-hipError_t launch_share_products(ShareGroups G, int64_t B, hipStream_t stream);
-
 // reduced product with M <= 8 rows per unit (decode); workspace holds the
 // per-slice fp32 partials when the retained list is split
 void gemv_slices(int64_t B, int64_t N, int64_t k, int *SR, int *S);
