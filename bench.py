@@ -86,21 +86,21 @@ def _sources(main):
 # file, the shared headers and the build script) is the one it was measured
 # with, and for the same launch mix; re-run the counters after any change.
 GEMM_TRAFFIC = {"sources": _sources("gemm.hip"),
-                "sha256": "eebd71f2a084f19113e8d51dc6e8396ea9e8cf117fe6379b7b8bdd71993cd407",
+                "sha256": "2f2c9f14c1ee2a707e502647b0ed6082ecc70473c4370aa1de688d67103f4f47",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0 grouped",
-                "bytes": round((399445.33 * 2.0 + 172204.41) * 1024)}
+                "bytes": round((399447.85 * 2.0 + 172169.57) * 1024)}
 # per fused attention call: attn_fwd_kernel (mean over the four ratios' kernels)
 # plus attn_compact_k_kernel
 ATTN_TRAFFIC = {"sources": _sources("attn.hip"),
-                "sha256": "78a06861ba1af214523ec104f18a06e59b9e766f3c38fa9fd060ee7905c1f7ac",
+                "sha256": "2ef66f0b47540990067c3d74bdff9c5089cd7921d90f6202cdc486f4c9858b0d",
                 "mix": "layer_8b r=0.25,0.5,0.75,1.0",
-                "bytes": round((103635.35 * 2.0 + 65550.76 + 8249.07 * 2.0 + 40960.00) * 1024)}
+                "bytes": round((103628.45 * 2.0 + 65550.75 + 8249.02 * 2.0 + 40960.00) * 1024)}
 # per rmm_rmsnorm_kmajor call (8192 x 4096, the same whatever r):
 # rms_block_kmajor_kernel and its score_finalize_grouped_kernel
 NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip")],
-                "sha256": "26c671468611fa6009c83e25452a99ffb9597b878b3c3fa3c974f27c2d99c0ad",
+                "sha256": "0340673358c97aa4fbe9598a3ef098cffc971f6775443e358ce25fb38375a34e",
                 "mix": "layer_8b attn_in,mlp_in",
-                "bytes": round((33033.04 * 2.0 + 74167.11 + 4115.00 * 2.0 + 32.00) * 1024)}
+                "bytes": round((33033.05 * 2.0 + 74159.67 + 4115.00 * 2.0 + 32.00) * 1024)}
 
 
 def sources_sha256(paths):
