@@ -102,6 +102,16 @@ NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip
                 "mix": "layer_8b attn_in,mlp_in",
                 "bytes": round((33033.05 * 2.0 + 74159.67 + 4115.00 * 2.0 + 32.00) * 1024)}
 
+# per rmm_decode_products_shared call at B = 16, r = 0.5 on the 8B groups:
+# its four kernels (boundaries, union pass, product, range reduction)
+SHARED_TRAFFIC = {"sources": [os.path.join(CSRC, f) for f in ("gemv_shared.hip", "gemv_shared.h",
+                                                              "kernels.h", "device_common.h")]
+                  + [BUILD_SCRIPT],
+                  "sha256": "7c312c2936bb3855686f59ad095ab0d5a6bfa8657bc397231fe60e4724f12af6",
+                  "mix": "layer_8b B=16 r=0.5",
+                  "bytes": round((483.0 * 2.0 + 24.5 + 939.6 * 2.0 + 937.6 + 217030.5 * 2.0 + 26646.8
+                                  + 13333.0 * 2.0 + 1344.1) * 1024)}
+
 
 def sources_sha256(paths):
     h = hashlib.sha256()
@@ -1409,7 +1419,8 @@ def main():
                          "achieved": round(head["shared_gbs"], 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(head["shared_gbs"] / PEAK_HBM_GBS, 4),
                          "bytes_basis": "the union rows of every W once + the tokens and outputs",
-                         "traffic": None},
+                         "traffic": recorded_traffic(SHARED_TRAFFIC, f"{wk.name} B=16 r={HEADLINE_R}"),
+                         "traffic_unit": "HBM bytes per call (FETCH_SIZE + WRITE_SIZE, all four kernels)"},
         }
     if not (args.no_pv_chain and args.no_pv):
         # the value-product records take the layer's causal scores at the
