@@ -102,6 +102,17 @@ NORM_TRAFFIC = {"sources": _sources("norm.hip") + [os.path.join(CSRC, "score.hip
                 "mix": "layer_8b attn_in,mlp_in",
                 "bytes": round((33033.05 * 2.0 + 74159.67 + 4115.00 * 2.0 + 32.00) * 1024)}
 
+# per rmm_decode_products call of the batch-1 decode step (the four 8B
+# groups; mean over the four ratios): gemv_partial_grouped_kernel and
+# gemv_reduce_grouped_kernel
+DECODE_TRAFFIC = {"sources": [os.path.join(CSRC, f) for f in ("gemv.hip", "kernels.h", "device_common.h")]
+                  + [BUILD_SCRIPT],
+                  "sha256": "40da861c585557e8e1d6f6498bd11aa8d6d194f9f5d21c30863040a4de695740",
+                  "mix": "layer_8b r=0.25,0.5,0.75,1.0 B=1",
+                  "bytes": round(((53592.86 * 2.0 + 2661.30 + 1349.0 * 2.0 + 84.0)
+                                  + (106951.50 * 2.0 + 3431.99 + 1733.0 * 2.0 + 84.0)
+                                  + (160329.72 * 2.0 + 3948.19 + 1993.0 * 2.0 + 84.0)
+                                  + (213691.84 * 2.0 + 4222.14 + 2121.0 * 2.0 + 84.0)) / 4 * 1024)}
 # per rmm_decode_products_shared call at B = 16, r = 0.5 on the 8B groups:
 # its four kernels (boundaries, union pass, product, range reduction)
 SHARED_TRAFFIC = {"sources": [os.path.join(CSRC, f) for f in ("gemv_shared.hip", "gemv_shared.h",
@@ -1394,7 +1405,11 @@ def main():
             "speedup_vs_r1": round(d_1["us_per_step"] / d_h["us_per_step"], 3) if d_1 else None,
             "roofline": {"bound": "hbm", "kernel": "gemv_partial_grouped_kernel (+ gemv_reduce_grouped_kernel)",
                          "achieved": round(d_ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                         "frac": round(d_ach / PEAK_HBM_GBS, 4), "traffic": None},
+                         "frac": round(d_ach / PEAK_HBM_GBS, 4),
+                         "traffic": recorded_traffic(
+                             DECODE_TRAFFIC, f"{wk.name} r={','.join(str(r) for r in sorted(dec))} B=1"),
+                         "traffic_unit": "HBM bytes per products call (FETCH_SIZE + WRITE_SIZE, mean "
+                                         "over the ratios)"},
         }
     if not args.no_decode_batched:
         recs = [time_decode_batched(L, r, B, args.steps, args.warmup)
