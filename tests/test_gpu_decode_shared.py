@@ -63,9 +63,10 @@ def _shared_case(dev, groups_np, sets, cols=None):
                                       (5, 0.001, 4), (7, 1.0, 5)])
 def test_shared_products_ragged_groups(B, r, seed):
     """Ragged groups: one range (K < 512), K just past a range, a ragged last
-    range and column chunk, a wide group of 40 ranges."""
+    range and column chunk, a wide group of 40 ranges, and eight channels
+    with fewer columns than one chunk."""
     dev = require_gpu()
-    shapes = [(296, 136), (520, 520), (2048, 3000), (1000, 1536), (20000, 200)]
+    shapes = [(296, 136), (520, 520), (2048, 3000), (1000, 1536), (20000, 200), (8, 24)]
     groups, sets = [], []
     for i, (K, N) in enumerate(shapes):
         Xb = wl.random_case(seed + 10 * i, (B, K), "bf16", n_outlier=max(1, K // 100))
