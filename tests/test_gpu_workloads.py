@@ -201,6 +201,12 @@ def test_layer_70b_projection(proj):
     _projection_case("layer_70b", proj, RATIOS)
 
 
+def test_layer_70b_fused_attention():
+    """The reduced attention block on the 70B layer's 64 query / 8 kv heads
+    and 16384 tokens, at the outer ratios."""
+    _fused_attention_case("layer_70b", (0.25, 1.0), n_rows=5)
+
+
 def test_layer_70b_attention():
     """Every one of the 64 heads: energies, sets, the -inf count, and
     sampled rows of S against the oracle."""
