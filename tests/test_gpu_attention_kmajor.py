@@ -132,14 +132,17 @@ def test_kmajor_is_deterministic():
     assert torch.equal(e1, e2)
 
 
-def test_layer_8b_chain():
+@pytest.mark.parametrize("name", ["layer_8b", "layer_70b"])
+def test_layer_chain(name):
     """Full size, the launch configuration the benchmark times: the 8B
-    attention shape (32 q / 8 kv heads, 8192 tokens, causal) at r = 0.5, then
-    the output projection [4096 x 4096] at r = 0.5: K-major copy equal to the
+    attention shape (32 q / 8 kv heads, 8192 tokens, causal; the 70B layer:
+    64 / 8 heads, 16384 tokens) at r = 0.5, then the output projection
+    ([4096 x 4096]; [8192 x 8192]) at r = 0.5: K-major copy equal to the
     block's output, energies exact to float64 rounding, the projection's set
     bit-exact, its output on sampled rows against the oracle."""
     dev = require_gpu()
-    wk = wl.WORKLOADS["layer_8b"]
+    wk = wl.WORKLOADS[name]
+    print(f"{name}: attention block -> output projection, r = 0.5", flush=True)
     a = wk.attention
     q, kk = wl.workload_qk(wk)
     qb, kb = wl.f32_to_bf16_bits(q), wl.f32_to_bf16_bits(kk)

@@ -183,14 +183,17 @@ def test_swiglu_is_deterministic():
     assert torch.equal(outs[0][1], outs[1][1])
 
 
-def test_layer_8b_mlp_chain():
+@pytest.mark.parametrize("name", ["layer_8b", "layer_70b"])
+def test_layer_mlp_chain(name):
     """Full size, the launch configuration the benchmark times: the 8B MLP
     input [8192 x 4096] at r = 0.5 through gate|up [4096 x 14336 each] with
-    the SwiGLU epilogue, then the down projection [14336 x 4096] at r = 0.5:
-    index sets bit-exact, H's energies exact to float64 rounding, H and the
-    down output on sampled rows against the oracle."""
+    the SwiGLU epilogue, then the down projection [14336 x 4096] at r = 0.5
+    (the 70B layer: [16384 x 8192], 8192 -> 2 x 28672 -> 8192): index sets
+    bit-exact, H's energies exact to float64 rounding, H and the down output
+    on sampled rows against the oracle."""
     dev = require_gpu()
-    wk = wl.WORKLOADS["layer_8b"]
+    wk = wl.WORKLOADS[name]
+    print(f"{name}: gate|up with the SwiGLU epilogue -> down, r = 0.5", flush=True)
     Xbits = wl.f32_to_bf16_bits(wl.workload_input(wk, "mlp_in"))
     X = wl.decode(Xbits, "bf16").astype(np.float64)[None]
     proj = {p.name: p for p in wk.projections}
