@@ -278,12 +278,16 @@ def test_decode_step_groups(B, r, seed):
     _decode_case(dev, groups, B, r)
 
 
-@pytest.mark.parametrize("B", [1, 16])
-def test_layer_8b_decode_step(B):
-    """The 8B layer's four projection groups (q|k|v, o, gate|up, down) as one
-    grouped decode step at every ratio, B sequences."""
+@pytest.mark.parametrize("name,B,ratios", [("layer_8b", 1, (0.25, 0.5, 0.75, 1.0)),
+                                           ("layer_8b", 16, (0.25, 0.5, 0.75, 1.0)),
+                                           ("layer_70b", 1, (0.5,))])
+def test_layer_decode_step(name, B, ratios):
+    """A layer's four projection groups (q|k|v, o, gate|up, down) as one
+    grouped decode step, B sequences: the 8B layer at every ratio, the 70B
+    layer (down: 28672 channels, one-pass token selection with 32 keys per
+    thread) at r = 0.5."""
     dev = require_gpu()
-    wk = wl.WORKLOADS["layer_8b"]
+    wk = wl.WORKLOADS[name]
     by = {}
     for p in wk.projections:
         by.setdefault(p.input_name, []).append(p)
@@ -292,5 +296,6 @@ def test_layer_8b_decode_step(B):
         Xb = wl.f32_to_bf16_bits(wl.workload_input(wk, name, M=B))
         Wb = np.concatenate([wl.f32_to_bf16_bits(wl.workload_weight(wk, p)) for p in projs], axis=1)
         groups.append((Xb, Wb))
-    for r in (0.25, 0.5, 0.75, 1.0):
+    print(f"{name}: decode step, B={B}, r in {ratios}", flush=True)
+    for r in ratios:
         _decode_case(dev, groups, B, r)
